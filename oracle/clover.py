@@ -1,0 +1,294 @@
+"""Clover speculator, token tree, verification and acceptance (oracle side).
+
+Test infrastructure only.  Follows Sec. 3 of the paper:
+
+* Regressive Connection (Sec. 3.1, 3.4): the embedding of a speculated token is
+  its row of the LM-head weight after normalisation; read here as row-wise L2
+  normalisation.
+* Attention Decoder (Sec. 3.2, Eq. 1-2): Q from the RMS-normalised hidden state
+  h_{i-1}, K and V from e_{i-1}; h_i = h_{i-1} + Attention(Q, K, V).  Read
+  literally, the key set is the single vector e_{i-1}, so the softmax weight is
+  exactly 1.  The attention has the base model's head layout and an output
+  projection; its weights are shared by all heads.
+* Per-head MLP (Sec. 3.2, Sec. 4.1 "Medusa initialisation"): read as the Medusa
+  residual block r = h + SiLU(W1 h + b1), one per head.
+* Shared LM head (Sec. 3.4): every head reuses the target's final norm and LM
+  head.
+* Augmenting Block (Sec. 3.3): one extra decoder layer over the residual stream
+  after the last base layer, with its own KV cache; its output at the last
+  committed position is h_0.
+* Token tree (Sec. 2.2): per-depth top-k expansion, truncation to the
+  configured number of verify tokens by cumulative log-probability, mask =
+  ancestor-or-self matrix.  The paper names no tree construction or sampling
+  algorithm (Sec. 4.1), so this one is a reading.
+* Verification and greedy acceptance (Sec. 2.1): the target's argmax at each
+  node decides which child, if any, is kept; the accepted path plus one bonus
+  token is emitted, so outputs equal plain greedy decoding.
+
+Parity unpinned: the composition AB -> AD -> MLP -> LM head beyond the
+single-key closed form (the architecture figure is not available).
+"""
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+from .model import BaseModel, LayerWeights, Precision, layer_forward, logsumexp, rmsnorm, silu
+
+
+# --------------------------------------------------------------------------------------------
+# small pure functions
+
+
+def topk_ids(logits: np.ndarray, k: int) -> np.ndarray:
+    """The k largest entries, ordered by value descending, then token id ascending."""
+    ids = np.arange(logits.shape[0])
+    order = np.lexsort((ids, -logits))
+    return order[:k]
+
+
+def rc_embed(w_lm: np.ndarray, token: int) -> np.ndarray:
+    """Regressive Connection embedding: e(t) = W_lm[t] / max(||W_lm[t]||_2, 1e-12).
+
+    Sec. 3.4: the one-hot token times the transposed, normalised LM-head weight.
+    """
+    row = w_lm[token]
+    return row / max(float(np.sqrt(np.sum(row * row))), 1e-12)
+
+
+def attention_decoder(h: np.ndarray, e_keys: np.ndarray, w: Dict[str, np.ndarray], n_heads: int,
+                      head_dim: int, eps: float, prec: Precision) -> np.ndarray:
+    """Sec. 3.2, Eq. 1-2.  h: [d] hidden state h_{i-1}; e_keys: [n_keys, d] token embeddings.
+
+    Q = W_Q RMSNorm(h); K = W_K e; V = W_V e; h_i = h + W_O Attention(Q, K, V).
+    """
+    a = prec.store(rmsnorm(h, w["ad.norm"], eps))
+    E = prec.store(np.atleast_2d(e_keys))
+    q = (a @ w["ad.wq"].T).reshape(n_heads, head_dim)
+    k = (E @ w["ad.wk"].T).reshape(-1, n_heads, head_dim)
+    v = (E @ w["ad.wv"].T).reshape(-1, n_heads, head_dim)
+    s = np.einsum("hd,khd->hk", q, k) / np.sqrt(head_dim)
+    s = s - np.max(s, axis=1, keepdims=True)
+    p = np.exp(s)
+    p = p / np.sum(p, axis=1, keepdims=True)
+    o = np.einsum("hk,khd->hd", p, v).reshape(-1)
+    return h + prec.store(o) @ w["ad.wo"].T
+
+
+def head_mlp(s: np.ndarray, w1: np.ndarray, b1: np.ndarray, prec: Precision) -> np.ndarray:
+    """Per-head residual MLP block: r = s + SiLU(W1 s + b1)."""
+    return s + silu(prec.store(s) @ w1.T + b1)
+
+
+def tree_mask(parent: Sequence[int]) -> np.ndarray:
+    """Ancestor-or-self matrix: mask[i][j] is True iff j == i or j is an ancestor of i."""
+    T = len(parent)
+    m = np.zeros((T, T), dtype=bool)
+    for i in range(T):
+        j = i
+        while j >= 0:
+            m[i, j] = True
+            j = parent[j]
+    return m
+
+
+@dataclass
+class Candidates:
+    """Draft output in creation order (index 0 is the root)."""
+    depth: np.ndarray
+    token: np.ndarray
+    parent: np.ndarray
+    lp: np.ndarray                     # float32 cumulative log-probability
+    row_logits: Dict[int, np.ndarray] = field(default_factory=dict)   # node -> head logits
+    row_state: Dict[int, np.ndarray] = field(default_factory=dict)    # node -> AD output
+
+
+@dataclass
+class Tree:
+    tokens: np.ndarray
+    parent: np.ndarray
+    depth: np.ndarray
+    pos: np.ndarray
+    mask: np.ndarray
+    src: np.ndarray                    # candidate index of each tree node
+
+
+def build_tree(depth, token, parent, lp, T: int, L: int) -> Tree:
+    """Truncate the candidate tree to T verify tokens (root included).
+
+    Non-root candidates are ranked by (lp descending, depth ascending, creation
+    index ascending) and the first T-1 kept; the root and the kept nodes are then
+    listed in creation order, which is breadth-first.  Positions are L + depth.
+    """
+    depth, token, parent = np.asarray(depth), np.asarray(token), np.asarray(parent)
+    lp = np.asarray(lp, dtype=np.float32)
+    n = len(depth)
+    idx = np.arange(1, n)
+    order = np.lexsort((idx, depth[1:], -lp[1:].astype(np.float64)))
+    kept = np.sort(idx[order[: T - 1]])
+    src = np.concatenate([[0], kept]).astype(np.int64)
+    remap = {int(s): i for i, s in enumerate(src)}
+    par = np.array([-1] + [remap[int(parent[s])] for s in kept], dtype=np.int64)
+    dep = depth[src].astype(np.int64)
+    return Tree(tokens=token[src].astype(np.int64), parent=par, depth=dep, pos=L + dep,
+                mask=tree_mask(par), src=src)
+
+
+def accept(tokens: Sequence[int], parent: Sequence[int], target: Sequence[int]):
+    """Greedy acceptance (Sec. 2.1): follow the children whose token equals the
+    target's argmax at their parent; the lowest-index matching child wins.
+
+    Returns (acc, bonus): acc lists accepted node indices starting at the root,
+    bonus is the target's argmax at the last accepted node.
+    """
+    acc = [0]
+    cur = 0
+    while True:
+        nxt = None
+        for c in range(len(tokens)):
+            if parent[c] == cur and tokens[c] == target[cur]:
+                nxt = c
+                break
+        if nxt is None:
+            break
+        acc.append(nxt)
+        cur = nxt
+    return acc, int(target[cur])
+
+
+# --------------------------------------------------------------------------------------------
+# stateful decoding
+
+
+@dataclass
+class SeqState:
+    tokens: List[int]                                  # committed tokens, positions 0..L-1
+    kv: List[Tuple[np.ndarray, np.ndarray]]           # per base layer, [L, n_kv, hd]
+    ab_kv: Tuple[np.ndarray, np.ndarray]               # Augmenting Block cache
+    h0: np.ndarray                                     # AB output at position L-1
+    t0: int                                            # next token (root of the next tree)
+
+    @property
+    def L(self) -> int:
+        return len(self.tokens)
+
+
+@dataclass
+class VerifyOut:
+    logits: np.ndarray            # [T, V]
+    target: np.ndarray            # [T] argmax, lowest id on ties
+    x_last: np.ndarray            # [T, d] residual after the last base layer
+    kv: List[Tuple[np.ndarray, np.ndarray]]   # per layer, tree-node K/V [T, n_kv, hd]
+
+
+class CloverOracle:
+    def __init__(self, cfg, weights):
+        self.cfg = cfg
+        self.w = {k: np.asarray(v.float().numpy() if hasattr(v, "float") else v, dtype=np.float64)
+                  for k, v in weights.items()}
+        self.base = BaseModel(cfg, self.w)
+        self.prec = self.base.prec
+        self.ab = LayerWeights.from_dict(self.w, "ab")
+
+    # -- Augmenting Block -------------------------------------------------------------------
+    def ab_forward(self, x_rows, pos, ab_kv, tail_visible):
+        c = self.cfg
+        return layer_forward(x_rows, np.asarray(pos), self.ab, ab_kv[0], ab_kv[1], tail_visible,
+                             c.n_heads, c.n_kv_heads, c.head_dim, c.rms_eps, c.rope_theta,
+                             self.prec)
+
+    # -- prefill (Sec. 1: the prompt is processed in one pass and yields the first token) ---
+    def prefill(self, prompt: Sequence[int]) -> SeqState:
+        n = len(prompt)
+        causal = np.tril(np.ones((n, n), dtype=bool))
+        x, kv = self.base.forward_rows(prompt, np.arange(n), None, causal)
+        t0 = int(np.argmax(self.base.logits(x[-1:])[0]))
+        h, k, v = self.ab_forward(x, np.arange(n), self.base.empty_kv(), causal)
+        return SeqState(tokens=list(prompt), kv=kv, ab_kv=(k, v), h0=h[-1].copy(), t0=t0)
+
+    # -- drafting (Sec. 3) ---------------------------------------------------------------
+    def head_logits(self, j: int, s: np.ndarray) -> np.ndarray:
+        r = head_mlp(s, self.w[f"head{j}.w1"], self.w[f"head{j}.b1"], self.prec)
+        return self.base.logits(r[None, :])[0]
+
+    def draft(self, st: SeqState) -> Candidates:
+        c = self.cfg
+        depth, token, parent = [0], [st.t0], [-1]
+        lp = [np.float32(0.0)]
+        state = {0: st.h0}
+        out = Candidates(depth=None, token=None, parent=None, lp=None)
+        for j in range(1, c.n_spec_heads + 1):
+            frontier = [i for i in range(len(depth)) if depth[i] == j - 1]
+            for n in frontier:
+                e = rc_embed(self.w["lm_head"], token[n])
+                s = attention_decoder(state[n], e, self.w, c.n_heads, c.head_dim, c.rms_eps,
+                                      self.prec)
+                logits = self.head_logits(j - 1, s)
+                logp = logits - logsumexp(logits)
+                out.row_logits[n] = logits
+                out.row_state[n] = s
+                for t in topk_ids(logits, c.topk[j - 1]):
+                    depth.append(j)
+                    token.append(int(t))
+                    parent.append(n)
+                    lp.append(np.float32(np.float32(lp[n]) + np.float32(logp[t])))
+                    state[len(depth) - 1] = s
+        out.depth = np.array(depth)
+        out.token = np.array(token)
+        out.parent = np.array(parent)
+        out.lp = np.array(lp, dtype=np.float32)
+        return out
+
+    # -- verification (Sec. 2.1, 2.2) ----------------------------------------------------
+    def verify(self, st: SeqState, tree: Tree) -> VerifyOut:
+        x, kv = self.base.forward_rows(tree.tokens, tree.pos, st.kv, tree.mask)
+        logits = self.base.logits(x)
+        return VerifyOut(logits=logits, target=np.argmax(logits, axis=1), x_last=x, kv=kv)
+
+    # -- commit: compaction of the accepted KV entries and the Augmenting Block ------------
+    def commit(self, st: SeqState, tree: Tree, ver: VerifyOut, acc: List[int], bonus: int):
+        L, A = st.L, len(acc)
+        acc = np.asarray(acc)
+        st.kv = [(np.concatenate([kp, k[acc]]), np.concatenate([vp, v[acc]]))
+                 for (kp, vp), (k, v) in zip(st.kv, ver.kv)]
+        causal = np.tril(np.ones((A, A), dtype=bool))
+        h, k, v = self.ab_forward(ver.x_last[acc], L + np.arange(A), st.ab_kv, causal)
+        st.ab_kv = (np.concatenate([st.ab_kv[0], k]), np.concatenate([st.ab_kv[1], v]))
+        st.h0 = h[-1].copy()
+        st.tokens.extend(int(t) for t in tree.tokens[acc])
+        st.t0 = bonus
+
+    def step_tree(self, st: SeqState, tree: Tree):
+        """Verify a given tree, accept, commit.  Returns (emitted, acc, verify output)."""
+        ver = self.verify(st, tree)
+        acc, bonus = accept(tree.tokens, tree.parent, ver.target)
+        emitted = [int(tree.tokens[i]) for i in acc[1:]] + [bonus]
+        self.commit(st, tree, ver, acc, bonus)
+        return emitted, acc, ver
+
+    def step(self, st: SeqState):
+        """One speculate-and-verify step.  Returns (emitted, details)."""
+        cands = self.draft(st)
+        tree = build_tree(cands.depth, cands.token, cands.parent, cands.lp,
+                          self.cfg.tree_tokens, st.L)
+        emitted, acc, ver = self.step_tree(st, tree)
+        return emitted, dict(cands=cands, tree=tree, acc=acc, ver=ver)
+
+    def planted_tree(self, st: SeqState, tokens: Sequence[int], parents: Sequence[int]) -> Tree:
+        parent = np.asarray(parents, dtype=np.int64)
+        depth = np.zeros(len(parent), dtype=np.int64)
+        for i in range(1, len(parent)):
+            depth[i] = depth[parent[i]] + 1
+        return Tree(tokens=np.asarray(tokens, dtype=np.int64), parent=parent, depth=depth,
+                    pos=st.L + depth, mask=tree_mask(parent), src=np.arange(len(parent)))
+
+    def generate(self, prompt: Sequence[int], n_new: int, max_steps: int = 10_000):
+        """Speculative greedy generation of at least n_new tokens (first token from prefill)."""
+        st = self.prefill(prompt)
+        out = [st.t0]
+        steps = 0
+        while len(out) < n_new and steps < max_steps:
+            emitted, _ = self.step(st)
+            out.extend(emitted)
+            steps += 1
+        return out[:n_new], st

@@ -1,0 +1,120 @@
+"""Pins for the oracle's base transformer against library routines and closed forms."""
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import synth
+from oracle import Precision, attention, logsumexp, rmsnorm, rope
+from oracle.model import BaseModel
+
+
+def _torch_forward_full(cfg, w, tokens):
+    """Independent float64 torch implementation: SDPA with a boolean mask, torch rms_norm,
+    complex-number rotary, F.silu."""
+    W = {k: v.double() for k, v in w.items()}
+    n, hd, H, Hk = len(tokens), cfg.head_dim, cfg.n_heads, cfg.n_kv_heads
+    x = W["emb"][torch.tensor(tokens)]
+    pos = torch.arange(n, dtype=torch.float64)
+    inv = cfg.rope_theta ** (-torch.arange(0, hd, 2, dtype=torch.float64) / hd)
+    rot = torch.polar(torch.ones(n, hd // 2, dtype=torch.float64), pos[:, None] * inv[None, :])
+
+    def apply_rot(t):  # t: [n, heads, hd]; pair (i, i+hd/2) is the complex number t_i + j t_{i+hd/2}
+        z = torch.complex(t[..., : hd // 2], t[..., hd // 2:]) * rot[:, None, :]
+        return torch.cat([z.real, z.imag], dim=-1)
+
+    mask = torch.ones(n, n, dtype=torch.bool).tril()
+    for l in range(cfg.n_layers):
+        p = f"layer{l}."
+        a = F.rms_norm(x, (cfg.d_model,), W[p + "attn_norm"], cfg.rms_eps)
+        q = apply_rot((a @ W[p + "wq"].T).view(n, H, hd)).transpose(0, 1)
+        k = apply_rot((a @ W[p + "wk"].T).view(n, Hk, hd)).transpose(0, 1)
+        v = (a @ W[p + "wv"].T).view(n, Hk, hd).transpose(0, 1)
+        k = k.repeat_interleave(H // Hk, dim=0)
+        v = v.repeat_interleave(H // Hk, dim=0)
+        o = F.scaled_dot_product_attention(q, k, v, attn_mask=mask)
+        x = x + o.transpose(0, 1).reshape(n, H * hd) @ W[p + "wo"].T
+        m = F.rms_norm(x, (cfg.d_model,), W[p + "mlp_norm"], cfg.rms_eps)
+        x = x + (F.silu(m @ W[p + "w_gate"].T) * (m @ W[p + "w_up"].T)) @ W[p + "w_down"].T
+    xf = F.rms_norm(x, (cfg.d_model,), W["final_norm"], cfg.rms_eps)
+    return (xf @ W["lm_head"].T).numpy()
+
+
+@pytest.mark.parametrize("kv_heads", [2, 1])
+def test_base_forward_matches_torch_reference(kv_heads):
+    cfg = synth.tiny_test_config(n_kv_heads=kv_heads)
+    w = synth.make_weights(cfg, seed=3, perturb=True)
+    toks = synth.make_prompt(cfg, n=20)
+    got = BaseModel(cfg, {k: v.double().numpy() for k, v in w.items()}).forward_full(toks)
+    ref = _torch_forward_full(cfg, w, toks)
+    assert np.max(np.abs(got - ref)) < 1e-10
+
+
+def test_rope_closed_forms():
+    rng = np.random.default_rng(0)
+    q = rng.standard_normal((1, 1, 64))
+    k = rng.standard_normal((1, 1, 64))
+    # position 0 is the identity
+    assert np.allclose(rope(q, np.array([0]), 1e4), q, atol=0, rtol=0)
+    # rotations preserve the norm
+    for p in (1, 7, 1000, 32767):
+        assert abs(np.linalg.norm(rope(q, np.array([p]), 1e4)) - np.linalg.norm(q)) < 1e-12
+    # <R_m q, R_n k> depends only on m - n
+    dots = [float(np.sum(rope(q, np.array([m]), 1e4) * rope(k, np.array([m - 5]), 1e4)))
+            for m in (5, 17, 300, 9000)]
+    assert np.ptp(dots) < 1e-9
+    # a single pair rotates by pos * theta^0 = pos radians
+    x = np.zeros((1, 1, 4)); x[0, 0, 0] = 1.0
+    r = rope(x, np.array([3]), 1e4)[0, 0]
+    assert np.allclose([r[0], r[2]], [np.cos(3.0), np.sin(3.0)], atol=1e-15)
+
+
+def test_rmsnorm_closed_forms():
+    rng = np.random.default_rng(1)
+    x = rng.standard_normal((5, 32)) * 3
+    y = rmsnorm(x, np.ones(32), 0.0)
+    assert np.allclose(np.sqrt(np.mean(y * y, axis=-1)), 1.0, atol=1e-14)
+    assert np.allclose(rmsnorm(7.5 * x, np.ones(32), 0.0), y, atol=1e-14)   # scale invariance
+    ref = F.rms_norm(torch.tensor(x), (32,), None, 1e-6).numpy()
+    assert np.allclose(rmsnorm(x, np.ones(32), 1e-6), ref, atol=1e-14)
+
+
+def test_attention_special_cases():
+    rng = np.random.default_rng(2)
+    q = rng.standard_normal((3, 4, 8)); k = rng.standard_normal((5, 2, 8)); v = rng.standard_normal((5, 2, 8))
+    # one visible key: the output is exactly that key's value
+    vis = np.zeros((3, 5), dtype=bool); vis[:, 2] = True
+    o = attention(q, k, v, vis)
+    assert np.array_equal(o[:, 0], np.broadcast_to(v[2, 0], (3, 8)))
+    assert np.array_equal(o[:, 3], np.broadcast_to(v[2, 1], (3, 8)))
+    # equal keys: uniform weights, output is the mean of the visible values
+    kk = np.repeat(k[:1], 5, axis=0)
+    vis = np.ones((3, 5), dtype=bool)
+    assert np.allclose(attention(q, kk, v, vis)[:, 1], v[:, 0].mean(0), atol=1e-14)
+    # against torch SDPA (GQA by repeating kv heads)
+    vis = rng.random((3, 5)) < 0.6; vis[:, 0] = True
+    tq = torch.tensor(q).transpose(0, 1)
+    tk = torch.tensor(k).repeat_interleave(2, dim=1).transpose(0, 1)
+    tv = torch.tensor(v).repeat_interleave(2, dim=1).transpose(0, 1)
+    ref = F.scaled_dot_product_attention(tq, tk, tv, attn_mask=torch.tensor(vis)).transpose(0, 1)
+    assert np.allclose(attention(q, k, v, vis), ref.numpy(), atol=1e-13)
+
+
+def test_logsumexp_and_softmax():
+    import scipy.special
+    rng = np.random.default_rng(3)
+    z = rng.standard_normal((4, 1000)) * 30
+    assert np.allclose(logsumexp(z), scipy.special.logsumexp(z, axis=-1), atol=1e-12)
+    p = np.exp(z - logsumexp(z)[:, None])
+    assert np.allclose(p.sum(1), 1.0, atol=1e-12)
+
+
+def test_bf16_rounding_matches_torch():
+    rng = np.random.default_rng(4)
+    x = np.concatenate([rng.standard_normal(10000) * 10.0 ** rng.integers(-6, 6, 10000),
+                        # exact ties between two bf16 values: round half to even
+                        np.array([1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -(1.0 + 2 ** -8)])])
+    got = Precision("bf16").store(x)
+    ref = torch.tensor(x, dtype=torch.float32).to(torch.bfloat16).double().numpy()
+    assert np.array_equal(got, ref)
+    assert np.array_equal(Precision("f32").store(x), x)
