@@ -1,0 +1,1191 @@
+// C ABI of the Clover library: configuration queries, weight packing, context
+// lifetime, prefill, the speculate-and-verify step and test hooks.
+//
+// The host side validates every call before enqueuing work, keeps the paged-KV
+// allocator and a mirror of each sequence's committed length, and orchestrates the
+// kernels of one step on the context's stream:
+//   draft  (Sec. 3): per depth j, Attention Decoder (Eq. 1-2) on the frontier, head MLP,
+//          shared LM head, top-k -> candidate tree;  truncation -> verify tree
+//   verify (Sec. 2.1, 2.2): one tree-masked forward of all layers, final norm, LM head,
+//          greedy argmax per node; the Augmenting Block (Sec. 3.3) runs as one extra
+//          layer over the tree with its own KV cache
+//   accept: longest path matching the greedy tokens, bonus token, KV compaction of every
+//          layer, h_0 for the next draft = Augmenting Block output at the last accepted node
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/clover.h"
+#include "kernels.h"
+
+using namespace clover;
+
+namespace {
+
+thread_local std::string g_err;
+
+void set_global_err(const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+}
+
+constexpr size_t ALIGN = 256;
+size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
+
+int es_of(int dtype) { return dtype == CLOVER_BF16 ? 2 : 4; }
+int kc_of(int dtype) { return dtype == CLOVER_BF16 ? 32 : 16; }
+
+// ---- canonical weights ----------------------------------------------------------------
+const char* kLayer[9] = {"attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "w_gate", "w_up", "w_down"};
+
+struct WSpec {
+  std::string name;
+  int64_t rows, cols;  // cols == 0: vector of rows elements
+  bool matrix;
+};
+
+void layer_specs(const clover_config& c, const std::string& pre, std::vector<WSpec>& out) {
+  const int64_t d = c.d_model, F = c.ffn_dim, qd = (int64_t)c.n_heads * c.head_dim,
+                kvd = (int64_t)c.n_kv_heads * c.head_dim;
+  const int64_t shp[9][2] = {{d, 0}, {qd, d}, {kvd, d}, {kvd, d}, {d, qd}, {d, 0}, {F, d}, {F, d}, {d, F}};
+  for (int i = 0; i < 9; ++i)
+    out.push_back({pre + "." + kLayer[i], shp[i][0], shp[i][1], shp[i][1] != 0});
+}
+
+std::vector<WSpec> weight_specs(const clover_config& c) {
+  std::vector<WSpec> s;
+  const int64_t d = c.d_model, V = c.vocab, qd = (int64_t)c.n_heads * c.head_dim;
+  s.push_back({"emb", V, d, false});  // gathered by rows, kept row-major
+  for (int l = 0; l < c.n_layers; ++l) layer_specs(c, "layer" + std::to_string(l), s);
+  s.push_back({"final_norm", d, 0, false});
+  s.push_back({"lm_head", V, d, true});
+  layer_specs(c, "ab", s);
+  s.push_back({"ad.norm", d, 0, false});
+  s.push_back({"ad.wq", qd, d, true});
+  s.push_back({"ad.wk", qd, d, true});
+  s.push_back({"ad.wv", qd, d, true});
+  s.push_back({"ad.wo", d, qd, true});
+  for (int j = 0; j < c.n_spec_heads; ++j) {
+    s.push_back({"head" + std::to_string(j) + ".w1", d, d, true});
+    s.push_back({"head" + std::to_string(j) + ".b1", d, 0, false});
+  }
+  return s;
+}
+
+int n_candidates(const clover_config& c) {  // root excluded
+  int total = 0, width = 1;
+  for (int j = 0; j < c.n_spec_heads; ++j) {
+    width *= c.topk[j];
+    total += width;
+  }
+  return total;
+}
+int frontier(const clover_config& c, int j) {  // rows expanded at depth j (1-based)
+  int w = 1;
+  for (int i = 0; i < j - 1; ++i) w *= c.topk[i];
+  return w;
+}
+int depth_base(const clover_config& c, int depth) {  // first candidate index of a depth
+  int base = 0, w = 1;
+  for (int i = 0; i < depth; ++i) {
+    base += w;
+    w *= c.topk[i];
+  }
+  return base;
+}
+int prefill_chunk(const clover_config& c) { return c.prefill_chunk > 0 ? c.prefill_chunk : 256; }
+
+bool check_config(const clover_config* c, std::string& why) {
+  char buf[256];
+  auto fail = [&](const char* m) { why = m; return false; };
+  if (!c) return fail("config is null");
+  if (c->dtype != CLOVER_F32 && c->dtype != CLOVER_BF16) return fail("dtype must be F32 or BF16");
+  const int kc = kc_of(c->dtype);
+  if (c->n_layers < 1 || c->n_layers > 1024) return fail("n_layers out of range");
+  if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128) return fail("head_dim must be 32, 64 or 128");
+  if (c->n_heads < 1 || c->n_kv_heads < 1 || c->n_heads % c->n_kv_heads) return fail("n_kv_heads must divide n_heads");
+  if (c->d_model < kc || c->d_model % kc || c->d_model % 16) return fail("d_model must be a multiple of 16 (fp32) or 32 (bf16)");
+  if (((int64_t)c->n_heads * c->head_dim) % kc) return fail("n_heads*head_dim must be a multiple of the K chunk");
+  if (c->ffn_dim < 16 || c->ffn_dim % 16 || c->ffn_dim % kc) return fail("ffn_dim must be a multiple of 16 (fp32) or 32 (bf16)");
+  if (c->vocab < 16 || c->vocab % 16) return fail("vocab must be a positive multiple of 16");
+  if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f)) return fail("rms_eps/rope_theta invalid");
+  if (c->n_spec_heads < 1 || c->n_spec_heads > CLOVER_MAX_HEADS) return fail("n_spec_heads must be 1..8");
+  for (int j = 0; j < c->n_spec_heads; ++j)
+    if (c->topk[j] < 1 || c->topk[j] > 16) return fail("topk entries must be 1..16");
+  if (c->tree_tokens < 1 || c->tree_tokens > 128) return fail("tree_tokens must be 1..128");
+  const int64_t nc = n_candidates(*c);
+  if (nc + 1 < c->tree_tokens) return fail("the full candidate tree has fewer nodes than tree_tokens");
+  if (nc + 1 > 1024) return fail("candidate tree larger than 1024 nodes");
+  if (c->max_batch < 1 || c->max_batch > 256) return fail("max_batch must be 1..256");
+  if (c->kv_block != 16) return fail("kv_block must be 16");
+  if (c->max_context < c->tree_tokens + 1) return fail("max_context must exceed tree_tokens");
+  if (c->prefill_chunk < 0 || c->prefill_chunk % 64) return fail("prefill_chunk must be a multiple of 64");
+  if ((int64_t)c->max_batch * frontier(*c, c->n_spec_heads) > 4096) return fail("draft frontier too large");
+  (void)buf;
+  return true;
+}
+
+// ---- workspace layout ------------------------------------------------------------------
+struct Layout {
+  int es, T, W, H, NC, Mv, Mp, Mmax, Fsum, Fmaxrows, mbps, nblocks;
+  size_t pool_bytes;
+  size_t kpool, vpool, pool_ptrs, block_table, seq_len, seq_ids;
+  size_t x, xa, xn, qbuf, obuf, act, vlogits, row_tok, row_pos, row_slot, row_seq, amax;
+  size_t h0, t0, cand_token, cand_parent, cand_depth, cand_lp;
+  size_t tree_token, tree_parent, tree_depth, tree_pos, tree_mask, target, acc, acc_len, out_tokens;
+  size_t dstate[CLOVER_MAX_HEADS], dlogits[CLOVER_MAX_HEADS];
+  size_t d_hin, d_a, d_e, d_q, d_kv, d_o, d_sst, d_r, d_rn;
+  size_t gpart, gsem, apart, asem;
+  size_t gpart_floats, gsem_n, apart_floats, asem_n;
+  size_t total;
+};
+
+void gemm_need(const clover_config& c, int M, int ntiles, int nchunks, bool swiglu, size_t& pf,
+               size_t& sems) {
+  if (M <= 0) return;
+  GemmPlan pl = plan_gemm(c.dtype, M, ntiles, nchunks, swiglu);
+  pf = std::max(pf, pl.part_floats);
+  sems = std::max(sems, (size_t)pl.ngroups * pl.mchunks);
+}
+
+Layout make_layout(const clover_config& c) {
+  Layout L{};
+  L.es = es_of(c.dtype);
+  L.T = c.tree_tokens;
+  L.W = (L.T + 63) / 64;
+  L.H = c.n_spec_heads;
+  L.NC = n_candidates(c) + 1;
+  L.Mv = c.max_batch * L.T;
+  L.Mp = prefill_chunk(c);
+  L.Mmax = std::max(L.Mv, L.Mp);
+  L.Fsum = 0;
+  L.Fmaxrows = 0;
+  for (int j = 1; j <= L.H; ++j) {
+    L.Fsum += c.max_batch * frontier(c, j);
+    L.Fmaxrows = std::max(L.Fmaxrows, c.max_batch * frontier(c, j));
+  }
+  L.mbps = (c.max_context + 15) / 16;
+  L.nblocks = c.max_batch * L.mbps;
+  const int64_t d = c.d_model, V = c.vocab, F = c.ffn_dim, hd = c.head_dim;
+  const int64_t qd = c.n_heads * hd, kvd = c.n_kv_heads * hd;
+  const int NL = c.n_layers + 1;  // base layers + Augmenting Block
+  L.pool_bytes = align_up((size_t)L.nblocks * kvd * 16 * L.es);
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + std::max<size_t>(bytes, 1)); return o; };
+  L.kpool = take(L.pool_bytes * NL);
+  L.vpool = take(L.pool_bytes * NL);
+  L.pool_ptrs = take(sizeof(void*) * 2 * NL);
+  L.block_table = take(sizeof(int) * (size_t)c.max_batch * L.mbps);
+  L.seq_len = take(sizeof(int) * c.max_batch);
+  L.seq_ids = take(sizeof(int) * c.max_batch);
+  L.x = take(4 * (size_t)L.Mmax * d);
+  L.xa = take(4 * (size_t)L.Mmax * d);
+  L.xn = take((size_t)L.es * L.Mmax * d);
+  L.qbuf = take((size_t)L.es * L.Mmax * qd);
+  L.obuf = take((size_t)L.es * L.Mmax * qd);
+  L.act = take((size_t)L.es * L.Mmax * F);
+  L.vlogits = take(4 * (size_t)L.Mv * V);
+  L.row_tok = take(4 * (size_t)L.Mmax);
+  L.row_pos = take(4 * (size_t)L.Mmax);
+  L.row_slot = take(4 * (size_t)L.Mmax);
+  L.row_seq = take(4 * (size_t)L.Mmax);
+  L.amax = take(4 * (size_t)L.Mv);
+  L.h0 = take(4 * (size_t)c.max_batch * d);
+  L.t0 = take(4 * (size_t)c.max_batch);
+  const size_t ncand = (size_t)c.max_batch * L.NC;
+  L.cand_token = take(4 * ncand);
+  L.cand_parent = take(4 * ncand);
+  L.cand_depth = take(4 * ncand);
+  L.cand_lp = take(4 * ncand);
+  const size_t nt = (size_t)c.max_batch * L.T;
+  L.tree_token = take(4 * nt);
+  L.tree_parent = take(4 * nt);
+  L.tree_depth = take(4 * nt);
+  L.tree_pos = take(4 * nt);
+  L.tree_mask = take(8 * nt * L.W);
+  L.target = take(4 * nt);
+  L.acc = take(4 * (size_t)c.max_batch * (L.H + 1));
+  L.acc_len = take(4 * (size_t)c.max_batch);
+  L.out_tokens = take(4 * (size_t)c.max_batch * (L.H + 1));
+  for (int j = 1; j <= L.H; ++j) {
+    const size_t rows = (size_t)c.max_batch * frontier(c, j);
+    L.dstate[j - 1] = take(4 * rows * d);
+    L.dlogits[j - 1] = take(4 * rows * V);
+  }
+  const size_t fr = L.Fmaxrows;
+  L.d_hin = take(4 * fr * d);
+  L.d_a = take((size_t)L.es * fr * d);
+  L.d_e = take((size_t)L.es * fr * d);
+  L.d_q = take(4 * fr * qd);
+  L.d_kv = take(4 * fr * 2 * qd);
+  L.d_o = take((size_t)L.es * fr * qd);
+  L.d_sst = take((size_t)L.es * fr * d);
+  L.d_r = take(4 * fr * d);
+  L.d_rn = take((size_t)L.es * fr * d);
+  // split-K partials: every GEMM shape the context launches
+  const int kc = kc_of(c.dtype);
+  size_t pf = 0, sems = 0;
+  for (int M : {L.Mv, L.Mp, 1}) {
+    gemm_need(c, M, (int)((qd + 2 * kvd) / 16), (int)(d / kc), false, pf, sems);
+    gemm_need(c, M, (int)(d / 16), (int)(qd / kc), false, pf, sems);
+    gemm_need(c, M, (int)(2 * F / 16), (int)(d / kc), true, pf, sems);
+    gemm_need(c, M, (int)(d / 16), (int)(F / kc), false, pf, sems);
+    gemm_need(c, M, (int)(V / 16), (int)(d / kc), false, pf, sems);
+  }
+  for (int j = 1; j <= L.H; ++j) {
+    const int M = c.max_batch * frontier(c, j);
+    for (int m = 1; m <= M; ++m) {
+      gemm_need(c, m, (int)(qd / 16), (int)(d / kc), false, pf, sems);
+      gemm_need(c, m, (int)(2 * qd / 16), (int)(d / kc), false, pf, sems);
+      gemm_need(c, m, (int)(d / 16), (int)(qd / kc), false, pf, sems);
+      gemm_need(c, m, (int)(d / 16), (int)(d / kc), false, pf, sems);
+      gemm_need(c, m, (int)(V / 16), (int)(d / kc), false, pf, sems);
+    }
+  }
+  for (int M = 1; M <= L.Mv; ++M) {  // verify with any number of active sequences
+    if (M % L.T) continue;
+    gemm_need(c, M, (int)((qd + 2 * kvd) / 16), (int)(d / kc), false, pf, sems);
+    gemm_need(c, M, (int)(d / 16), (int)(qd / kc), false, pf, sems);
+    gemm_need(c, M, (int)(2 * F / 16), (int)(d / kc), true, pf, sems);
+    gemm_need(c, M, (int)(d / 16), (int)(F / kc), false, pf, sems);
+    gemm_need(c, M, (int)(V / 16), (int)(d / kc), false, pf, sems);
+  }
+  for (int M = 1; M <= L.Mp; ++M) {  // prefill chunks of any length
+    gemm_need(c, M, (int)((qd + 2 * kvd) / 16), (int)(d / kc), false, pf, sems);
+    gemm_need(c, M, (int)(d / 16), (int)(qd / kc), false, pf, sems);
+    gemm_need(c, M, (int)(2 * F / 16), (int)(d / kc), true, pf, sems);
+    gemm_need(c, M, (int)(d / 16), (int)(F / kc), false, pf, sems);
+  }
+  L.gpart_floats = pf;
+  L.gsem_n = std::max<size_t>(sems, 1);
+  L.gpart = take(4 * pf);
+  L.gsem = take(4 * L.gsem_n);
+  // attention partials: worst case over batch sizes and prefill
+  size_t apf = 0, asn = 1;
+  auto att_need = [&](int nbatch, int nq, int max_keys) {
+    AttnParams a{};
+    a.nbatch = nbatch; a.nq = nq; a.n_heads = c.n_heads;
+    plan_attention(a, max_keys);
+    apf = std::max(apf, attention_part_floats(nbatch, a.qtiles, c.n_heads, a.splits, c.head_dim));
+    asn = std::max(asn, (size_t)nbatch * a.qtiles * c.n_heads);
+  };
+  for (int b = 1; b <= c.max_batch; ++b) att_need(b, L.T, c.max_context);
+  for (int nq = 1; nq <= L.Mp; nq += 1) att_need(1, nq, c.max_context);
+  L.apart_floats = apf;
+  L.asem_n = asn;
+  L.apart = take(4 * apf);
+  L.asem = take(4 * asn);
+  L.total = off;
+  return L;
+}
+
+}  // namespace
+
+// ---- context -----------------------------------------------------------------------------
+
+struct LayerPtrs {
+  const void *attn_norm, *wq, *wk, *wv, *wo, *mlp_norm, *wg, *wu, *wd;
+};
+
+struct clover_ctx {
+  clover_config cfg;
+  Layout L;
+  hipStream_t st;
+  char* ws;
+  std::vector<const void*> w;
+  std::vector<LayerPtrs> layers;  // n_layers + 1 (Augmenting Block last)
+  const void *emb, *final_norm, *lm_head, *ad_norm, *ad_wq, *ad_wk, *ad_wv, *ad_wo;
+  std::vector<const void*> head_w1, head_b1;
+  // host state
+  std::vector<int> seq_len;                  // -1 inactive
+  std::vector<std::vector<int>> seq_blocks;  // physical KV blocks per slot
+  std::vector<int> free_blocks;
+  std::vector<int> bt_host;
+  std::vector<int> host_ids, host_len, host_out;
+  std::string err;
+  bool dead = false;
+  hipEvent_t ev[4];
+  clover_timings tim{};
+  int last_nbatch = 0;
+
+  template <typename T> T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
+};
+
+namespace {
+
+clover_status ctx_fail(clover_ctx* c, clover_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  c->err = buf;
+  return s;
+}
+
+#define HIPCK(ctx, expr)                                                                  \
+  do {                                                                                    \
+    hipError_t e_ = (expr);                                                               \
+    if (e_ != hipSuccess) {                                                               \
+      (ctx)->dead = true;                                                                 \
+      return ctx_fail((ctx), CLOVER_ERR_DEVICE, "%s failed: %s", #expr, hipGetErrorString(e_)); \
+    }                                                                                     \
+  } while (0)
+
+int gemm_tiles(int n) { return n / 16; }
+
+// Y = X W^T through the streaming GEMM with the given epilogue.
+hipError_t run_gemm(clover_ctx* c, GemmParams p, int M, int K, std::initializer_list<std::pair<const void*, int>> segs) {
+  p.M = M;
+  p.K = K;
+  p.nchunks = K / kc_of(c->cfg.dtype);
+  p.nseg = 0;
+  p.ntiles = 0;
+  for (auto& s : segs) {
+    p.seg[p.nseg++] = GemmSeg{s.first, s.second / 16};
+    p.ntiles += s.second / 16;
+  }
+  if (p.mode != EP_SWIGLU) p.N = p.ntiles * 16;
+  p.part = c->at<float>(c->L.gpart);
+  p.sem = c->at<int>(c->L.gsem);
+  return launch_gemm(c->cfg.dtype, p, c->st);
+}
+
+// One pre-norm decoder layer over rows of c->x-like buffer `x` (in place).
+hipError_t run_layer(clover_ctx* c, const LayerPtrs& lw, int layer_idx, float* x, int M,
+                     AttnParams att, int max_keys) {
+  const clover_config& cf = c->cfg;
+  const Layout& L = c->L;
+  const int d = cf.d_model, hd = cf.head_dim, qd = cf.n_heads * hd, kvd = cf.n_kv_heads * hd;
+  void* xn = c->at<void>(L.xn);
+  void* kp = c->ws + L.kpool + L.pool_bytes * layer_idx;
+  void* vp = c->ws + L.vpool + L.pool_bytes * layer_idx;
+  hipError_t e;
+  if ((e = launch_rmsnorm(cf.dtype, x, d, M, d, lw.attn_norm, cf.rms_eps, xn, d, nullptr, c->st))) return e;
+  GemmParams g{};
+  g.X = xn; g.ldx = d; g.mode = EP_QKV;
+  g.qbuf = c->at<void>(L.qbuf); g.ldq = qd;
+  g.kcache = kp; g.vcache = vp;
+  g.row_seq = c->at<int>(L.row_seq); g.row_slot = c->at<int>(L.row_slot); g.row_pos = c->at<int>(L.row_pos);
+  g.block_table = c->at<int>(L.block_table); g.max_blocks = L.mbps;
+  g.n_heads = cf.n_heads; g.n_kv = cf.n_kv_heads; g.hd = hd; g.theta = cf.rope_theta;
+  if ((e = run_gemm(c, g, M, d, {{lw.wq, qd}, {lw.wk, kvd}, {lw.wv, kvd}}))) return e;
+  att.Q = c->at<void>(L.qbuf); att.ldq = qd;
+  att.O = c->at<void>(L.obuf); att.ldo = qd;
+  att.kcache = kp; att.vcache = vp;
+  att.block_table = c->at<int>(L.block_table); att.max_blocks = L.mbps;
+  att.n_heads = cf.n_heads; att.n_kv = cf.n_kv_heads; att.hd = hd;
+  att.part = c->at<float>(L.apart); att.sem = c->at<int>(L.asem);
+  if ((e = launch_attention(cf.dtype, att, max_keys, c->st))) return e;
+  GemmParams o{};
+  o.X = c->at<void>(L.obuf); o.ldx = qd; o.mode = EP_RESID;
+  o.resid = x; o.ldr = d; o.out_f = x; o.ldo = d;
+  if ((e = run_gemm(c, o, M, qd, {{lw.wo, d}}))) return e;
+  if ((e = launch_rmsnorm(cf.dtype, x, d, M, d, lw.mlp_norm, cf.rms_eps, xn, d, nullptr, c->st))) return e;
+  GemmParams gu{};
+  gu.X = xn; gu.ldx = d; gu.mode = EP_SWIGLU;
+  gu.out_s = c->at<void>(L.act); gu.ldos = cf.ffn_dim; gu.N = cf.ffn_dim;
+  if ((e = run_gemm(c, gu, M, d, {{lw.wg, cf.ffn_dim}, {lw.wu, cf.ffn_dim}}))) return e;
+  GemmParams dn{};
+  dn.X = c->at<void>(L.act); dn.ldx = cf.ffn_dim; dn.mode = EP_RESID;
+  dn.resid = x; dn.ldr = d; dn.out_f = x; dn.ldo = d;
+  return run_gemm(c, dn, M, cf.ffn_dim, {{lw.wd, d}});
+}
+
+clover_status ensure_blocks(clover_ctx* c, int slot, int upto) {
+  const int need = (upto + 15) / 16;
+  auto& bl = c->seq_blocks[slot];
+  if (need > c->L.mbps) return ctx_fail(c, CLOVER_ERR_CAPACITY, "sequence %d needs %d KV blocks > %d", slot, need, c->L.mbps);
+  if ((int)bl.size() >= need) return CLOVER_OK;
+  if ((int)c->free_blocks.size() < need - (int)bl.size())
+    return ctx_fail(c, CLOVER_ERR_CAPACITY, "KV pool exhausted");
+  const int first = (int)bl.size();
+  while ((int)bl.size() < need) {
+    bl.push_back(c->free_blocks.back());
+    c->free_blocks.pop_back();
+  }
+  int* row = c->bt_host.data() + (size_t)slot * c->L.mbps;
+  for (int i = first; i < need; ++i) row[i] = bl[i];
+  HIPCK(c, hipMemcpyAsync(c->at<int>(c->L.block_table) + (size_t)slot * c->L.mbps + first,
+                          row + first, sizeof(int) * (need - first), hipMemcpyHostToDevice, c->st));
+  return CLOVER_OK;
+}
+
+// verify + accept + commit for the batch in seq_ids (tree already in device buffers)
+clover_status verify_accept(clover_ctx* c, int B, int* out_tokens, int* out_count, int max_keys) {
+  const clover_config& cf = c->cfg;
+  const Layout& L = c->L;
+  const int T = L.T, M = B * T, d = cf.d_model, H = L.H;
+  float* x = c->at<float>(L.x);
+  float* xa = c->at<float>(L.xa);
+  HIPCK(c, launch_embed(cf.dtype, c->emb, c->at<int>(L.row_tok), M, d, x, c->st));
+  AttnParams att{};
+  att.seq_ids = c->at<int>(L.seq_ids);
+  att.prefix_dev = c->at<int>(L.seq_len);
+  att.rows_per_seq = T; att.nq = T; att.n_tail = T; att.causal = 0;
+  att.mask = c->at<uint64_t>(L.tree_mask); att.mask_words = L.W; att.mask_seq_stride = T * L.W;
+  att.nbatch = B;
+  for (int l = 0; l < cf.n_layers; ++l) HIPCK(c, run_layer(c, c->layers[l], l, x, M, att, max_keys));
+  // final norm (x_N kept in xa for the Augmenting Block), LM head, greedy argmax
+  HIPCK(c, launch_rmsnorm(cf.dtype, x, d, M, d, c->final_norm, cf.rms_eps, c->at<void>(L.xn), d, xa, c->st));
+  GemmParams lm{};
+  lm.X = c->at<void>(L.xn); lm.ldx = d; lm.mode = EP_F32;
+  lm.out_f = c->at<float>(L.vlogits); lm.ldo = cf.vocab;
+  HIPCK(c, run_gemm(c, lm, M, d, {{c->lm_head, cf.vocab}}));
+  HIPCK(c, launch_argmax(c->at<float>(L.vlogits), M, cf.vocab, c->at<int>(L.target), c->st));
+  // Augmenting Block over the tree (tree mask, its own KV cache)
+  HIPCK(c, run_layer(c, c->layers[cf.n_layers], cf.n_layers, xa, M, att, max_keys));
+  HIPCK(c, hipEventRecord(c->ev[2], c->st));
+  AcceptParams ap{};
+  ap.seq_ids = c->at<int>(L.seq_ids); ap.nbatch = B; ap.T = T; ap.H = H;
+  ap.tree_token = c->at<int>(L.tree_token); ap.tree_parent = c->at<int>(L.tree_parent);
+  ap.target = c->at<int>(L.target);
+  ap.acc = c->at<int>(L.acc); ap.acc_len = c->at<int>(L.acc_len);
+  ap.out_tokens = c->at<int>(L.out_tokens); ap.t0 = c->at<int>(L.t0);
+  ap.ab_out = xa; ap.d = d; ap.h0 = c->at<float>(L.h0);
+  HIPCK(c, launch_accept(ap, c->st));
+  CompactParams cp{};
+  cp.seq_ids = c->at<int>(L.seq_ids); cp.nbatch = B; cp.H = H;
+  cp.acc = c->at<int>(L.acc); cp.acc_len = c->at<int>(L.acc_len); cp.seq_len = c->at<int>(L.seq_len);
+  cp.kpools = c->at<void*>(L.pool_ptrs); cp.vpools = c->at<void*>(L.pool_ptrs) + (cf.n_layers + 1);
+  cp.nlayers = cf.n_layers + 1;
+  cp.block_table = c->at<int>(L.block_table); cp.max_blocks = L.mbps;
+  cp.n_kv = cf.n_kv_heads; cp.hd = cf.head_dim;
+  HIPCK(c, launch_compact(cf.dtype, cp, c->st));
+  c->host_out.resize((size_t)B * (H + 1));
+  HIPCK(c, hipMemcpyAsync(c->host_out.data(), c->at<int>(L.out_tokens), sizeof(int) * B * (H + 1),
+                          hipMemcpyDeviceToHost, c->st));
+  HIPCK(c, hipEventRecord(c->ev[3], c->st));
+  HIPCK(c, hipStreamSynchronize(c->st));
+  for (int b = 0; b < B; ++b) {
+    int n = 0;
+    for (int i = 0; i <= H; ++i) {
+      const int t = c->host_out[(size_t)b * (H + 1) + i];
+      out_tokens[(size_t)b * (H + 1) + i] = t;
+      if (t >= 0) ++n;
+    }
+    out_count[b] = n;
+    c->seq_len[c->host_ids[b]] += n;
+  }
+  float ms;
+  if (hipEventElapsedTime(&ms, c->ev[0], c->ev[1]) == hipSuccess) c->tim.draft_ms = ms;
+  if (hipEventElapsedTime(&ms, c->ev[1], c->ev[2]) == hipSuccess) c->tim.verify_ms = ms;
+  if (hipEventElapsedTime(&ms, c->ev[2], c->ev[3]) == hipSuccess) c->tim.accept_ms = ms;
+  if (hipEventElapsedTime(&ms, c->ev[0], c->ev[3]) == hipSuccess) c->tim.total_ms = ms;
+  c->tim.steps++;
+  return CLOVER_OK;
+}
+
+clover_status check_ctx(clover_ctx* c) {
+  if (!c) {
+    set_global_err("context is null");
+    return CLOVER_ERR_INVALID_ARG;
+  }
+  if (c->dead) return ctx_fail(c, CLOVER_ERR_DEVICE, "context unusable after a device error");
+  return CLOVER_OK;
+}
+
+// upload batch ids and committed lengths; make KV room for L + T
+clover_status begin_batch(clover_ctx* c, const int32_t* seqs, int B, int& max_keys) {
+  const Layout& L = c->L;
+  c->host_ids.assign(seqs, seqs + B);
+  max_keys = 0;
+  for (int b = 0; b < B; ++b) {
+    const int s = seqs[b];
+    clover_status st = ensure_blocks(c, s, c->seq_len[s] + L.T);
+    if (st != CLOVER_OK) return st;
+    max_keys = std::max(max_keys, c->seq_len[s] + L.T);
+  }
+  c->host_len.assign(c->seq_len.begin(), c->seq_len.end());
+  for (auto& v : c->host_len) v = std::max(v, 0);
+  HIPCK(c, hipMemcpyAsync(c->at<int>(L.seq_ids), c->host_ids.data(), sizeof(int) * B, hipMemcpyHostToDevice, c->st));
+  HIPCK(c, hipMemcpyAsync(c->at<int>(L.seq_len), c->host_len.data(), sizeof(int) * c->cfg.max_batch,
+                          hipMemcpyHostToDevice, c->st));
+  return CLOVER_OK;
+}
+
+clover_status check_seqs(clover_ctx* c, const int32_t* seqs, int n) {
+  if (!seqs || n < 1 || n > c->cfg.max_batch) return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "bad sequence list");
+  for (int i = 0; i < n; ++i) {
+    const int s = seqs[i];
+    if (s < 0 || s >= c->cfg.max_batch) return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "sequence %d out of range", s);
+    for (int j = 0; j < i; ++j)
+      if (seqs[j] == s) return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "sequence %d listed twice", s);
+    if (c->seq_len[s] < 0) return ctx_fail(c, CLOVER_ERR_STATE, "sequence %d is not active", s);
+    if (c->seq_len[s] + c->L.T > c->cfg.max_context)
+      return ctx_fail(c, CLOVER_ERR_CAPACITY, "sequence %d would exceed max_context", s);
+  }
+  return CLOVER_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+clover_status clover_check_config(const clover_config* cfg) {
+  std::string why;
+  if (!check_config(cfg, why)) {
+    set_global_err("invalid config: %s", why.c_str());
+    return CLOVER_ERR_INVALID_ARG;
+  }
+  return CLOVER_OK;
+}
+
+size_t clover_weight_count(const clover_config* cfg) {
+  if (clover_check_config(cfg) != CLOVER_OK) return 0;
+  return weight_specs(*cfg).size();
+}
+
+int clover_weight_name(const clover_config* cfg, size_t i, char* buf, size_t buflen) {
+  if (clover_check_config(cfg) != CLOVER_OK) return -1;
+  auto s = weight_specs(*cfg);
+  if (i >= s.size() || !buf || buflen == 0) return -1;
+  snprintf(buf, buflen, "%s", s[i].name.c_str());
+  return (int)s[i].name.size();
+}
+
+int clover_weight_shape(const clover_config* cfg, size_t i, int64_t out[2]) {
+  if (clover_check_config(cfg) != CLOVER_OK) return -1;
+  auto s = weight_specs(*cfg);
+  if (i >= s.size() || !out) return -1;
+  out[0] = s[i].rows;
+  out[1] = s[i].cols;
+  return s[i].cols ? 2 : 1;
+}
+
+size_t clover_packed_bytes(const clover_config* cfg, size_t i) {
+  if (clover_check_config(cfg) != CLOVER_OK) return 0;
+  auto s = weight_specs(*cfg);
+  if (i >= s.size()) return 0;
+  return (size_t)s[i].rows * std::max<int64_t>(s[i].cols, 1) * es_of(cfg->dtype);
+}
+
+size_t clover_workspace_bytes(const clover_config* cfg) {
+  if (clover_check_config(cfg) != CLOVER_OK) return 0;
+  return make_layout(*cfg).total;
+}
+
+clover_status clover_pack_weight(const clover_config* cfg, size_t i, const void* src, void* dst,
+                                 void* hip_stream) {
+  if (clover_check_config(cfg) != CLOVER_OK) return CLOVER_ERR_INVALID_ARG;
+  auto s = weight_specs(*cfg);
+  if (i >= s.size() || !src || !dst) {
+    set_global_err("pack: bad index or null pointer");
+    return CLOVER_ERR_INVALID_ARG;
+  }
+  hipStream_t st = (hipStream_t)hip_stream;
+  hipError_t e;
+  if (s[i].matrix)
+    e = launch_pack(cfg->dtype, src, (int)s[i].rows, (int)s[i].cols, dst, st);
+  else
+    e = hipMemcpyAsync(dst, src, clover_packed_bytes(cfg, i), hipMemcpyDeviceToDevice, st);
+  if (e != hipSuccess) {
+    set_global_err("pack: %s", hipGetErrorString(e));
+    return CLOVER_ERR_DEVICE;
+  }
+  return CLOVER_OK;
+}
+
+const char* clover_last_error(const clover_ctx* ctx) { return ctx ? ctx->err.c_str() : g_err.c_str(); }
+
+clover_status clover_init(const clover_config* cfg, void* const* weights, void* workspace,
+                          size_t ws_bytes, void* hip_stream, clover_ctx** out) {
+  if (!out) {
+    set_global_err("out is null");
+    return CLOVER_ERR_INVALID_ARG;
+  }
+  *out = nullptr;
+  if (clover_check_config(cfg) != CLOVER_OK) return CLOVER_ERR_INVALID_ARG;
+  if (!weights || !workspace) {
+    set_global_err("weights or workspace is null");
+    return CLOVER_ERR_INVALID_ARG;
+  }
+  auto specs = weight_specs(*cfg);
+  for (size_t i = 0; i < specs.size(); ++i)
+    if (!weights[i]) {
+      set_global_err("weight %zu (%s) is null", i, specs[i].name.c_str());
+      return CLOVER_ERR_INVALID_ARG;
+    }
+  Layout L = make_layout(*cfg);
+  if (ws_bytes < L.total) {
+    set_global_err("workspace too small: %zu < %zu bytes", ws_bytes, L.total);
+    return CLOVER_ERR_CAPACITY;
+  }
+  clover_ctx* c = new clover_ctx();
+  c->cfg = *cfg;
+  c->L = L;
+  c->st = (hipStream_t)hip_stream;
+  c->ws = (char*)workspace;
+  c->w.assign(weights, weights + specs.size());
+  size_t k = 0;
+  c->emb = c->w[k++];
+  auto take_layer = [&]() {
+    LayerPtrs p;
+    p.attn_norm = c->w[k++]; p.wq = c->w[k++]; p.wk = c->w[k++]; p.wv = c->w[k++]; p.wo = c->w[k++];
+    p.mlp_norm = c->w[k++]; p.wg = c->w[k++]; p.wu = c->w[k++]; p.wd = c->w[k++];
+    return p;
+  };
+  for (int l = 0; l < cfg->n_layers; ++l) c->layers.push_back(take_layer());
+  c->final_norm = c->w[k++];
+  c->lm_head = c->w[k++];
+  c->layers.push_back(take_layer());
+  c->ad_norm = c->w[k++]; c->ad_wq = c->w[k++]; c->ad_wk = c->w[k++]; c->ad_wv = c->w[k++]; c->ad_wo = c->w[k++];
+  for (int j = 0; j < cfg->n_spec_heads; ++j) {
+    c->head_w1.push_back(c->w[k++]);
+    c->head_b1.push_back(c->w[k++]);
+  }
+  c->seq_len.assign(cfg->max_batch, -1);
+  c->seq_blocks.assign(cfg->max_batch, {});
+  for (int b = L.nblocks - 1; b >= 0; --b) c->free_blocks.push_back(b);
+  c->bt_host.assign((size_t)cfg->max_batch * L.mbps, 0);
+  auto fail = [&](hipError_t e, const char* what) {
+    set_global_err("init: %s: %s", what, hipGetErrorString(e));
+    delete c;
+    return CLOVER_ERR_DEVICE;
+  };
+  hipError_t e;
+  for (int i = 0; i < 4; ++i)
+    if ((e = hipEventCreate(&c->ev[i])) != hipSuccess) return fail(e, "event");
+  // zero the KV pools (attention reads whole 16-key blocks), counters and state
+  if ((e = hipMemsetAsync(c->ws, 0, L.pool_ptrs, c->st)) != hipSuccess) return fail(e, "memset pools");
+  if ((e = hipMemsetAsync(c->ws + L.block_table, 0, L.x - L.block_table, c->st)) != hipSuccess) return fail(e, "memset state");
+  if ((e = hipMemsetAsync(c->ws + L.gsem, 0, 4 * L.gsem_n, c->st)) != hipSuccess) return fail(e, "memset gsem");
+  if ((e = hipMemsetAsync(c->ws + L.asem, 0, 4 * L.asem_n, c->st)) != hipSuccess) return fail(e, "memset asem");
+  std::vector<void*> pools(2 * (cfg->n_layers + 1));
+  for (int l = 0; l <= cfg->n_layers; ++l) {
+    pools[l] = c->ws + L.kpool + L.pool_bytes * l;
+    pools[cfg->n_layers + 1 + l] = c->ws + L.vpool + L.pool_bytes * l;
+  }
+  if ((e = hipMemcpyAsync(c->ws + L.pool_ptrs, pools.data(), sizeof(void*) * pools.size(),
+                          hipMemcpyHostToDevice, c->st)) != hipSuccess)
+    return fail(e, "pool table");
+  if ((e = hipStreamSynchronize(c->st)) != hipSuccess) return fail(e, "sync");
+  *out = c;
+  return CLOVER_OK;
+}
+
+void clover_destroy(clover_ctx* ctx) {
+  if (!ctx) return;
+  hipStreamSynchronize(ctx->st);
+  for (int i = 0; i < 4; ++i) hipEventDestroy(ctx->ev[i]);
+  delete ctx;
+}
+
+int32_t clover_seq_len(const clover_ctx* ctx, int32_t seq) {
+  if (!ctx || seq < 0 || seq >= ctx->cfg.max_batch) return -1;
+  return ctx->seq_len[seq];
+}
+
+clover_status clover_release(clover_ctx* c, int32_t seq) {
+  clover_status s = check_ctx(c);
+  if (s) return s;
+  if (seq < 0 || seq >= c->cfg.max_batch) return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "sequence out of range");
+  if (c->seq_len[seq] < 0) return ctx_fail(c, CLOVER_ERR_STATE, "sequence %d is not active", seq);
+  for (int b : c->seq_blocks[seq]) c->free_blocks.push_back(b);
+  c->seq_blocks[seq].clear();
+  c->seq_len[seq] = -1;
+  return CLOVER_OK;
+}
+
+clover_status clover_prefill(clover_ctx* c, int32_t seq, const int32_t* tokens, int32_t n,
+                             int32_t* first_token) {
+  clover_status s = check_ctx(c);
+  if (s) return s;
+  const clover_config& cf = c->cfg;
+  const Layout& L = c->L;
+  if (seq < 0 || seq >= cf.max_batch) return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "sequence %d out of range", seq);
+  if (!tokens || n < 1 || !first_token) return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "bad prompt");
+  if (c->seq_len[seq] >= 0) return ctx_fail(c, CLOVER_ERR_STATE, "sequence %d is already active", seq);
+  if ((int64_t)n + L.T > cf.max_context) return ctx_fail(c, CLOVER_ERR_CAPACITY, "prompt of %d tokens exceeds max_context", n);
+  for (int i = 0; i < n; ++i)
+    if (tokens[i] < 0 || tokens[i] >= cf.vocab) return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "token %d out of range", tokens[i]);
+  if ((s = ensure_blocks(c, seq, n + L.T))) return s;
+  const int d = cf.d_model, C = L.Mp;
+  float* x = c->at<float>(L.x);
+  float* xa = c->at<float>(L.xa);
+  std::vector<int> meta(4 * (size_t)C);
+  c->host_ids.assign(1, seq);
+  HIPCK(c, hipMemcpyAsync(c->at<int>(L.seq_ids), c->host_ids.data(), sizeof(int), hipMemcpyHostToDevice, c->st));
+  for (int c0 = 0; c0 < n; c0 += C) {
+    const int rows = std::min(C, n - c0);
+    for (int i = 0; i < rows; ++i) {
+      meta[i] = tokens[c0 + i];
+      meta[C + i] = c0 + i;      // position
+      meta[2 * C + i] = c0 + i;  // slot
+      meta[3 * C + i] = seq;
+    }
+    HIPCK(c, hipMemcpyAsync(c->at<int>(L.row_tok), meta.data(), sizeof(int) * rows, hipMemcpyHostToDevice, c->st));
+    HIPCK(c, hipMemcpyAsync(c->at<int>(L.row_pos), meta.data() + C, sizeof(int) * rows, hipMemcpyHostToDevice, c->st));
+    HIPCK(c, hipMemcpyAsync(c->at<int>(L.row_slot), meta.data() + 2 * C, sizeof(int) * rows, hipMemcpyHostToDevice, c->st));
+    HIPCK(c, hipMemcpyAsync(c->at<int>(L.row_seq), meta.data() + 3 * C, sizeof(int) * rows, hipMemcpyHostToDevice, c->st));
+    HIPCK(c, launch_embed(cf.dtype, c->emb, c->at<int>(L.row_tok), rows, d, x, c->st));
+    AttnParams att{};
+    att.seq_ids = c->at<int>(L.seq_ids);
+    att.prefix_dev = nullptr; att.prefix_host = c0;
+    att.rows_per_seq = rows; att.nq = rows; att.n_tail = rows; att.causal = 1;
+    att.nbatch = 1;
+    for (int l = 0; l < cf.n_layers; ++l) HIPCK(c, run_layer(c, c->layers[l], l, x, rows, att, c0 + rows));
+    HIPCK(c, launch_rmsnorm(cf.dtype, x, d, rows, d, c->final_norm, cf.rms_eps, c->at<void>(L.xn), d, xa, c->st));
+    if (c0 + rows == n) {
+      GemmParams lm{};
+      lm.X = (const char*)c->at<char>(L.xn) + (size_t)(rows - 1) * d * L.es; lm.ldx = d; lm.mode = EP_F32;
+      lm.out_f = c->at<float>(L.vlogits); lm.ldo = cf.vocab;
+      HIPCK(c, run_gemm(c, lm, 1, d, {{c->lm_head, cf.vocab}}));
+      HIPCK(c, launch_argmax(c->at<float>(L.vlogits), 1, cf.vocab, c->at<int>(L.amax), c->st));
+    }
+    HIPCK(c, run_layer(c, c->layers[cf.n_layers], cf.n_layers, xa, rows, att, c0 + rows));
+    if (c0 + rows == n)
+      HIPCK(c, launch_finish_prefill(seq, c->at<int>(L.amax), xa + (size_t)(rows - 1) * d, d,
+                                     c->at<int>(L.t0), c->at<float>(L.h0), c->st));
+    HIPCK(c, hipStreamSynchronize(c->st));  // meta is reused by the next chunk
+  }
+  int t0 = -1;
+  HIPCK(c, hipMemcpyAsync(&t0, c->at<int>(L.t0) + seq, sizeof(int), hipMemcpyDeviceToHost, c->st));
+  HIPCK(c, hipStreamSynchronize(c->st));
+  c->seq_len[seq] = n;
+  *first_token = t0;
+  return CLOVER_OK;
+}
+
+clover_status clover_step(clover_ctx* c, const int32_t* seqs, int32_t n_seqs, int32_t* out_tokens,
+                          int32_t* out_count) {
+  clover_status s = check_ctx(c);
+  if (s) return s;
+  if (!out_tokens || !out_count) return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "null output");
+  if ((s = check_seqs(c, seqs, n_seqs))) return s;
+  const clover_config& cf = c->cfg;
+  const Layout& L = c->L;
+  const int B = n_seqs, d = cf.d_model, qd = cf.n_heads * cf.head_dim, H = L.H;
+  int max_keys = 0;
+  if ((s = begin_batch(c, seqs, B, max_keys))) return s;
+  HIPCK(c, hipEventRecord(c->ev[0], c->st));
+  int* ids = c->at<int>(L.seq_ids);
+  int *ct = c->at<int>(L.cand_token), *cpar = c->at<int>(L.cand_parent), *cd = c->at<int>(L.cand_depth);
+  float* clp = c->at<float>(L.cand_lp);
+  HIPCK(c, launch_set_root(ids, B, c->at<int>(L.t0), ct, cpar, cd, clp, L.NC, c->st));
+  for (int j = 1; j <= H; ++j) {
+    const int F = frontier(cf, j), M = B * F;
+    AdPrepParams ap{};
+    ap.use_slot_state = (j == 1);
+    ap.prev = (j == 1) ? c->at<float>(L.h0) : c->at<float>(L.dstate[j - 2]);
+    ap.Fprev = (j == 1) ? 1 : frontier(cf, j - 1);
+    ap.kprev = (j == 1) ? 1 : cf.topk[j - 2];
+    ap.seq_ids = ids; ap.nbatch = B; ap.F = F;
+    ap.cand_token = ct; ap.cand_stride = L.NC; ap.base_node = depth_base(cf, j - 1);
+    ap.lm_packed = c->lm_head; ap.lm_nchunks = d / kc_of(cf.dtype);
+    ap.ad_norm = c->ad_norm; ap.eps = cf.rms_eps; ap.d = d;
+    ap.hin = c->at<float>(L.d_hin); ap.a_out = c->at<void>(L.d_a); ap.e_out = c->at<void>(L.d_e);
+    HIPCK(c, launch_ad_prep(cf.dtype, ap, c->st));
+    GemmParams q{};
+    q.X = c->at<void>(L.d_a); q.ldx = d; q.mode = EP_F32; q.out_f = c->at<float>(L.d_q); q.ldo = qd;
+    HIPCK(c, run_gemm(c, q, M, d, {{c->ad_wq, qd}}));
+    GemmParams kv{};
+    kv.X = c->at<void>(L.d_e); kv.ldx = d; kv.mode = EP_F32; kv.out_f = c->at<float>(L.d_kv); kv.ldo = 2 * qd;
+    HIPCK(c, run_gemm(c, kv, M, d, {{c->ad_wk, qd}, {c->ad_wv, qd}}));
+    HIPCK(c, launch_ad_attn(cf.dtype, c->at<float>(L.d_q), c->at<float>(L.d_kv), M, cf.n_heads,
+                            cf.head_dim, c->at<void>(L.d_o), c->st));
+    GemmParams o{};
+    o.X = c->at<void>(L.d_o); o.ldx = qd; o.mode = EP_RESID;
+    o.resid = c->at<float>(L.d_hin); o.ldr = d;
+    o.out_f = c->at<float>(L.dstate[j - 1]); o.ldo = d;
+    o.out_s = c->at<void>(L.d_sst); o.ldos = d;
+    HIPCK(c, run_gemm(c, o, M, qd, {{c->ad_wo, d}}));
+    GemmParams hm{};
+    hm.X = c->at<void>(L.d_sst); hm.ldx = d; hm.mode = EP_HEAD;
+    hm.resid = c->at<float>(L.dstate[j - 1]); hm.ldr = d; hm.bias = c->head_b1[j - 1];
+    hm.out_f = c->at<float>(L.d_r); hm.ldo = d;
+    HIPCK(c, run_gemm(c, hm, M, d, {{c->head_w1[j - 1], d}}));
+    HIPCK(c, launch_rmsnorm(cf.dtype, c->at<float>(L.d_r), d, M, d, c->final_norm, cf.rms_eps,
+                            c->at<void>(L.d_rn), d, nullptr, c->st));
+    GemmParams lm{};
+    lm.X = c->at<void>(L.d_rn); lm.ldx = d; lm.mode = EP_F32;
+    lm.out_f = c->at<float>(L.dlogits[j - 1]); lm.ldo = cf.vocab;
+    HIPCK(c, run_gemm(c, lm, M, d, {{c->lm_head, cf.vocab}}));
+    TopkParams tp{};
+    tp.logits = c->at<float>(L.dlogits[j - 1]); tp.M = M; tp.V = cf.vocab; tp.k = cf.topk[j - 1];
+    tp.seq_ids = ids; tp.F = F;
+    tp.cand_token = ct; tp.cand_parent = cpar; tp.cand_depth = cd; tp.cand_lp = clp; tp.cand_stride = L.NC;
+    tp.base_parent = depth_base(cf, j - 1); tp.base_child = depth_base(cf, j); tp.depth = j;
+    HIPCK(c, launch_topk(tp, c->st));
+  }
+  TreeParams tr{};
+  tr.seq_ids = ids; tr.nbatch = B;
+  tr.cand_token = ct; tr.cand_parent = cpar; tr.cand_depth = cd; tr.cand_lp = clp;
+  tr.cand_stride = L.NC; tr.n_cand = L.NC; tr.T = L.T; tr.mask_words = L.W;
+  tr.seq_len = c->at<int>(L.seq_len);
+  tr.tree_token = c->at<int>(L.tree_token); tr.tree_parent = c->at<int>(L.tree_parent);
+  tr.tree_depth = c->at<int>(L.tree_depth); tr.tree_pos = c->at<int>(L.tree_pos);
+  tr.tree_mask = c->at<uint64_t>(L.tree_mask);
+  tr.row_tok = c->at<int>(L.row_tok); tr.row_pos = c->at<int>(L.row_pos);
+  tr.row_slot = c->at<int>(L.row_slot); tr.row_seq = c->at<int>(L.row_seq);
+  HIPCK(c, launch_tree_build(tr, c->st));
+  HIPCK(c, hipEventRecord(c->ev[1], c->st));
+  c->last_nbatch = B;
+  return verify_accept(c, B, out_tokens, out_count, max_keys);
+}
+
+clover_status clover_verify_tree(clover_ctx* c, int32_t seq, const int32_t* tokens,
+                                 const int32_t* parents, int32_t T, int32_t* out_tokens,
+                                 int32_t* out_count) {
+  clover_status s = check_ctx(c);
+  if (s) return s;
+  const clover_config& cf = c->cfg;
+  const Layout& L = c->L;
+  if (!tokens || !parents || !out_tokens || !out_count) return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "null argument");
+  if ((s = check_seqs(c, &seq, 1))) return s;
+  if (T < 1 || T > L.T) return ctx_fail(c, CLOVER_ERR_BAD_TREE, "tree of %d tokens (max %d)", T, L.T);
+  if (parents[0] != -1) return ctx_fail(c, CLOVER_ERR_BAD_TREE, "parents[0] must be -1");
+  std::vector<int> depth(L.T, 0), tok(L.T, 0), par(L.T, -1);
+  for (int i = 0; i < T; ++i) {
+    if (tokens[i] < 0 || tokens[i] >= cf.vocab) return ctx_fail(c, CLOVER_ERR_BAD_TREE, "token %d out of range", tokens[i]);
+    if (i > 0 && (parents[i] < 0 || parents[i] >= i)) return ctx_fail(c, CLOVER_ERR_BAD_TREE, "parents[%d] = %d", i, parents[i]);
+    tok[i] = tokens[i];
+    par[i] = parents[i];
+    if (i > 0) depth[i] = depth[parents[i]] + 1;
+    if (depth[i] > L.H) return ctx_fail(c, CLOVER_ERR_BAD_TREE, "tree deeper than %d", L.H);
+  }
+  // Pad to the configured size: padding nodes have parent -2, which no accepted node
+  // index equals, and see only themselves (plus the committed prefix) in attention.
+  for (int i = T; i < L.T; ++i) {
+    tok[i] = tokens[0];
+    par[i] = -2;
+    depth[i] = 1;
+  }
+  int max_keys = 0;
+  if ((s = begin_batch(c, &seq, 1, max_keys))) return s;
+  const int Ln = c->seq_len[seq];
+  // tree arrays and verify rows for slot `seq`
+  std::vector<int> meta(8 * (size_t)L.T);
+  std::vector<uint64_t> mask((size_t)L.T * L.W, 0);
+  for (int i = 0; i < L.T; ++i) {
+    if (i < T)
+      for (int j = i; j >= 0; j = par[j]) mask[(size_t)i * L.W + j / 64] |= 1ull << (j % 64);
+    else
+      mask[(size_t)i * L.W + i / 64] |= 1ull << (i % 64);
+    meta[i] = tok[i];
+    meta[L.T + i] = par[i];
+    meta[2 * L.T + i] = depth[i];
+    meta[3 * L.T + i] = Ln + depth[i];
+    meta[4 * L.T + i] = tok[i];          // row_tok
+    meta[5 * L.T + i] = Ln + depth[i];   // row_pos
+    meta[6 * L.T + i] = Ln + i;          // row_slot
+    meta[7 * L.T + i] = seq;             // row_seq
+  }
+  const size_t tb = (size_t)seq * L.T;
+  HIPCK(c, hipMemcpyAsync(c->at<int>(L.tree_token) + tb, meta.data(), 4 * L.T, hipMemcpyHostToDevice, c->st));
+  HIPCK(c, hipMemcpyAsync(c->at<int>(L.tree_parent) + tb, meta.data() + L.T, 4 * L.T, hipMemcpyHostToDevice, c->st));
+  HIPCK(c, hipMemcpyAsync(c->at<int>(L.tree_depth) + tb, meta.data() + 2 * L.T, 4 * L.T, hipMemcpyHostToDevice, c->st));
+  HIPCK(c, hipMemcpyAsync(c->at<int>(L.tree_pos) + tb, meta.data() + 3 * L.T, 4 * L.T, hipMemcpyHostToDevice, c->st));
+  HIPCK(c, hipMemcpyAsync(c->at<uint64_t>(L.tree_mask) + tb * L.W, mask.data(), 8 * mask.size(), hipMemcpyHostToDevice, c->st));
+  HIPCK(c, hipMemcpyAsync(c->at<int>(L.row_tok), meta.data() + 4 * L.T, 4 * L.T, hipMemcpyHostToDevice, c->st));
+  HIPCK(c, hipMemcpyAsync(c->at<int>(L.row_pos), meta.data() + 5 * L.T, 4 * L.T, hipMemcpyHostToDevice, c->st));
+  HIPCK(c, hipMemcpyAsync(c->at<int>(L.row_slot), meta.data() + 6 * L.T, 4 * L.T, hipMemcpyHostToDevice, c->st));
+  HIPCK(c, hipMemcpyAsync(c->at<int>(L.row_seq), meta.data() + 7 * L.T, 4 * L.T, hipMemcpyHostToDevice, c->st));
+  HIPCK(c, hipEventRecord(c->ev[0], c->st));
+  HIPCK(c, hipEventRecord(c->ev[1], c->st));
+  c->last_nbatch = 1;
+  return verify_accept(c, 1, out_tokens, out_count, max_keys);
+}
+
+clover_status clover_debug_read(clover_ctx* c, const char* name, void* host_dst, size_t bytes,
+                                size_t* written) {
+  clover_status s = check_ctx(c);
+  if (s) return s;
+  if (!name || !host_dst) return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "null argument");
+  const clover_config& cf = c->cfg;
+  const Layout& L = c->L;
+  const size_t B = cf.max_batch, T = L.T, NC = L.NC, H = L.H;
+  struct Item { const char* n; size_t off, bytes; };
+  std::vector<Item> items = {
+      {"cand_token", L.cand_token, 4 * B * NC}, {"cand_parent", L.cand_parent, 4 * B * NC},
+      {"cand_depth", L.cand_depth, 4 * B * NC}, {"cand_lp", L.cand_lp, 4 * B * NC},
+      {"tree_token", L.tree_token, 4 * B * T}, {"tree_parent", L.tree_parent, 4 * B * T},
+      {"tree_depth", L.tree_depth, 4 * B * T}, {"tree_pos", L.tree_pos, 4 * B * T},
+      {"tree_mask", L.tree_mask, 8 * B * T * L.W}, {"target", L.target, 4 * B * T},
+      {"acc", L.acc, 4 * B * (H + 1)}, {"acc_len", L.acc_len, 4 * B}, {"h0", L.h0, 4 * B * cf.d_model},
+      {"t0", L.t0, 4 * B}, {"verify_logits", L.vlogits, 4 * B * T * (size_t)cf.vocab},
+      {"x_last", L.x, 4 * B * T * (size_t)cf.d_model}, {"ab_out", L.xa, 4 * B * T * (size_t)cf.d_model}};
+  std::vector<std::string> dn;
+  for (int j = 1; j <= L.H; ++j) dn.push_back("draft_logits" + std::to_string(j));
+  for (int j = 1; j <= L.H; ++j)
+    items.push_back({dn[j - 1].c_str(), L.dlogits[j - 1], 4 * B * frontier(cf, j) * (size_t)cf.vocab});
+  for (auto& it : items) {
+    if (strcmp(it.n, name)) continue;
+    const size_t n = std::min(bytes, it.bytes);
+    HIPCK(c, hipStreamSynchronize(c->st));
+    HIPCK(c, hipMemcpy(host_dst, c->ws + it.off, n, hipMemcpyDeviceToHost));
+    if (written) *written = n;
+    return CLOVER_OK;
+  }
+  return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "unknown debug buffer '%s'", name);
+}
+
+clover_status clover_debug_kv(clover_ctx* c, int32_t seq, int32_t layer, int32_t pos, int32_t which_v,
+                              float* host_out) {
+  clover_status s = check_ctx(c);
+  if (s) return s;
+  const clover_config& cf = c->cfg;
+  const Layout& L = c->L;
+  if (seq < 0 || seq >= cf.max_batch || layer < 0 || layer > cf.n_layers || !host_out)
+    return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "bad argument");
+  if (pos < 0 || pos >= (int)c->seq_blocks[seq].size() * 16) return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "position not allocated");
+  const int hd = cf.head_dim, nkv = cf.n_kv_heads, EPL = 16 / L.es, KC = 4 * EPL;
+  const int blk = c->seq_blocks[seq][pos / 16], key = pos % 16;
+  std::vector<char> buf((size_t)nkv * 16 * hd * L.es);
+  const size_t off = (which_v ? L.vpool : L.kpool) + L.pool_bytes * layer + (size_t)blk * nkv * 16 * hd * L.es;
+  HIPCK(c, hipStreamSynchronize(c->st));
+  HIPCK(c, hipMemcpy(buf.data(), c->ws + off, buf.size(), hipMemcpyDeviceToHost));
+  for (int h = 0; h < nkv; ++h)
+    for (int dd = 0; dd < hd; ++dd) {
+      int idx;
+      if (!which_v) {
+        const int cc = dd / KC, q = dd % KC;
+        idx = (cc * 64 + key + 16 * (q / EPL)) * EPL + (q % EPL);
+      } else {
+        idx = (((dd >> 4) * 4 + (key >> 2)) * 16 + (dd & 15)) * 4 + (key & 3);
+      }
+      const size_t e = (size_t)h * 16 * hd + idx;
+      float v;
+      if (L.es == 2) {
+        uint32_t u = (uint32_t)(*(uint16_t*)(buf.data() + 2 * e)) << 16;
+        memcpy(&v, &u, 4);
+      } else {
+        memcpy(&v, buf.data() + 4 * e, 4);
+      }
+      host_out[h * hd + dd] = v;
+    }
+  return CLOVER_OK;
+}
+
+clover_status clover_get_timings(clover_ctx* c, clover_timings* out) {
+  clover_status s = check_ctx(c);
+  if (s) return s;
+  if (!out) return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "null output");
+  *out = c->tim;
+  return CLOVER_OK;
+}
+
+// ---- single-kernel entry points --------------------------------------------------------
+
+size_t clover_op_scratch_bytes(int32_t dtype, int32_t M, int32_t N, int32_t K) {
+  if ((dtype != 0 && dtype != 1) || M < 1 || N < 16 || N % 16 || K < 1 || K % kc_of(dtype)) return 0;
+  GemmPlan pl = plan_gemm(dtype, M, N / 16, K / kc_of(dtype), false);
+  return align_up(4 * pl.part_floats) + align_up(4 * (size_t)pl.ngroups * pl.mchunks);
+}
+
+size_t clover_packed_matrix_bytes(int32_t dtype, int32_t rows, int32_t cols) {
+  if ((dtype != 0 && dtype != 1) || rows < 16 || rows % 16 || cols < 1 || cols % kc_of(dtype)) return 0;
+  return packed_matrix_bytes(dtype, rows, cols);
+}
+
+clover_status clover_pack_matrix(int32_t dtype, const void* src, int32_t rows, int32_t cols, void* dst,
+                                 void* hip_stream) {
+  if (!clover_packed_matrix_bytes(dtype, rows, cols) || !src || !dst) {
+    set_global_err("pack_matrix: bad arguments");
+    return CLOVER_ERR_INVALID_ARG;
+  }
+  hipError_t e = launch_pack(dtype, src, rows, cols, dst, (hipStream_t)hip_stream);
+  if (e != hipSuccess) {
+    set_global_err("pack_matrix: %s", hipGetErrorString(e));
+    return CLOVER_ERR_DEVICE;
+  }
+  return CLOVER_OK;
+}
+
+clover_status clover_op_linear(int32_t dtype, const void* X, int32_t M, int32_t K, const void* Wp,
+                               int32_t N, float* Y, void* scratch, size_t scratch_bytes,
+                               void* hip_stream) {
+  const size_t need = clover_op_scratch_bytes(dtype, M, N, K);
+  if (!need || !X || !Wp || !Y || !scratch) {
+    set_global_err("op_linear: bad arguments");
+    return CLOVER_ERR_INVALID_ARG;
+  }
+  if (scratch_bytes < need) {
+    set_global_err("op_linear: scratch %zu < %zu bytes", scratch_bytes, need);
+    return CLOVER_ERR_CAPACITY;
+  }
+  hipStream_t st = (hipStream_t)hip_stream;
+  GemmPlan pl = plan_gemm(dtype, M, N / 16, K / kc_of(dtype), false);
+  GemmParams p{};
+  p.X = X; p.ldx = K; p.M = M; p.K = K; p.nchunks = K / kc_of(dtype);
+  p.seg[0] = GemmSeg{Wp, N / 16}; p.nseg = 1; p.ntiles = N / 16; p.N = N;
+  p.part = (float*)scratch;
+  p.sem = (int*)((char*)scratch + align_up(4 * pl.part_floats));
+  p.mode = EP_F32; p.out_f = Y; p.ldo = N;
+  hipError_t e = hipMemsetAsync(p.sem, 0, 4 * (size_t)pl.ngroups * pl.mchunks, st);
+  if (e == hipSuccess) e = launch_gemm(dtype, p, st);
+  if (e != hipSuccess) {
+    set_global_err("op_linear: %s", hipGetErrorString(e));
+    return CLOVER_ERR_DEVICE;
+  }
+  return CLOVER_OK;
+}
+
+size_t clover_op_attention_scratch_bytes(int32_t dtype, int32_t L, int32_t T, int32_t n_heads,
+                                         int32_t n_kv, int32_t head_dim) {
+  if ((dtype != 0 && dtype != 1) || L < 0 || T < 1 || n_heads < 1 || n_kv < 1 || n_heads % n_kv ||
+      (head_dim != 32 && head_dim != 64 && head_dim != 128))
+    return 0;
+  const int nblocks = (L + T + 15) / 16;
+  AttnParams a{};
+  a.nbatch = 1; a.nq = T; a.n_heads = n_heads;
+  plan_attention(a, L + T);
+  size_t b = 0;
+  b += align_up((size_t)nblocks * n_kv * 16 * head_dim * es_of(dtype)) * 2;  // K and V pools
+  b += align_up(4 * (size_t)nblocks);                                          // block table
+  b += align_up(8 * (size_t)T * ((T + 63) / 64));                              // mask
+  b += align_up(4 * 2);                                                        // seq id, prefix
+  b += align_up(4 * attention_part_floats(1, a.qtiles, n_heads, a.splits, head_dim));
+  b += align_up(4 * (size_t)a.qtiles * n_heads);
+  return b;
+}
+
+clover_status clover_op_attention(int32_t dtype, const void* Q, const void* Kpre, const void* Vpre,
+                                  const void* Ktree, const void* Vtree, int32_t L, int32_t T,
+                                  const int32_t* parents, int32_t causal, int32_t n_heads,
+                                  int32_t n_kv, int32_t head_dim, void* O, void* scratch,
+                                  size_t scratch_bytes, void* hip_stream) {
+  const size_t need = clover_op_attention_scratch_bytes(dtype, L, T, n_heads, n_kv, head_dim);
+  if (!need || !Q || !Ktree || !Vtree || !O || !scratch || (L > 0 && (!Kpre || !Vpre)) ||
+      (!causal && (!parents || T > 128))) {
+    set_global_err("op_attention: bad arguments");
+    return CLOVER_ERR_INVALID_ARG;
+  }
+  if (scratch_bytes < need) {
+    set_global_err("op_attention: scratch too small");
+    return CLOVER_ERR_CAPACITY;
+  }
+  hipStream_t st = (hipStream_t)hip_stream;
+  const int nblocks = (L + T + 15) / 16, W = (T + 63) / 64;
+  const int es = es_of(dtype);
+  char* p = (char*)scratch;
+  char* kp = p; p += align_up((size_t)nblocks * n_kv * 16 * head_dim * es);
+  char* vp = p; p += align_up((size_t)nblocks * n_kv * 16 * head_dim * es);
+  int* bt = (int*)p; p += align_up(4 * (size_t)nblocks);
+  uint64_t* mask = (uint64_t*)p; p += align_up(8 * (size_t)T * W);
+  int* ids = (int*)p; p += align_up(8);
+  AttnParams a{};
+  a.nbatch = 1; a.nq = T; a.n_heads = n_heads;
+  plan_attention(a, L + T);
+  float* part = (float*)p; p += align_up(4 * attention_part_floats(1, a.qtiles, n_heads, a.splits, head_dim));
+  int* sem = (int*)p;
+  std::vector<int> hbt(nblocks);
+  for (int i = 0; i < nblocks; ++i) hbt[i] = nblocks - 1 - i;  // reversed pages: exercises the table
+  std::vector<uint64_t> hm((size_t)T * W, 0);
+  if (!causal) {
+    for (int i = 0; i < T; ++i) {
+      if (i == 0 ? parents[0] != -1 : (parents[i] < 0 || parents[i] >= i)) {
+        set_global_err("op_attention: malformed parents");
+        return CLOVER_ERR_BAD_TREE;
+      }
+      for (int j = i; j >= 0; j = parents[j]) hm[(size_t)i * W + j / 64] |= 1ull << (j % 64);
+    }
+  }
+  int zero = 0;
+  hipError_t e = hipSuccess;
+  if (!e) e = hipMemsetAsync(kp, 0, (size_t)nblocks * n_kv * 16 * head_dim * es, st);
+  if (!e) e = hipMemsetAsync(vp, 0, (size_t)nblocks * n_kv * 16 * head_dim * es, st);
+  if (!e) e = hipMemcpyAsync(bt, hbt.data(), 4 * nblocks, hipMemcpyHostToDevice, st);
+  if (!e) e = hipMemcpyAsync(mask, hm.data(), 8 * hm.size(), hipMemcpyHostToDevice, st);
+  if (!e) e = hipMemcpyAsync(ids, &zero, 4, hipMemcpyHostToDevice, st);
+  if (!e) e = hipMemsetAsync(sem, 0, 4 * (size_t)a.qtiles * n_heads, st);
+  if (!e && L > 0) e = launch_kv_write(dtype, Kpre, Vpre, L, 0, 0, kp, vp, bt, nblocks, n_kv, head_dim, st);
+  if (!e) e = launch_kv_write(dtype, Ktree, Vtree, T, L, 0, kp, vp, bt, nblocks, n_kv, head_dim, st);
+  a.Q = Q; a.ldq = n_heads * head_dim; a.O = O; a.ldo = n_heads * head_dim;
+  a.kcache = kp; a.vcache = vp; a.block_table = bt; a.max_blocks = nblocks;
+  a.seq_ids = ids; a.prefix_dev = nullptr; a.prefix_host = L;
+  a.rows_per_seq = T; a.n_tail = T; a.causal = causal ? 1 : 0;
+  a.mask = mask; a.mask_words = W; a.mask_seq_stride = T * W;
+  a.n_kv = n_kv; a.hd = head_dim; a.part = part; a.sem = sem;
+  if (!e) e = launch_attention(dtype, a, L + T, st);
+  if (!e) e = hipStreamSynchronize(st);  // host staging vectors die with this call
+  if (e != hipSuccess) {
+    set_global_err("op_attention: %s", hipGetErrorString(e));
+    return CLOVER_ERR_DEVICE;
+  }
+  return CLOVER_OK;
+}
+
+clover_status clover_op_argmax(const float* logits, int32_t M, int32_t V, int32_t* out, void* hip_stream) {
+  if (!logits || !out || M < 1 || V < 1) {
+    set_global_err("op_argmax: bad arguments");
+    return CLOVER_ERR_INVALID_ARG;
+  }
+  hipError_t e = launch_argmax(logits, M, V, out, (hipStream_t)hip_stream);
+  if (e != hipSuccess) {
+    set_global_err("op_argmax: %s", hipGetErrorString(e));
+    return CLOVER_ERR_DEVICE;
+  }
+  return CLOVER_OK;
+}
+
+clover_status clover_op_topk(const float* logits, int32_t M, int32_t V, int32_t k, int32_t* tok,
+                             float* logp, void* hip_stream) {
+  if (!logits || !tok || !logp || M < 1 || k < 1 || k > 16 || V < k) {
+    set_global_err("op_topk: bad arguments");
+    return CLOVER_ERR_INVALID_ARG;
+  }
+  TopkParams p{};
+  p.logits = logits; p.M = M; p.V = V; p.k = k; p.tok = tok; p.logp = logp;
+  hipError_t e = launch_topk(p, (hipStream_t)hip_stream);
+  if (e != hipSuccess) {
+    set_global_err("op_topk: %s", hipGetErrorString(e));
+    return CLOVER_ERR_DEVICE;
+  }
+  return CLOVER_OK;
+}
+
+clover_status clover_op_tree_build(const int32_t* cand_token, const int32_t* cand_parent,
+                                   const int32_t* cand_depth, const float* cand_lp, int32_t n_cand,
+                                   int32_t T, int32_t L, int32_t* tokens, int32_t* parent,
+                                   int32_t* depth, int32_t* pos, uint64_t* mask, void* hip_stream) {
+  if (!cand_token || !cand_parent || !cand_depth || !cand_lp || !tokens || !parent || !depth || !pos ||
+      !mask || T < 1 || T > 128 || n_cand < T || n_cand > 1024 || L < 0) {
+    set_global_err("op_tree_build: bad arguments");
+    return CLOVER_ERR_INVALID_ARG;
+  }
+  TreeParams p{};
+  p.seq_ids = nullptr; p.nbatch = 1;
+  p.cand_token = cand_token; p.cand_parent = cand_parent; p.cand_depth = cand_depth; p.cand_lp = cand_lp;
+  p.cand_stride = n_cand; p.n_cand = n_cand; p.T = T; p.mask_words = (T + 63) / 64;
+  p.seq_len = nullptr; p.seq_len_host = L;
+  p.tree_token = tokens; p.tree_parent = parent; p.tree_depth = depth; p.tree_pos = pos; p.tree_mask = mask;
+  hipError_t e = launch_tree_build(p, (hipStream_t)hip_stream);
+  if (e != hipSuccess) {
+    set_global_err("op_tree_build: %s", hipGetErrorString(e));
+    return CLOVER_ERR_DEVICE;
+  }
+  return CLOVER_OK;
+}
+
+clover_status clover_op_accept(const int32_t* tokens, const int32_t* parent, const int32_t* target,
+                               int32_t T, int32_t max_depth, int32_t* acc, int32_t* acc_len,
+                               int32_t* bonus, void* hip_stream) {
+  if (!tokens || !parent || !target || !acc || !acc_len || !bonus || T < 1 || T > 1024 ||
+      max_depth < 0 || max_depth > 15) {
+    set_global_err("op_accept: bad arguments");
+    return CLOVER_ERR_INVALID_ARG;
+  }
+  AcceptParams p{};
+  p.seq_ids = nullptr; p.nbatch = 1; p.T = T; p.H = max_depth;
+  p.tree_token = tokens; p.tree_parent = parent; p.target = target;
+  p.acc = acc; p.acc_len = acc_len; p.out_tokens = nullptr; p.t0 = bonus;
+  p.ab_out = nullptr; p.d = 0; p.h0 = nullptr;
+  hipError_t e = launch_accept(p, (hipStream_t)hip_stream);
+  if (e != hipSuccess) {
+    set_global_err("op_accept: %s", hipGetErrorString(e));
+    return CLOVER_ERR_DEVICE;
+  }
+  return CLOVER_OK;
+}
+
+}  // extern "C"

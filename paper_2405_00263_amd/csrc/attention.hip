@@ -1,0 +1,253 @@
+// Tree-masked attention over the paged KV cache (tree attention, Sec. 2.2 of the
+// paper: the causal mask of the verify forward is the token tree's ancestor matrix).
+//
+// Each query row attends to every committed key (slots 0..P-1) and to the tail keys
+// P..P+n_tail-1 its mask row admits: the tree's ancestor-or-self bits during verify,
+// or the causal rule during chunked prefill.  The score product is computed
+// transposed (S^T = K Q^T) so the matrix-core accumulator already holds, per lane,
+// four consecutive keys of one query row: exactly the operand layout the P*V product
+// needs, with no shuffles.  Softmax is online in the log2 domain.  Keys are split over
+// workgroups (split-KV); the last split of a (sequence, head, query tile) combines the
+// partial results in split order.
+#include "common.h"
+#include "kernels.h"
+
+#include <algorithm>
+
+namespace clover {
+
+static constexpr int ATT_THREADS = 256;  // 4 waves x 16 query rows
+static constexpr int ATT_TARGET_WGS = 512;
+
+__device__ __forceinline__ f32x4_t mma_pv(u32x2_t v, const float p[4], f32x4_t c, bf16_t) {
+  u32x2_t pb;
+  pb[0] = (uint32_t)f2bf(p[0]) | ((uint32_t)f2bf(p[1]) << 16);
+  pb[1] = (uint32_t)f2bf(p[2]) | ((uint32_t)f2bf(p[3]) << 16);
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, v),
+                                                   __builtin_bit_cast(s16x4_t, pb), c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4_t mma_pv(u32x4_t v, const float p[4], f32x4_t c, float) {
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(v[0]), p[0], c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(v[1]), p[1], c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(v[2]), p[2], c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(v[3]), p[3], c, 0, 0, 0);
+  return c;
+}
+
+template <typename S> struct VFrag;
+template <> struct VFrag<bf16_t> { typedef u32x2_t type; };
+template <> struct VFrag<float> { typedef u32x4_t type; };
+
+template <typename S, int HD>
+__global__ __launch_bounds__(ATT_THREADS) void attn_kernel(const AttnParams p) {
+  using T = St<S>;
+  using VT = typename VFrag<S>::type;
+  constexpr int EPL = T::EPL, KC = 4 * EPL, NQC = HD / KC, NT = HD / 16;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, j = lane & 15;
+  const int split = blockIdx.x, h = blockIdx.y, bq = blockIdx.z;
+  const int b = bq / p.qtiles, qt = bq % p.qtiles;
+  const int slot = p.seq_ids[b];
+  const int P = p.prefix_dev ? p.prefix_dev[slot] : p.prefix_host;
+  const int nkeys = P + p.n_tail;
+  const int kvh = h / (p.n_heads / p.n_kv);
+  const int row = qt * 64 + wave * 16 + j;
+  const bool valid = row < p.nq;
+  const S* Q = reinterpret_cast<const S*>(p.Q);
+
+  u32x4_t qf[NQC];
+#pragma unroll
+  for (int c = 0; c < NQC; ++c) {
+    qf[c] = u32x4_t{0u, 0u, 0u, 0u};
+    if (valid)
+      qf[c] = *reinterpret_cast<const u32x4_t*>(
+          Q + (size_t)(b * p.rows_per_seq + row) * p.ldq + h * HD + c * KC + g * EPL);
+  }
+  uint64_t mw0 = 0, mw1 = 0;
+  if (!p.causal && valid) {
+    const uint64_t* mr = p.mask + (size_t)slot * p.mask_seq_stride + (size_t)row * p.mask_words;
+    mw0 = mr[0];
+    if (p.mask_words > 1) mw1 = mr[1];
+  }
+
+  const int nblocks = (nkeys + 15) >> 4;
+  const int kb0 = split * p.blocks_per_split;
+  const int kb1 = min(nblocks, kb0 + p.blocks_per_split);
+  const float scale2 = rsqrtf((float)HD) * 1.4426950408889634f;
+  float m_i = -INFINITY, l_i = 0.f;
+  f32x4_t o[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) o[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const S* kc = reinterpret_cast<const S*>(p.kcache);
+  const S* vc = reinterpret_cast<const S*>(p.vcache);
+  for (int kb = kb0; kb < kb1; ++kb) {
+    const int blk = p.block_table[(size_t)slot * p.max_blocks + kb];
+    const size_t base = ((size_t)blk * p.n_kv + kvh) * (size_t)(16 * HD);
+    f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < NQC; ++c) {
+      const u32x4_t a = __builtin_nontemporal_load(
+          reinterpret_cast<const u32x4_t*>(kc + base + (size_t)(c * 64 + lane) * EPL));
+      s = mma_frag(a, qf[c], s, S{});
+    }
+    VT vf[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+      vf[t] = __builtin_nontemporal_load(reinterpret_cast<const VT*>(vc + base + (size_t)(t * 64 + lane) * 4));
+
+    float s2[4];
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int key = kb * 16 + 4 * g + r;
+      bool vis = valid && key < nkeys;
+      if (vis && key >= P) {
+        const int tk = key - P;
+        if (p.causal)
+          vis = tk <= row;
+        else
+          vis = ((tk < 64 ? mw0 >> tk : mw1 >> (tk - 64)) & 1ull) != 0;
+      }
+      s2[r] = vis ? s[r] * scale2 : -INFINITY;
+      mloc = fmaxf(mloc, s2[r]);
+    }
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+    const float m_new = fmaxf(m_i, mloc);
+    const float alpha = (m_new == -INFINITY) ? 1.f : exp2f(m_i - m_new);
+    float pr[4], lsum = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      pr[r] = (s2[r] == -INFINITY) ? 0.f : exp2f(s2[r] - m_new);
+      lsum += pr[r];
+    }
+    lsum += __shfl_xor(lsum, 16);
+    lsum += __shfl_xor(lsum, 32);
+    l_i = l_i * alpha + lsum;
+    m_i = m_new;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      o[t] *= alpha;
+      o[t] = mma_pv(vf[t], pr, o[t], S{});
+    }
+  }
+
+  S* O = reinterpret_cast<S*>(p.O);
+  const int rt = wave * 16 + j;
+  if (p.splits == 1) {
+    if (valid) {
+      const float inv = l_i > 0.f ? 1.f / l_i : 0.f;
+      S* orow = O + (size_t)(b * p.rows_per_seq + row) * p.ldo + h * HD;
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) orow[t * 16 + 4 * g + r] = T::from_f(o[t][r] * inv);
+    }
+    return;
+  }
+  const size_t pstride = (size_t)64 * (HD + 2);
+  const size_t item = (size_t)bq * p.n_heads + h;
+  float* pp = p.part + (item * p.splits + split) * pstride;
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) pp[(size_t)rt * HD + t * 16 + 4 * g + r] = o[t][r];
+  if (g == 0) {
+    pp[64 * HD + rt] = m_i;
+    pp[64 * HD + 64 + rt] = l_i;
+  }
+  __threadfence();
+  __syncthreads();
+  __shared__ int last;
+  if (threadIdx.x == 0) {
+    const int old = atomicAdd(p.sem + item, 1);
+    last = (old == p.splits - 1);
+    if (last) atomicExch(p.sem + item, 0);
+  }
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  const float* base = p.part + item * p.splits * pstride;
+  for (int e = threadIdx.x; e < 64 * HD; e += ATT_THREADS) {
+    const int r2 = e / HD, dim = e % HD;
+    const int row2 = qt * 64 + r2;
+    if (row2 >= p.nq) continue;
+    float M = -INFINITY;
+    for (int s2 = 0; s2 < p.splits; ++s2)
+      M = fmaxf(M, __builtin_nontemporal_load(base + s2 * pstride + 64 * HD + r2));
+    float num = 0.f, den = 0.f;
+    for (int s2 = 0; s2 < p.splits; ++s2) {
+      const float ms = __builtin_nontemporal_load(base + s2 * pstride + 64 * HD + r2);
+      const float w = (ms == -INFINITY) ? 0.f : exp2f(ms - M);
+      num += w * __builtin_nontemporal_load(base + s2 * pstride + (size_t)r2 * HD + dim);
+      den += w * __builtin_nontemporal_load(base + s2 * pstride + 64 * HD + 64 + r2);
+    }
+    O[(size_t)(b * p.rows_per_seq + row2) * p.ldo + h * HD + dim] = T::from_f(den > 0.f ? num / den : 0.f);
+  }
+}
+
+void plan_attention(AttnParams& p, int max_keys) {
+  p.qtiles = (p.nq + 63) / 64;
+  const int nblocks = std::max(1, (max_keys + 15) / 16);
+  const int base = p.nbatch * p.qtiles * p.n_heads;
+  int splits = std::max(1, std::min(nblocks, (ATT_TARGET_WGS + base - 1) / base));
+  p.blocks_per_split = (nblocks + splits - 1) / splits;
+  p.splits = (nblocks + p.blocks_per_split - 1) / p.blocks_per_split;
+}
+
+size_t attention_part_floats(int nbatch, int qtiles, int n_heads, int splits, int hd) {
+  return splits > 1 ? (size_t)nbatch * qtiles * n_heads * splits * 64 * (hd + 2) : 0;
+}
+
+template <typename S>
+static hipError_t launch_attn_t(AttnParams& p, hipStream_t st) {
+  dim3 grid(p.splits, p.n_heads, p.nbatch * p.qtiles), block(ATT_THREADS);
+  switch (p.hd) {
+    case 32: hipLaunchKernelGGL((attn_kernel<S, 32>), grid, block, 0, st, p); break;
+    case 64: hipLaunchKernelGGL((attn_kernel<S, 64>), grid, block, 0, st, p); break;
+    case 128: hipLaunchKernelGGL((attn_kernel<S, 128>), grid, block, 0, st, p); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_attention(int dtype, AttnParams& p, int max_keys, hipStream_t st) {
+  plan_attention(p, max_keys);
+  if (p.nq <= 0 || p.nbatch <= 0) return hipSuccess;
+  return dtype == 1 ? launch_attn_t<bf16_t>(p, st) : launch_attn_t<float>(p, st);
+}
+
+}  // namespace clover
+
+namespace clover {
+
+template <typename S>
+__global__ void kv_write_kernel(const S* __restrict__ K, const S* __restrict__ V, int n, int slot0,
+                                int seq, S* __restrict__ kc, S* __restrict__ vc,
+                                const int* __restrict__ bt, int max_blocks, int n_kv, int hd) {
+  const int r = blockIdx.x;
+  const int slot = slot0 + r;
+  for (int e = threadIdx.x; e < n_kv * hd; e += blockDim.x) {
+    const int kvh = e / hd, d = e % hd;
+    const size_t base = kv_block_base(bt, max_blocks, seq, slot, kvh, n_kv, hd);
+    kc[base + kblk_off(slot & 15, d, St<S>::EPL)] = K[(size_t)r * n_kv * hd + e];
+    vc[base + vblk_off(slot & 15, d)] = V[(size_t)r * n_kv * hd + e];
+  }
+}
+
+hipError_t launch_kv_write(int dtype, const void* K, const void* V, int n, int slot0, int seq,
+                           void* kcache, void* vcache, const int* block_table, int max_blocks,
+                           int n_kv, int hd, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  if (dtype == 1)
+    hipLaunchKernelGGL(kv_write_kernel<bf16_t>, dim3(n), dim3(256), 0, st, (const bf16_t*)K,
+                       (const bf16_t*)V, n, slot0, seq, (bf16_t*)kcache, (bf16_t*)vcache,
+                       block_table, max_blocks, n_kv, hd);
+  else
+    hipLaunchKernelGGL(kv_write_kernel<float>, dim3(n), dim3(256), 0, st, (const float*)K,
+                       (const float*)V, n, slot0, seq, (float*)kcache, (float*)vcache, block_table,
+                       max_blocks, n_kv, hd);
+  return hipGetLastError();
+}
+
+}  // namespace clover

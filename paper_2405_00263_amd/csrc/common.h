@@ -1,0 +1,94 @@
+// Shared device helpers for the Clover gfx950 kernels: storage types, bf16
+// conversion, matrix-core wrappers and the tiled layouts of packed weights and of
+// the paged KV cache.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+typedef uint16_t bf16_t;  // bf16 bit pattern in storage
+
+__device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float((uint32_t)h << 16); }
+// round to nearest even (finite inputs)
+__device__ __forceinline__ bf16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+// Storage type traits.  A "lane vector" is 16 bytes: EPL elements.  A matrix-core
+// fragment is 64 lanes x 16 bytes and covers 16 rows x KC columns (KC = 4 * EPL).
+template <typename S> struct St;
+template <> struct St<float> {
+  static constexpr int EPL = 4;
+  __device__ static __forceinline__ float ld(const float* p) { return *p; }
+  __device__ static __forceinline__ float to_f(float v) { return v; }
+  __device__ static __forceinline__ float from_f(float v) { return v; }
+};
+template <> struct St<bf16_t> {
+  static constexpr int EPL = 8;
+  __device__ static __forceinline__ float to_f(bf16_t v) { return bf2f(v); }
+  __device__ static __forceinline__ bf16_t from_f(float v) { return f2bf(v); }
+};
+
+// acc[16x16] += A[16 x KC] * B[KC x 16], A/B given as one lane vector each in the
+// matrix-core layout: lane l holds row (l % 16) and the EPL consecutive k values of
+// lane group (l / 16).  The k order inside a fragment only has to agree between A
+// and B, which the packed layouts guarantee.
+__device__ __forceinline__ f32x4_t mma_frag(u32x4_t a, u32x4_t b, f32x4_t c, bf16_t) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4_t mma_frag(u32x4_t a, u32x4_t b, f32x4_t c, float) {
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[0]), __uint_as_float(b[0]), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[1]), __uint_as_float(b[1]), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[2]), __uint_as_float(b[2]), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[3]), __uint_as_float(b[3]), c, 0, 0, 0);
+  return c;
+}
+
+// ---- packed weight layout ----------------------------------------------------------
+// W[N][K] row-major is stored as fragments (tile t = n/16, chunk c = k/KC) of 64 lanes
+// x EPL elements; lane = n%16 + 16 * ((k%KC)/EPL), element = k%EPL.
+__host__ __device__ __forceinline__ size_t packed_index(int n, int k, int nchunks, int EPL) {
+  const int KC = 4 * EPL;
+  const int t = n >> 4, c = k / KC, q = k % KC;
+  const int lane = (n & 15) + 16 * (q / EPL);
+  return (((size_t)t * nchunks + c) * 64 + lane) * EPL + (q % EPL);
+}
+
+// ---- paged KV cache layout --------------------------------------------------------
+// Pool per layer: [n_blocks][n_kv][16 keys * hd].  Inside a block:
+//  K: fragment order for the score product (keys are matrix rows): chunk c = d/KC,
+//     lane = key + 16*((d%KC)/EPL), element d%EPL.
+//  V: per 16-column tile nt = d/16: [g = key/4][i = d%16][e = key%4], so one lane
+//     reads the 4 keys of its group for one column.
+__device__ __forceinline__ int kblk_off(int key, int d, int EPL) {
+  const int KC = 4 * EPL;
+  const int c = d / KC, q = d % KC;
+  return (c * 64 + key + 16 * (q / EPL)) * EPL + (q % EPL);
+}
+__device__ __forceinline__ int vblk_off(int key, int d) {
+  const int nt = d >> 4, i = d & 15, g = key >> 2, e = key & 3;
+  return ((nt * 4 + g) * 16 + i) * 4 + e;
+}
+__device__ __forceinline__ size_t kv_block_base(const int* block_table, int max_blocks, int seq,
+                                                int slot, int kvh, int n_kv, int hd) {
+  const int blk = block_table[(size_t)seq * max_blocks + (slot >> 4)];
+  return ((size_t)blk * n_kv + kvh) * (size_t)(16 * hd);
+}
+
+__device__ __forceinline__ float warp_sum(float v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ float warp_max(float v) {
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ float silu_f(float x) { return x / (1.0f + __expf(-x)); }

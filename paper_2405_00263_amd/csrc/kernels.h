@@ -1,0 +1,156 @@
+// Host-side launch interfaces of the Clover gfx950 kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace clover {
+
+// ---- weight-streaming GEMM ------------------------------------------------------------
+enum GemmEpilogue : int {
+  EP_F32 = 0,     // out_f[m][n] = y
+  EP_RESID = 1,   // out_f[m][n] = resid[m][n] + y ; out_s (optional) = storage copy
+  EP_QKV = 2,     // rotary on q/k, q -> qbuf, k/v -> paged KV cache
+  EP_SWIGLU = 3,  // out_s[m][j] = silu(gate) * up  (gate/up tiles paired per group)
+  EP_HEAD = 4,    // out_f[m][n] = resid[m][n] + silu(y + bias[n]); out_s optional copy
+};
+
+struct GemmSeg {
+  const void* w;  // packed weight
+  int tiles;      // 16-row tiles in this segment
+};
+
+struct GemmParams {
+  const void* X;  // [M][ldx] storage type
+  int ldx, M, K, nchunks;
+  GemmSeg seg[3];
+  int nseg, ntiles, N;
+  int ngroups, mchunks, S, cps;
+  float* part;
+  int* sem;
+  int mode;
+  float* out_f; int ldo;
+  void* out_s; int ldos;
+  const float* resid; int ldr;
+  const void* bias;
+  // EP_QKV
+  void* qbuf; int ldq;
+  void* kcache; void* vcache;
+  const int* row_seq; const int* row_slot; const int* row_pos;
+  const int* block_table; int max_blocks;
+  int n_heads, n_kv, hd;
+  float theta;
+};
+
+struct GemmPlan {
+  int mt;        // m-tiles of 16 rows per chunk (1, 2 or 4)
+  int mchunks, ngroups, S, cps;
+  size_t lds_bytes;
+  size_t part_floats;
+};
+
+GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu);
+// Fills plan fields of p and launches; returns hipSuccess or an error.
+hipError_t launch_gemm(int dtype, GemmParams& p, hipStream_t st);
+hipError_t launch_pack(int dtype, const void* src, int rows, int cols, void* dst, hipStream_t st);
+size_t packed_matrix_bytes(int dtype, int rows, int cols);
+
+// ---- attention -------------------------------------------------------------------------
+struct AttnParams {
+  const void* Q; int ldq;          // rows [M][n_heads*hd] storage
+  void* O; int ldo;                // output rows, storage
+  const void* kcache; const void* vcache;
+  const int* block_table; int max_blocks;
+  const int* seq_ids;              // batch index -> sequence slot
+  const int* prefix_dev;           // per slot committed length (or null)
+  int prefix_host;                 // used when prefix_dev is null
+  int rows_per_seq;                // query rows of one sequence in Q (T or chunk)
+  int nq;                          // valid query rows per sequence
+  int n_tail;                      // tail keys (slots prefix .. prefix+n_tail-1)
+  int causal;                      // tail mask: causal (1) or tree bitmask (0)
+  const uint64_t* mask; int mask_words; int mask_seq_stride;  // per slot [T][words]
+  int n_heads, n_kv, hd;
+  int nbatch, qtiles, splits, blocks_per_split;
+  float* part; int* sem;
+};
+hipError_t launch_attention(int dtype, AttnParams& p, int max_keys, hipStream_t st);
+// write rows [n][n_kv*hd] (storage) of K and V into the paged cache at slots slot0.. of seq
+hipError_t launch_kv_write(int dtype, const void* K, const void* V, int n, int slot0, int seq,
+                           void* kcache, void* vcache, const int* block_table, int max_blocks,
+                           int n_kv, int hd, hipStream_t st);
+size_t attention_part_floats(int nbatch, int qtiles, int n_heads, int splits, int hd);
+void plan_attention(AttnParams& p, int max_keys);
+
+// ---- row kernels -------------------------------------------------------------------------
+hipError_t launch_embed(int dtype, const void* emb, const int* tok, int M, int d, float* x,
+                        hipStream_t st);
+hipError_t launch_rmsnorm(int dtype, const float* x, int ldx, int M, int d, const void* g,
+                          float eps, void* out, int ldo, float* copy, hipStream_t st);
+hipError_t launch_argmax(const float* logits, int M, int V, int* out, hipStream_t st);
+// top-k of rows with log-softmax; writes either plain (tok/logp [M][k]) or candidate
+// records (children of frontier rows).
+struct TopkParams {
+  const float* logits; int M, V, k;
+  int* tok; float* logp;                          // plain output (may be null)
+  // candidate output: frontier row f = b*F + fl, children at cand index base_child + fl*k + r
+  const int* seq_ids; int F;
+  int* cand_token; int* cand_parent; int* cand_depth; float* cand_lp; int cand_stride;
+  int base_parent, base_child, depth;
+};
+hipError_t launch_topk(TopkParams& p, hipStream_t st);
+
+struct AdPrepParams {
+  // frontier row f = b*F + fl of depth j; parent state row = prev[b*Fprev + fl/kprev]
+  const float* prev; int Fprev, kprev;   // prev = per-slot h0 when j == 1 (indexed by slot)
+  int use_slot_state;                    // 1: prev indexed by seq slot (h0), 0: by batch row
+  const int* seq_ids; int nbatch, F;
+  const int* cand_token; int cand_stride, base_node;
+  const void* lm_packed; int lm_nchunks;
+  const void* ad_norm; float eps; int d;
+  float* hin; void* a_out; void* e_out;
+};
+hipError_t launch_ad_prep(int dtype, AdPrepParams& p, hipStream_t st);
+hipError_t launch_ad_attn(int dtype, const float* q, const float* kv, int M, int n_heads, int hd,
+                          void* out, hipStream_t st);
+
+// ---- tree, acceptance, compaction -----------------------------------------------------------
+struct TreeParams {
+  const int* seq_ids; int nbatch;
+  const int* cand_token; const int* cand_parent; const int* cand_depth; const float* cand_lp;
+  int cand_stride, n_cand;  // n_cand includes the root
+  int T, mask_words;
+  const int* seq_len;       // per slot (or null: seq_len_host)
+  int seq_len_host;
+  int* tree_token; int* tree_parent; int* tree_depth; int* tree_pos; uint64_t* tree_mask;
+  int* row_tok; int* row_pos; int* row_slot; int* row_seq;   // verify rows [nbatch*T] (optional)
+};
+hipError_t launch_tree_build(TreeParams& p, hipStream_t st);
+
+struct AcceptParams {
+  const int* seq_ids; int nbatch, T, H;
+  const int* tree_token; const int* tree_parent; const int* target;  // target rows [nbatch*T]
+  int* acc; int* acc_len; int* out_tokens; int* t0;
+  const float* ab_out; int d; float* h0;      // AB output rows [nbatch*T][d]
+  const float* x_last; float* x_keep;          // optional
+};
+hipError_t launch_accept(AcceptParams& p, hipStream_t st);
+
+struct CompactParams {
+  const int* seq_ids; int nbatch, H;
+  const int* acc; const int* acc_len; const int* seq_len;
+  void* const* kpools; void* const* vpools; int nlayers;   // device arrays of pool pointers
+  const int* block_table; int max_blocks;
+  int n_kv, hd;
+};
+hipError_t launch_compact(int dtype, CompactParams& p, hipStream_t st);
+
+hipError_t launch_fill_i32(int* p, int v, size_t n, hipStream_t st);
+// draft root (candidate 0 of each listed slot) from the pending token t0[slot]
+hipError_t launch_set_root(const int* seq_ids, int nbatch, const int* t0, int* cand_token,
+                           int* cand_parent, int* cand_depth, float* cand_lp, int cand_stride,
+                           hipStream_t st);
+// end of prefill: t0[slot] = argmax result, h0[slot] = AB output row
+hipError_t launch_finish_prefill(int slot, const int* amax, const float* ab_row, int d, int* t0,
+                                 float* h0, hipStream_t st);
+
+}  // namespace clover
