@@ -1,0 +1,210 @@
+#!/usr/bin/env python3
+"""Benchmark of one Clover speculate-and-verify step on one MI355X.
+
+Workload (default): the 7B-shape bf16 model (32 layers, d_model 4096, 32 heads of
+128, SwiGLU 11008, vocab 125696) with the Clover speculator (Augmenting Block + 3
+heads), batch 1, a 1024-token uniform-random prompt and a 64-token verify tree
+from per-depth top-k (8, 4, 2).  Weights are random-init N(0, 0.02) drawn on the
+device; nothing here is a trained model, so acceptance is ~1 token per step and
+only per-step costs are comparable to the paper.
+
+A step is one clover_step call: draft (Augmenting Block state, Attention Decoder,
+head MLPs, shared LM head + top-k, tree truncation), the tree-masked verify
+forward, greedy acceptance and KV compaction.  The timed region runs --steps steps
+after --warmup untimed ones, bracketed by device synchronisation.
+
+Prints one JSON line with the throughput (tree tokens verified per second over
+whole steps), the per-phase latencies, the streaming GEMM's achieved HBM
+bandwidth against the 8 TB/s peak (HIP events around every launch in the timed
+region) and the CPU oracle's throughput on a bounded sample of the same workload.
+"""
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "verify-step latency (ms) & tree-tokens/s at 7B shape; weight-stream HBM GB/s vs peak"
+
+
+def _prompt_lengths(cfg):
+    import synth
+    if cfg.batch == 1:
+        return [cfg.prompt_len[0]]
+    return synth.make_prompt_lengths(cfg)
+
+
+def cpu_baseline(cfg, seed=0):
+    """The oracle, as written, on a bounded sample of the workload.
+
+    Sample: one oracle step (draft over all depths, tree truncation, verify, accept,
+    commit) of a 1-layer slice of the workload with a synthetic committed context of
+    the workload's prompt length, plus (n_layers - 1) timings of one oracle decoder
+    layer over the T tree rows against that context; the sum is the oracle's time for
+    one full-depth step.
+    """
+    import numpy as np
+    import synth
+    import oracle
+    from oracle.model import BaseModel
+
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    c1 = cfg.with_(n_layers=1, batch=1)
+    w = synth.make_weights(c1, seed=seed, device="cpu")
+    o = oracle.CloverOracle(c1, w)
+    del w
+    rng = np.random.default_rng(1)
+    L = _prompt_lengths(cfg)[0]
+    prec = o.prec
+    shape = (L, c1.n_kv_heads, c1.head_dim)
+    kv = [(prec.store(rng.standard_normal(shape)), prec.store(rng.standard_normal(shape)))]
+    ab = (prec.store(rng.standard_normal(shape)), prec.store(rng.standard_normal(shape)))
+    st = oracle.SeqState(tokens=list(rng.integers(0, c1.vocab, L)), kv=kv, ab_kv=ab,
+                         h0=rng.standard_normal(c1.d_model), t0=int(rng.integers(0, c1.vocab)))
+    t0 = time.perf_counter()
+    o.step(st)
+    t_step = time.perf_counter() - t0
+    # one decoder layer over the tree rows against the committed context
+    T = cfg.tree_tokens
+    x = rng.standard_normal((T, c1.d_model))
+    pos = L + np.minimum(np.arange(T), 3)
+    mask = oracle.tree_mask([-1] + [0] * (T - 1))
+    t0 = time.perf_counter()
+    o.base.run_layer(o.base.layers[0], x, pos, kv[0][0], kv[0][1], mask)
+    t_layer = time.perf_counter() - t0
+    total = t_step + (cfg.n_layers - 1) * t_layer
+    return {
+        "value": round(cfg.batch * T / total, 4),
+        "unit": "tree-tokens/s",
+        "cores": int(cores),
+        "kind": "oracle",
+        "sample": (f"one oracle step of a 1-layer slice of {cfg.name} (T={T}, context {L}) "
+                   f"{t_step:.2f}s + {cfg.n_layers - 1} x one oracle decoder layer over the "
+                   f"{T} tree rows {t_layer:.2f}s = {total:.2f}s per full step (float64 NumPy)"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama7b_b1")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-kernel-timing", action="store_true",
+                    help="do not time each launch with HIP events (no roofline figure)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "
+              "(each sequence is independent, so more GPUs would each run their own batch)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    import paper_2405_00263_amd as P
+
+    cfg = synth.get_config(args.workload)
+    torch.cuda.set_device(0)
+    lens = _prompt_lengths(cfg)
+    H1 = cfg.n_spec_heads + 1
+    max_context = max(lens) + (args.warmup + args.steps) * H1 + cfg.tree_tokens + 16
+    print(f"[bench] workload {cfg.name}: generating weights on device", file=sys.stderr, flush=True)
+    w = synth.make_weights(cfg, seed=args.seed, device="cuda")
+    eng = P.CloverEngine(cfg, w, max_batch=cfg.batch, max_context=max_context,
+                         flags=0 if args.no_kernel_timing else P.FLAG_PROFILE, free_source=True)
+    del w
+    torch.cuda.empty_cache()
+    seqs = list(range(cfg.batch))
+    for b in seqs:
+        eng.prefill(b, synth.make_prompt(cfg, seq=b, n=lens[b]))
+    ctx_start = [eng.seq_len(b) for b in seqs]
+    print(f"[bench] prefill done (context {ctx_start}); warmup {args.warmup} steps",
+          file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        eng.step(seqs)
+    eng.reset_kernel_stats()
+    phase = {"draft_ms": [], "verify_ms": [], "accept_ms": [], "total_ms": []}
+    emitted = 0
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        out = eng.step(seqs)
+        emitted += sum(len(o) for o in out)
+        tm = eng.timings()
+        for k in phase:
+            phase[k].append(tm[k])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = 1e3 * elapsed / args.steps
+    T = cfg.tree_tokens
+    value = cfg.batch * T * args.steps / elapsed
+    ks = eng.kernel_stats()
+    g = ks["gemm_verify"]
+    achieved = g["bytes"] / (g["total_ms"] * 1e-3) / 1e9 if g["total_ms"] > 0 else 0.0
+    med = {k: statistics.median(v) for k, v in phase.items()}
+    # weight bytes streamed by one verify forward (layers + Augmenting Block + LM head)
+    es = 2 if cfg.dtype == "bf16" else 4
+    d, F, V = cfg.d_model, cfg.ffn_dim, cfg.vocab
+    qd, kvd = cfg.n_heads * cfg.head_dim, cfg.n_kv_heads * cfg.head_dim
+    layer_w = (qd * d + 2 * kvd * d + d * qd + 3 * F * d) * es
+    verify_wbytes = (cfg.n_layers + 1) * layer_w + V * d * es
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "tree-tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic: random-init N(0,0.02) weights, uniform-random prompt tokens",
+        "config": {"workload": cfg.name, "n_layers": cfg.n_layers, "d_model": d,
+                   "n_heads": cfg.n_heads, "n_kv_heads": cfg.n_kv_heads, "head_dim": cfg.head_dim,
+                   "ffn_dim": F, "vocab": V, "spec_heads": cfg.n_spec_heads, "topk": list(cfg.topk),
+                   "batch": cfg.batch, "tree_tokens": T, "prompt_len": lens,
+                   "context_at_timed_start": [c + args.warmup for c in ctx_start]},
+        "verify_ms": round(med["verify_ms"], 4),
+        "draft_ms": round(med["draft_ms"], 4),
+        "accept_ms": round(med["accept_ms"], 4),
+        "step_ms_events": round(med["total_ms"], 4),
+        "verify_weight_GBps": round(verify_wbytes / (med["verify_ms"] * 1e-3) / 1e9, 1),
+        "tokens_emitted_per_step": round(emitted / (args.steps * cfg.batch), 3),
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "kernel": "gemm_kernel (streaming GEMMs of the verify forward)",
+            "launches": g["launches"],
+            "avg_launch_us": round(1e3 * g["total_ms"] / max(g["launches"], 1), 3),
+            "bytes_per_launch": round(g["bytes"] / max(g["launches"], 1)),
+        },
+        "kernel_classes": {k: {"launches": v["launches"], "ms": round(v["total_ms"], 3),
+                               "GBps": round(v["bytes"] / (v["total_ms"] * 1e-3) / 1e9, 1) if v["total_ms"] else None}
+                           for k, v in ks.items()},
+    }
+    eng.close()
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(cfg, args.seed)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

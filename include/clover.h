@@ -69,6 +69,7 @@ typedef struct {
 } clover_config;
 
 #define CLOVER_FLAG_KEEP_LOGITS 1 /* keep draft and verify logits of the last step readable */
+#define CLOVER_FLAG_PROFILE 2     /* time every kernel launch with HIP events (clover_kernel_stats) */
 
 typedef struct clover_ctx clover_ctx;
 
@@ -171,6 +172,26 @@ typedef struct {
 } clover_timings;
 clover_status clover_get_timings(clover_ctx* ctx, clover_timings* out);
 
+/* Per-kernel-class statistics accumulated over steps while CLOVER_FLAG_PROFILE is
+ * set: launches, summed launch durations (HIP events on the context's stream) and the
+ * algorithmic bytes and flops those launches must move and compute (each weight,
+ * activation and output byte counted once).  Classes: */
+enum {
+  CLOVER_KSTAT_GEMM_VERIFY = 0, /* streaming GEMMs of the verify forward (layers, AB, LM head) */
+  CLOVER_KSTAT_GEMM_DRAFT = 1,  /* streaming GEMMs of the Clover heads */
+  CLOVER_KSTAT_ATTENTION = 2,   /* tree attention of the verify forward */
+  CLOVER_KSTAT_OTHER = 3,       /* norms, embeddings, reductions, tree, acceptance */
+  CLOVER_KSTAT_COUNT = 4
+};
+typedef struct {
+  int64_t launches;
+  double total_ms;
+  double bytes;
+  double flops;
+} clover_kernel_stats;
+clover_status clover_kernel_stats_get(clover_ctx* ctx, int32_t kind, clover_kernel_stats* out);
+clover_status clover_kernel_stats_reset(clover_ctx* ctx);
+
 /* ---- single-kernel entry points (parity tests at full size) ---------------------------
  * Each runs one hot-path kernel on caller buffers.  scratch: device memory of at least
  * scratch_bytes bytes (clover_op_scratch_bytes gives a sufficient size).  dtype is
@@ -201,13 +222,16 @@ clover_status clover_op_attention(int32_t dtype, const void* Q, const void* Kpre
                                   int32_t n_heads, int32_t n_kv, int32_t head_dim, void* O,
                                   void* scratch, size_t scratch_bytes, void* hip_stream);
 
-/* Per-row argmax (lowest index on ties) of f32 logits [M][V] -> out[M] int32 (device). */
-clover_status clover_op_argmax(const float* logits, int32_t M, int32_t V, int32_t* out,
+/* Per-row argmax (lowest index on ties) of f32 logits [M][V] -> out[M] int32 (device).
+ * scratch: device memory of at least 8*M bytes. */
+clover_status clover_op_argmax(const float* logits, int32_t M, int32_t V, int32_t* out, void* scratch,
                                void* hip_stream);
 /* Per-row top-k by (value desc, index asc) and log-softmax: tok[M][k] int32,
- * logp[M][k] f32 = logits - logsumexp(row) (device). */
+ * logp[M][k] f32 = logits - logsumexp(row) (device); scratch of
+ * clover_op_topk_scratch_bytes(M, V, k) bytes (0 = invalid arguments). */
+size_t clover_op_topk_scratch_bytes(int32_t M, int32_t V, int32_t k);
 clover_status clover_op_topk(const float* logits, int32_t M, int32_t V, int32_t k, int32_t* tok,
-                             float* logp, void* hip_stream);
+                             float* logp, void* scratch, void* hip_stream);
 
 /* Tree truncation (device arrays for one sequence): keep the T-1 best non-root
  * candidates by (lp desc, depth asc, index asc), list root + kept in creation

@@ -184,7 +184,7 @@ class VerifyOut:
 class CloverOracle:
     def __init__(self, cfg, weights):
         self.cfg = cfg
-        self.w = {k: np.asarray(v.float().numpy() if hasattr(v, "float") else v, dtype=np.float64)
+        self.w = {k: (v.double().numpy() if hasattr(v, "double") else np.asarray(v, dtype=np.float64))
                   for k, v in weights.items()}
         self.base = BaseModel(cfg, self.w)
         self.prec = self.base.prec

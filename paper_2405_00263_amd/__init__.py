@@ -16,6 +16,8 @@ LIB_PATH = os.path.join(_HERE, "libclover.so")
 MAX_HEADS = 8
 STATUS = {0: "OK", 1: "INVALID_ARG", 2: "CAPACITY", 3: "STATE", 4: "BAD_TREE", 5: "DEVICE"}
 FLAG_KEEP_LOGITS = 1
+FLAG_PROFILE = 2
+KSTAT = {"gemm_verify": 0, "gemm_draft": 1, "attention": 2, "other": 3}
 
 
 class CloverError(RuntimeError):
@@ -42,6 +44,11 @@ class TimingsC(ctypes.Structure):
                 ("steps", ctypes.c_int32)]
 
 
+class KernelStatsC(ctypes.Structure):
+    _fields_ = [("launches", ctypes.c_int64), ("total_ms", ctypes.c_double),
+                ("bytes", ctypes.c_double), ("flops", ctypes.c_double)]
+
+
 _lib = None
 
 EXPORTS = {
@@ -64,14 +71,17 @@ EXPORTS = {
     "clover_debug_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_char_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "clover_debug_kv": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p]),
     "clover_get_timings": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p]),
+    "clover_kernel_stats_get": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p]),
+    "clover_kernel_stats_reset": (ctypes.c_int, [ctypes.c_void_p]),
     "clover_op_scratch_bytes": (ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
     "clover_op_linear": (ctypes.c_int, [ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "clover_packed_matrix_bytes": (ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
     "clover_pack_matrix": (ctypes.c_int, [ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]),
     "clover_op_attention_scratch_bytes": (ctypes.c_size_t, [ctypes.c_int32] * 6),
     "clover_op_attention": (ctypes.c_int, [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
-    "clover_op_argmax": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]),
-    "clover_op_topk": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
+    "clover_op_argmax": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
+    "clover_op_topk_scratch_bytes": (ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
+    "clover_op_topk": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     "clover_op_tree_build": (ctypes.c_int, [ctypes.c_void_p] * 4 + [ctypes.c_int32] * 3 + [ctypes.c_void_p] * 6),
     "clover_op_accept": (ctypes.c_int, [ctypes.c_void_p] * 3 + [ctypes.c_int32] * 2 + [ctypes.c_void_p] * 4),
 }
@@ -251,6 +261,17 @@ class CloverEngine:
         return dict(draft_ms=t.draft_ms, verify_ms=t.verify_ms, accept_ms=t.accept_ms,
                     total_ms=t.total_ms, steps=t.steps)
 
+    def kernel_stats(self) -> dict:
+        out = {}
+        for name, k in KSTAT.items():
+            st = KernelStatsC()
+            _check(lib().clover_kernel_stats_get(self.ctx, k, ctypes.byref(st)), self.ctx)
+            out[name] = dict(launches=st.launches, total_ms=st.total_ms, bytes=st.bytes, flops=st.flops)
+        return out
+
+    def reset_kernel_stats(self):
+        _check(lib().clover_kernel_stats_reset(self.ctx), self.ctx)
+
     def close(self):
         if getattr(self, "ctx", None) and self.ctx.value:
             lib().clover_destroy(self.ctx)
@@ -321,7 +342,9 @@ def op_argmax(logits):
     import torch
     M, V = logits.shape
     out = torch.empty(M, dtype=torch.int32, device=logits.device)
-    _check(lib().clover_op_argmax(_ptr(logits.contiguous()), M, V, _ptr(out), ctypes.c_void_p(_stream_handle())))
+    keys = torch.empty(M, dtype=torch.int64, device=logits.device)
+    _check(lib().clover_op_argmax(_ptr(logits.contiguous()), M, V, _ptr(out), _ptr(keys),
+                                  ctypes.c_void_p(_stream_handle())))
     return out
 
 
@@ -330,7 +353,11 @@ def op_topk(logits, k: int):
     M, V = logits.shape
     tok = torch.empty(M, k, dtype=torch.int32, device=logits.device)
     logp = torch.empty(M, k, dtype=torch.float32, device=logits.device)
-    _check(lib().clover_op_topk(_ptr(logits.contiguous()), M, V, k, _ptr(tok), _ptr(logp),
+    need = lib().clover_op_topk_scratch_bytes(M, V, k)
+    if need == 0:
+        _check(1)
+    scratch = torch.empty(need, dtype=torch.uint8, device=logits.device)
+    _check(lib().clover_op_topk(_ptr(logits.contiguous()), M, V, k, _ptr(tok), _ptr(logp), _ptr(scratch),
                                 ctypes.c_void_p(_stream_handle())))
     return tok, logp
 

@@ -39,6 +39,7 @@ void set_global_err(const char* fmt, ...) {
 }
 
 constexpr size_t ALIGN = 256;
+constexpr int GEMM_MAX_SPLITS = 8;
 size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 int es_of(int dtype) { return dtype == CLOVER_BF16 ? 2 : 4; }
@@ -144,18 +145,10 @@ struct Layout {
   size_t tree_token, tree_parent, tree_depth, tree_pos, tree_mask, target, acc, acc_len, out_tokens;
   size_t dstate[CLOVER_MAX_HEADS], dlogits[CLOVER_MAX_HEADS];
   size_t d_hin, d_a, d_e, d_q, d_kv, d_o, d_sst, d_r, d_rn;
-  size_t gpart, gsem, apart, asem;
-  size_t gpart_floats, gsem_n, apart_floats, asem_n;
+  size_t gpart, gpart2, amax_keys, topk_scratch;
+  size_t gpart_floats, gpart2_floats;
   size_t total;
 };
-
-void gemm_need(const clover_config& c, int M, int ntiles, int nchunks, bool swiglu, size_t& pf,
-               size_t& sems) {
-  if (M <= 0) return;
-  GemmPlan pl = plan_gemm(c.dtype, M, ntiles, nchunks, swiglu);
-  pf = std::max(pf, pl.part_floats);
-  sems = std::max(sems, (size_t)pl.ngroups * pl.mchunks);
-}
 
 Layout make_layout(const clover_config& c) {
   Layout L{};
@@ -231,59 +224,15 @@ Layout make_layout(const clover_config& c) {
   L.d_sst = take((size_t)L.es * fr * d);
   L.d_r = take(4 * fr * d);
   L.d_rn = take((size_t)L.es * fr * d);
-  // split-K partials: every GEMM shape the context launches
-  const int kc = kc_of(c.dtype);
-  size_t pf = 0, sems = 0;
-  for (int M : {L.Mv, L.Mp, 1}) {
-    gemm_need(c, M, (int)((qd + 2 * kvd) / 16), (int)(d / kc), false, pf, sems);
-    gemm_need(c, M, (int)(d / 16), (int)(qd / kc), false, pf, sems);
-    gemm_need(c, M, (int)(2 * F / 16), (int)(d / kc), true, pf, sems);
-    gemm_need(c, M, (int)(d / 16), (int)(F / kc), false, pf, sems);
-    gemm_need(c, M, (int)(V / 16), (int)(d / kc), false, pf, sems);
-  }
-  for (int j = 1; j <= L.H; ++j) {
-    const int M = c.max_batch * frontier(c, j);
-    for (int m = 1; m <= M; ++m) {
-      gemm_need(c, m, (int)(qd / 16), (int)(d / kc), false, pf, sems);
-      gemm_need(c, m, (int)(2 * qd / 16), (int)(d / kc), false, pf, sems);
-      gemm_need(c, m, (int)(d / 16), (int)(qd / kc), false, pf, sems);
-      gemm_need(c, m, (int)(d / 16), (int)(d / kc), false, pf, sems);
-      gemm_need(c, m, (int)(V / 16), (int)(d / kc), false, pf, sems);
-    }
-  }
-  for (int M = 1; M <= L.Mv; ++M) {  // verify with any number of active sequences
-    if (M % L.T) continue;
-    gemm_need(c, M, (int)((qd + 2 * kvd) / 16), (int)(d / kc), false, pf, sems);
-    gemm_need(c, M, (int)(d / 16), (int)(qd / kc), false, pf, sems);
-    gemm_need(c, M, (int)(2 * F / 16), (int)(d / kc), true, pf, sems);
-    gemm_need(c, M, (int)(d / 16), (int)(F / kc), false, pf, sems);
-    gemm_need(c, M, (int)(V / 16), (int)(d / kc), false, pf, sems);
-  }
-  for (int M = 1; M <= L.Mp; ++M) {  // prefill chunks of any length
-    gemm_need(c, M, (int)((qd + 2 * kvd) / 16), (int)(d / kc), false, pf, sems);
-    gemm_need(c, M, (int)(d / 16), (int)(qd / kc), false, pf, sems);
-    gemm_need(c, M, (int)(2 * F / 16), (int)(d / kc), true, pf, sems);
-    gemm_need(c, M, (int)(d / 16), (int)(F / kc), false, pf, sems);
-  }
-  L.gpart_floats = pf;
-  L.gsem_n = std::max<size_t>(sems, 1);
-  L.gpart = take(4 * pf);
-  L.gsem = take(4 * L.gsem_n);
-  // attention partials: worst case over batch sizes and prefill
-  size_t apf = 0, asn = 1;
-  auto att_need = [&](int nbatch, int nq, int max_keys) {
-    AttnParams a{};
-    a.nbatch = nbatch; a.nq = nq; a.n_heads = c.n_heads;
-    plan_attention(a, max_keys);
-    apf = std::max(apf, attention_part_floats(nbatch, a.qtiles, c.n_heads, a.splits, c.head_dim));
-    asn = std::max(asn, (size_t)nbatch * a.qtiles * c.n_heads);
-  };
-  for (int b = 1; b <= c.max_batch; ++b) att_need(b, L.T, c.max_context);
-  for (int nq = 1; nq <= L.Mp; nq += 1) att_need(1, nq, c.max_context);
-  L.apart_floats = apf;
-  L.asem_n = asn;
-  L.apart = take(4 * apf);
-  L.asem = take(4 * asn);
+  // split-K partials [S][M][N] of the residual-type GEMMs (at most GEMM_MAX_SPLITS)
+  const size_t maxM = std::max<size_t>({(size_t)L.Mv, (size_t)L.Mp, (size_t)L.Fmaxrows});
+  const size_t maxN = std::max<size_t>({(size_t)d, (size_t)qd});
+  L.gpart_floats = (size_t)GEMM_MAX_SPLITS * maxM * maxN;
+  L.gpart2_floats = (size_t)GEMM_MAX_SPLITS * L.Fmaxrows * 2 * qd;  // Attention Decoder keys/values
+  L.gpart = take(4 * L.gpart_floats);
+  L.gpart2 = take(4 * L.gpart2_floats);
+  L.amax_keys = take(8 * (size_t)L.Mv);
+  L.topk_scratch = take(4 * topk_scratch_floats(L.Fmaxrows, (int)V, 16));
   L.total = off;
   return L;
 }
@@ -316,6 +265,13 @@ struct clover_ctx {
   hipEvent_t ev[4];
   clover_timings tim{};
   int last_nbatch = 0;
+  // per-launch profiling (CLOVER_FLAG_PROFILE)
+  bool profile = false, in_step = false;
+  int phase = CLOVER_KSTAT_GEMM_VERIFY;
+  std::vector<hipEvent_t> pev;
+  struct Pending { int kind; size_t ev; double bytes, flops; };
+  std::vector<Pending> pend;
+  clover_kernel_stats kst[CLOVER_KSTAT_COUNT]{};
 
   template <typename T> T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
 };
@@ -332,6 +288,39 @@ clover_status ctx_fail(clover_ctx* c, clover_status s, const char* fmt, ...) {
   return s;
 }
 
+// ---- per-launch timing ---------------------------------------------------------------
+struct ProfScope {
+  clover_ctx* c;
+  bool on;
+  ProfScope(clover_ctx* c_, int kind, double bytes, double flops) : c(c_), on(c_->profile && c_->in_step) {
+    if (!on) return;
+    const size_t i = c->pend.size() * 2;
+    while (c->pev.size() < i + 2) {
+      hipEvent_t e;
+      if (hipEventCreate(&e) != hipSuccess) { on = false; return; }
+      c->pev.push_back(e);
+    }
+    hipEventRecord(c->pev[i], c->st);
+    c->pend.push_back({kind, i, bytes, flops});
+  }
+  ~ProfScope() {
+    if (on) hipEventRecord(c->pev[c->pend.back().ev + 1], c->st);
+  }
+};
+
+void prof_collect(clover_ctx* c) {  // after a stream sync
+  for (auto& p : c->pend) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, c->pev[p.ev], c->pev[p.ev + 1]) != hipSuccess) continue;
+    auto& k = c->kst[p.kind];
+    k.launches += 1;
+    k.total_ms += ms;
+    k.bytes += p.bytes;
+    k.flops += p.flops;
+  }
+  c->pend.clear();
+}
+
 #define HIPCK(ctx, expr)                                                                  \
   do {                                                                                    \
     hipError_t e_ = (expr);                                                               \
@@ -341,10 +330,10 @@ clover_status ctx_fail(clover_ctx* c, clover_status s, const char* fmt, ...) {
     }                                                                                     \
   } while (0)
 
-int gemm_tiles(int n) { return n / 16; }
-
-// Y = X W^T through the streaming GEMM with the given epilogue.
-hipError_t run_gemm(clover_ctx* c, GemmParams p, int M, int K, std::initializer_list<std::pair<const void*, int>> segs) {
+// Y = X W^T through the streaming GEMM.  EP_PARTIAL writes [S][M][N] fp32 partials to
+// `part` (S <= max_splits; the consumer sums them) and returns S through *splits.
+hipError_t run_gemm(clover_ctx* c, GemmParams p, int M, int K,
+                    std::initializer_list<std::pair<const void*, int>> segs, int* splits = nullptr) {
   p.M = M;
   p.K = K;
   p.nchunks = K / kc_of(c->cfg.dtype);
@@ -355,22 +344,43 @@ hipError_t run_gemm(clover_ctx* c, GemmParams p, int M, int K, std::initializer_
     p.ntiles += s.second / 16;
   }
   if (p.mode != EP_SWIGLU) p.N = p.ntiles * 16;
-  p.part = c->at<float>(c->L.gpart);
-  p.sem = c->at<int>(c->L.gsem);
-  return launch_gemm(c->cfg.dtype, p, c->st);
+  const double es = es_of(c->cfg.dtype);
+  const double rows = p.ntiles * 16.0;
+  const double ybytes = (p.mode == EP_PARTIAL ? 4.0 : es) * M * p.N;
+  hipError_t e;
+  {
+    ProfScope ps(c, c->phase, rows * K * es + es * M * K + ybytes, 2.0 * M * rows * K);
+    e = launch_gemm(c->cfg.dtype, p, c->st);
+  }
+  if (splits) *splits = p.S;
+  return e;
 }
 
-// One pre-norm decoder layer over rows of c->x-like buffer `x` (in place).
+// resid_norm: x += sum of pending partials; xn = RMSNorm(x) * gain (storage)
+hipError_t run_rowfix(clover_ctx* c, RowFixParams rp) {
+  ProfScope ps(c, CLOVER_KSTAT_OTHER, 0, 0);
+  return launch_rowfix(c->cfg.dtype, rp, c->st);
+}
+
+// One pre-norm decoder layer over M rows of the residual `x` (in place).  `pend` is the
+// split count of the previous down-projection partials in gpart still to be added to
+// x (0: none); returns through *pend_out the split count of this layer's
+// down-projection partials, which the caller's next row kernel adds.
 hipError_t run_layer(clover_ctx* c, const LayerPtrs& lw, int layer_idx, float* x, int M,
-                     AttnParams att, int max_keys) {
+                     AttnParams att, int max_keys, int pend, int* pend_out) {
   const clover_config& cf = c->cfg;
   const Layout& L = c->L;
   const int d = cf.d_model, hd = cf.head_dim, qd = cf.n_heads * hd, kvd = cf.n_kv_heads * hd;
   void* xn = c->at<void>(L.xn);
+  float* part = c->at<float>(L.gpart);
   void* kp = c->ws + L.kpool + L.pool_bytes * layer_idx;
   void* vp = c->ws + L.vpool + L.pool_bytes * layer_idx;
   hipError_t e;
-  if ((e = launch_rmsnorm(cf.dtype, x, d, M, d, lw.attn_norm, cf.rms_eps, xn, d, nullptr, c->st))) return e;
+  RowFixParams rf{};
+  rf.M = M; rf.d = d; rf.part = part; rf.S = pend; rf.ldp = d;
+  rf.resid = x; rf.ldr = d; rf.out_f = x; rf.ldo = d;
+  rf.gain = lw.attn_norm; rf.eps = cf.rms_eps; rf.out_norm = xn; rf.ldn = d;
+  if ((e = run_rowfix(c, rf))) return e;
   GemmParams g{};
   g.X = xn; g.ldx = d; g.mode = EP_QKV;
   g.qbuf = c->at<void>(L.qbuf); g.ldq = qd;
@@ -384,21 +394,28 @@ hipError_t run_layer(clover_ctx* c, const LayerPtrs& lw, int layer_idx, float* x
   att.kcache = kp; att.vcache = vp;
   att.block_table = c->at<int>(L.block_table); att.max_blocks = L.mbps;
   att.n_heads = cf.n_heads; att.n_kv = cf.n_kv_heads; att.hd = hd;
-  att.part = c->at<float>(L.apart); att.sem = c->at<int>(L.asem);
-  if ((e = launch_attention(cf.dtype, att, max_keys, c->st))) return e;
+  {
+    const double es = L.es;
+    const double keys = (double)max_keys;  // upper bound over the batch
+    ProfScope ps(c, CLOVER_KSTAT_ATTENTION,
+                 att.nbatch * (2.0 * keys * kvd * es + 2.0 * att.nq * qd * es),
+                 att.nbatch * 4.0 * att.nq * keys * hd * cf.n_heads);
+    if ((e = launch_attention(cf.dtype, att, max_keys, c->st))) return e;
+  }
   GemmParams o{};
-  o.X = c->at<void>(L.obuf); o.ldx = qd; o.mode = EP_RESID;
-  o.resid = x; o.ldr = d; o.out_f = x; o.ldo = d;
-  if ((e = run_gemm(c, o, M, qd, {{lw.wo, d}}))) return e;
-  if ((e = launch_rmsnorm(cf.dtype, x, d, M, d, lw.mlp_norm, cf.rms_eps, xn, d, nullptr, c->st))) return e;
+  o.X = c->at<void>(L.obuf); o.ldx = qd; o.mode = EP_PARTIAL; o.max_splits = GEMM_MAX_SPLITS; o.part = part;
+  int so = 0;
+  if ((e = run_gemm(c, o, M, qd, {{lw.wo, d}}, &so))) return e;
+  rf.S = so; rf.gain = lw.mlp_norm;
+  if ((e = run_rowfix(c, rf))) return e;
   GemmParams gu{};
   gu.X = xn; gu.ldx = d; gu.mode = EP_SWIGLU;
   gu.out_s = c->at<void>(L.act); gu.ldos = cf.ffn_dim; gu.N = cf.ffn_dim;
   if ((e = run_gemm(c, gu, M, d, {{lw.wg, cf.ffn_dim}, {lw.wu, cf.ffn_dim}}))) return e;
   GemmParams dn{};
-  dn.X = c->at<void>(L.act); dn.ldx = cf.ffn_dim; dn.mode = EP_RESID;
-  dn.resid = x; dn.ldr = d; dn.out_f = x; dn.ldo = d;
-  return run_gemm(c, dn, M, cf.ffn_dim, {{lw.wd, d}});
+  dn.X = c->at<void>(L.act); dn.ldx = cf.ffn_dim; dn.mode = EP_PARTIAL; dn.max_splits = GEMM_MAX_SPLITS;
+  dn.part = part;
+  return run_gemm(c, dn, M, cf.ffn_dim, {{lw.wd, d}}, pend_out);
 }
 
 clover_status ensure_blocks(clover_ctx* c, int slot, int upto) {
@@ -434,16 +451,30 @@ clover_status verify_accept(clover_ctx* c, int B, int* out_tokens, int* out_coun
   att.rows_per_seq = T; att.nq = T; att.n_tail = T; att.causal = 0;
   att.mask = c->at<uint64_t>(L.tree_mask); att.mask_words = L.W; att.mask_seq_stride = T * L.W;
   att.nbatch = B;
-  for (int l = 0; l < cf.n_layers; ++l) HIPCK(c, run_layer(c, c->layers[l], l, x, M, att, max_keys));
-  // final norm (x_N kept in xa for the Augmenting Block), LM head, greedy argmax
-  HIPCK(c, launch_rmsnorm(cf.dtype, x, d, M, d, c->final_norm, cf.rms_eps, c->at<void>(L.xn), d, xa, c->st));
+  int pend = 0;
+  for (int l = 0; l < cf.n_layers; ++l) HIPCK(c, run_layer(c, c->layers[l], l, x, M, att, max_keys, pend, &pend));
+  // x_N = x + last partials; kept in xa for the Augmenting Block; final norm; LM head; argmax
+  RowFixParams rf{};
+  rf.M = M; rf.d = d; rf.part = c->at<float>(L.gpart); rf.S = pend; rf.ldp = d;
+  rf.resid = x; rf.ldr = d; rf.out_f = x; rf.ldo = d; rf.out_copy_f = xa;
+  rf.gain = c->final_norm; rf.eps = cf.rms_eps; rf.out_norm = c->at<void>(L.xn); rf.ldn = d;
+  rf.zero_keys = c->at<unsigned long long>(L.amax_keys); rf.zero_n = M;
+  HIPCK(c, run_rowfix(c, rf));
   GemmParams lm{};
-  lm.X = c->at<void>(L.xn); lm.ldx = d; lm.mode = EP_F32;
-  lm.out_f = c->at<float>(L.vlogits); lm.ldo = cf.vocab;
+  lm.X = c->at<void>(L.xn); lm.ldx = d; lm.mode = EP_PARTIAL; lm.max_splits = 1;
+  lm.part = c->at<float>(L.vlogits);
   HIPCK(c, run_gemm(c, lm, M, d, {{c->lm_head, cf.vocab}}));
-  HIPCK(c, launch_argmax(c->at<float>(L.vlogits), M, cf.vocab, c->at<int>(L.target), c->st));
+  {
+    ProfScope ps(c, CLOVER_KSTAT_OTHER, 0, 0);
+    HIPCK(c, launch_argmax(c->at<float>(L.vlogits), M, cf.vocab, c->at<int>(L.target),
+                           c->at<unsigned long long>(L.amax_keys), true, c->st));
+  }
   // Augmenting Block over the tree (tree mask, its own KV cache)
-  HIPCK(c, run_layer(c, c->layers[cf.n_layers], cf.n_layers, xa, M, att, max_keys));
+  HIPCK(c, run_layer(c, c->layers[cf.n_layers], cf.n_layers, xa, M, att, max_keys, 0, &pend));
+  RowFixParams ra{};
+  ra.M = M; ra.d = d; ra.part = c->at<float>(L.gpart); ra.S = pend; ra.ldp = d;
+  ra.resid = xa; ra.ldr = d; ra.out_f = xa; ra.ldo = d;
+  HIPCK(c, run_rowfix(c, ra));
   HIPCK(c, hipEventRecord(c->ev[2], c->st));
   AcceptParams ap{};
   ap.seq_ids = c->at<int>(L.seq_ids); ap.nbatch = B; ap.T = T; ap.H = H;
@@ -466,6 +497,7 @@ clover_status verify_accept(clover_ctx* c, int B, int* out_tokens, int* out_coun
                           hipMemcpyDeviceToHost, c->st));
   HIPCK(c, hipEventRecord(c->ev[3], c->st));
   HIPCK(c, hipStreamSynchronize(c->st));
+  prof_collect(c);
   for (int b = 0; b < B; ++b) {
     int n = 0;
     for (int i = 0; i <= H; ++i) {
@@ -584,8 +616,11 @@ clover_status clover_pack_weight(const clover_config* cfg, size_t i, const void*
   }
   hipStream_t st = (hipStream_t)hip_stream;
   hipError_t e;
+  const std::string& nm = s[i].name;
+  const bool qk = nm.rfind("ad.", 0) != 0 && nm.size() > 3 &&
+                  (nm.compare(nm.size() - 3, 3, ".wq") == 0 || nm.compare(nm.size() - 3, 3, ".wk") == 0);
   if (s[i].matrix)
-    e = launch_pack(cfg->dtype, src, (int)s[i].rows, (int)s[i].cols, dst, st);
+    e = launch_pack(cfg->dtype, src, (int)s[i].rows, (int)s[i].cols, dst, qk && cfg->head_dim == 128, st);
   else
     e = hipMemcpyAsync(dst, src, clover_packed_bytes(cfg, i), hipMemcpyDeviceToDevice, st);
   if (e != hipSuccess) {
@@ -643,6 +678,7 @@ clover_status clover_init(const clover_config* cfg, void* const* weights, void* 
     c->head_w1.push_back(c->w[k++]);
     c->head_b1.push_back(c->w[k++]);
   }
+  c->profile = (cfg->flags & CLOVER_FLAG_PROFILE) != 0;
   c->seq_len.assign(cfg->max_batch, -1);
   c->seq_blocks.assign(cfg->max_batch, {});
   for (int b = L.nblocks - 1; b >= 0; --b) c->free_blocks.push_back(b);
@@ -658,8 +694,6 @@ clover_status clover_init(const clover_config* cfg, void* const* weights, void* 
   // zero the KV pools (attention reads whole 16-key blocks), counters and state
   if ((e = hipMemsetAsync(c->ws, 0, L.pool_ptrs, c->st)) != hipSuccess) return fail(e, "memset pools");
   if ((e = hipMemsetAsync(c->ws + L.block_table, 0, L.x - L.block_table, c->st)) != hipSuccess) return fail(e, "memset state");
-  if ((e = hipMemsetAsync(c->ws + L.gsem, 0, 4 * L.gsem_n, c->st)) != hipSuccess) return fail(e, "memset gsem");
-  if ((e = hipMemsetAsync(c->ws + L.asem, 0, 4 * L.asem_n, c->st)) != hipSuccess) return fail(e, "memset asem");
   std::vector<void*> pools(2 * (cfg->n_layers + 1));
   for (int l = 0; l <= cfg->n_layers; ++l) {
     pools[l] = c->ws + L.kpool + L.pool_bytes * l;
@@ -677,6 +711,7 @@ void clover_destroy(clover_ctx* ctx) {
   if (!ctx) return;
   hipStreamSynchronize(ctx->st);
   for (int i = 0; i < 4; ++i) hipEventDestroy(ctx->ev[i]);
+  for (auto e : ctx->pev) hipEventDestroy(e);
   delete ctx;
 }
 
@@ -733,16 +768,28 @@ clover_status clover_prefill(clover_ctx* c, int32_t seq, const int32_t* tokens, 
     att.prefix_dev = nullptr; att.prefix_host = c0;
     att.rows_per_seq = rows; att.nq = rows; att.n_tail = rows; att.causal = 1;
     att.nbatch = 1;
-    for (int l = 0; l < cf.n_layers; ++l) HIPCK(c, run_layer(c, c->layers[l], l, x, rows, att, c0 + rows));
-    HIPCK(c, launch_rmsnorm(cf.dtype, x, d, rows, d, c->final_norm, cf.rms_eps, c->at<void>(L.xn), d, xa, c->st));
+    int pend = 0;
+    for (int l = 0; l < cf.n_layers; ++l)
+      HIPCK(c, run_layer(c, c->layers[l], l, x, rows, att, c0 + rows, pend, &pend));
+    RowFixParams rf{};
+    rf.M = rows; rf.d = d; rf.part = c->at<float>(L.gpart); rf.S = pend; rf.ldp = d;
+    rf.resid = x; rf.ldr = d; rf.out_f = x; rf.ldo = d; rf.out_copy_f = xa;
+    rf.gain = c->final_norm; rf.eps = cf.rms_eps; rf.out_norm = c->at<void>(L.xn); rf.ldn = d;
+    rf.zero_keys = c->at<unsigned long long>(L.amax_keys); rf.zero_n = 1;
+    HIPCK(c, run_rowfix(c, rf));
     if (c0 + rows == n) {
       GemmParams lm{};
-      lm.X = (const char*)c->at<char>(L.xn) + (size_t)(rows - 1) * d * L.es; lm.ldx = d; lm.mode = EP_F32;
-      lm.out_f = c->at<float>(L.vlogits); lm.ldo = cf.vocab;
+      lm.X = (const char*)c->at<char>(L.xn) + (size_t)(rows - 1) * d * L.es; lm.ldx = d;
+      lm.mode = EP_PARTIAL; lm.max_splits = 1; lm.part = c->at<float>(L.vlogits);
       HIPCK(c, run_gemm(c, lm, 1, d, {{c->lm_head, cf.vocab}}));
-      HIPCK(c, launch_argmax(c->at<float>(L.vlogits), 1, cf.vocab, c->at<int>(L.amax), c->st));
+      HIPCK(c, launch_argmax(c->at<float>(L.vlogits), 1, cf.vocab, c->at<int>(L.amax),
+                             c->at<unsigned long long>(L.amax_keys), true, c->st));
     }
-    HIPCK(c, run_layer(c, c->layers[cf.n_layers], cf.n_layers, xa, rows, att, c0 + rows));
+    HIPCK(c, run_layer(c, c->layers[cf.n_layers], cf.n_layers, xa, rows, att, c0 + rows, 0, &pend));
+    RowFixParams ra{};
+    ra.M = rows; ra.d = d; ra.part = c->at<float>(L.gpart); ra.S = pend; ra.ldp = d;
+    ra.resid = xa; ra.ldr = d; ra.out_f = xa; ra.ldo = d;
+    HIPCK(c, run_rowfix(c, ra));
     if (c0 + rows == n)
       HIPCK(c, launch_finish_prefill(seq, c->at<int>(L.amax), xa + (size_t)(rows - 1) * d, d,
                                      c->at<int>(L.t0), c->at<float>(L.h0), c->st));
@@ -768,6 +815,8 @@ clover_status clover_step(clover_ctx* c, const int32_t* seqs, int32_t n_seqs, in
   int max_keys = 0;
   if ((s = begin_batch(c, seqs, B, max_keys))) return s;
   HIPCK(c, hipEventRecord(c->ev[0], c->st));
+  c->in_step = true;
+  c->phase = CLOVER_KSTAT_GEMM_DRAFT;
   int* ids = c->at<int>(L.seq_ids);
   int *ct = c->at<int>(L.cand_token), *cpar = c->at<int>(L.cand_parent), *cd = c->at<int>(L.cand_depth);
   float* clp = c->at<float>(L.cand_lp);
@@ -785,36 +834,44 @@ clover_status clover_step(clover_ctx* c, const int32_t* seqs, int32_t n_seqs, in
     ap.ad_norm = c->ad_norm; ap.eps = cf.rms_eps; ap.d = d;
     ap.hin = c->at<float>(L.d_hin); ap.a_out = c->at<void>(L.d_a); ap.e_out = c->at<void>(L.d_e);
     HIPCK(c, launch_ad_prep(cf.dtype, ap, c->st));
+    float* part = c->at<float>(L.gpart);
+    float* part2 = c->at<float>(L.gpart2);
+    int sq = 0, skv = 0, so = 0, sh = 0;
     GemmParams q{};
-    q.X = c->at<void>(L.d_a); q.ldx = d; q.mode = EP_F32; q.out_f = c->at<float>(L.d_q); q.ldo = qd;
-    HIPCK(c, run_gemm(c, q, M, d, {{c->ad_wq, qd}}));
+    q.X = c->at<void>(L.d_a); q.ldx = d; q.mode = EP_PARTIAL; q.max_splits = GEMM_MAX_SPLITS; q.part = part;
+    HIPCK(c, run_gemm(c, q, M, d, {{c->ad_wq, qd}}, &sq));
     GemmParams kv{};
-    kv.X = c->at<void>(L.d_e); kv.ldx = d; kv.mode = EP_F32; kv.out_f = c->at<float>(L.d_kv); kv.ldo = 2 * qd;
-    HIPCK(c, run_gemm(c, kv, M, d, {{c->ad_wk, qd}, {c->ad_wv, qd}}));
-    HIPCK(c, launch_ad_attn(cf.dtype, c->at<float>(L.d_q), c->at<float>(L.d_kv), M, cf.n_heads,
-                            cf.head_dim, c->at<void>(L.d_o), c->st));
+    kv.X = c->at<void>(L.d_e); kv.ldx = d; kv.mode = EP_PARTIAL; kv.max_splits = GEMM_MAX_SPLITS; kv.part = part2;
+    HIPCK(c, run_gemm(c, kv, M, d, {{c->ad_wk, qd}, {c->ad_wv, qd}}, &skv));
+    HIPCK(c, launch_ad_attn(cf.dtype, part, sq, part2, skv, M, cf.n_heads, cf.head_dim,
+                            c->at<void>(L.d_o), c->st));
     GemmParams o{};
-    o.X = c->at<void>(L.d_o); o.ldx = qd; o.mode = EP_RESID;
-    o.resid = c->at<float>(L.d_hin); o.ldr = d;
-    o.out_f = c->at<float>(L.dstate[j - 1]); o.ldo = d;
-    o.out_s = c->at<void>(L.d_sst); o.ldos = d;
-    HIPCK(c, run_gemm(c, o, M, qd, {{c->ad_wo, d}}));
+    o.X = c->at<void>(L.d_o); o.ldx = qd; o.mode = EP_PARTIAL; o.max_splits = GEMM_MAX_SPLITS; o.part = part;
+    HIPCK(c, run_gemm(c, o, M, qd, {{c->ad_wo, d}}, &so));
+    RowFixParams rs{};  // s = h + W_O attn (Eq. 2): fp32 state and storage copy for the MLP
+    rs.M = M; rs.d = d; rs.part = part; rs.S = so; rs.ldp = d;
+    rs.resid = c->at<float>(L.d_hin); rs.ldr = d;
+    rs.out_f = c->at<float>(L.dstate[j - 1]); rs.ldo = d; rs.out_copy_s = c->at<void>(L.d_sst);
+    HIPCK(c, run_rowfix(c, rs));
     GemmParams hm{};
-    hm.X = c->at<void>(L.d_sst); hm.ldx = d; hm.mode = EP_HEAD;
-    hm.resid = c->at<float>(L.dstate[j - 1]); hm.ldr = d; hm.bias = c->head_b1[j - 1];
-    hm.out_f = c->at<float>(L.d_r); hm.ldo = d;
-    HIPCK(c, run_gemm(c, hm, M, d, {{c->head_w1[j - 1], d}}));
-    HIPCK(c, launch_rmsnorm(cf.dtype, c->at<float>(L.d_r), d, M, d, c->final_norm, cf.rms_eps,
-                            c->at<void>(L.d_rn), d, nullptr, c->st));
+    hm.X = c->at<void>(L.d_sst); hm.ldx = d; hm.mode = EP_PARTIAL; hm.max_splits = GEMM_MAX_SPLITS; hm.part = part;
+    HIPCK(c, run_gemm(c, hm, M, d, {{c->head_w1[j - 1], d}}, &sh));
+    RowFixParams rh{};  // r = s + SiLU(W1 s + b1), then the shared final norm
+    rh.M = M; rh.d = d; rh.part = part; rh.S = sh; rh.ldp = d;
+    rh.resid = c->at<float>(L.dstate[j - 1]); rh.ldr = d; rh.act = 1; rh.bias = c->head_b1[j - 1];
+    rh.out_f = c->at<float>(L.d_r); rh.ldo = d;
+    rh.gain = c->final_norm; rh.eps = cf.rms_eps; rh.out_norm = c->at<void>(L.d_rn); rh.ldn = d;
+    HIPCK(c, run_rowfix(c, rh));
     GemmParams lm{};
-    lm.X = c->at<void>(L.d_rn); lm.ldx = d; lm.mode = EP_F32;
-    lm.out_f = c->at<float>(L.dlogits[j - 1]); lm.ldo = cf.vocab;
+    lm.X = c->at<void>(L.d_rn); lm.ldx = d; lm.mode = EP_PARTIAL; lm.max_splits = 1;
+    lm.part = c->at<float>(L.dlogits[j - 1]);
     HIPCK(c, run_gemm(c, lm, M, d, {{c->lm_head, cf.vocab}}));
     TopkParams tp{};
     tp.logits = c->at<float>(L.dlogits[j - 1]); tp.M = M; tp.V = cf.vocab; tp.k = cf.topk[j - 1];
     tp.seq_ids = ids; tp.F = F;
     tp.cand_token = ct; tp.cand_parent = cpar; tp.cand_depth = cd; tp.cand_lp = clp; tp.cand_stride = L.NC;
     tp.base_parent = depth_base(cf, j - 1); tp.base_child = depth_base(cf, j); tp.depth = j;
+    tp.scratch = c->at<float>(L.topk_scratch);
     HIPCK(c, launch_topk(tp, c->st));
   }
   TreeParams tr{};
@@ -830,7 +887,10 @@ clover_status clover_step(clover_ctx* c, const int32_t* seqs, int32_t n_seqs, in
   HIPCK(c, launch_tree_build(tr, c->st));
   HIPCK(c, hipEventRecord(c->ev[1], c->st));
   c->last_nbatch = B;
-  return verify_accept(c, B, out_tokens, out_count, max_keys);
+  c->phase = CLOVER_KSTAT_GEMM_VERIFY;
+  s = verify_accept(c, B, out_tokens, out_count, max_keys);
+  c->in_step = false;
+  return s;
 }
 
 clover_status clover_verify_tree(clover_ctx* c, int32_t seq, const int32_t* tokens,
@@ -893,7 +953,11 @@ clover_status clover_verify_tree(clover_ctx* c, int32_t seq, const int32_t* toke
   HIPCK(c, hipEventRecord(c->ev[0], c->st));
   HIPCK(c, hipEventRecord(c->ev[1], c->st));
   c->last_nbatch = 1;
-  return verify_accept(c, 1, out_tokens, out_count, max_keys);
+  c->in_step = true;
+  c->phase = CLOVER_KSTAT_GEMM_VERIFY;
+  s = verify_accept(c, 1, out_tokens, out_count, max_keys);
+  c->in_step = false;
+  return s;
 }
 
 clover_status clover_debug_read(clover_ctx* c, const char* name, void* host_dst, size_t bytes,
@@ -974,12 +1038,31 @@ clover_status clover_get_timings(clover_ctx* c, clover_timings* out) {
   return CLOVER_OK;
 }
 
+clover_status clover_kernel_stats_get(clover_ctx* c, int32_t kind, clover_kernel_stats* out) {
+  clover_status s = check_ctx(c);
+  if (s) return s;
+  if (!out || kind < 0 || kind >= CLOVER_KSTAT_COUNT) return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "bad kernel class");
+  *out = c->kst[kind];
+  return CLOVER_OK;
+}
+
+clover_status clover_kernel_stats_reset(clover_ctx* c) {
+  clover_status s = check_ctx(c);
+  if (s) return s;
+  for (auto& k : c->kst) k = clover_kernel_stats{};
+  return CLOVER_OK;
+}
+
 // ---- single-kernel entry points --------------------------------------------------------
+
+// N <= 8192: split-K partials reduced by the row kernel (the path residual GEMMs take);
+// wider outputs: one unsplit launch (the LM-head path)
+static int op_linear_splits(int N) { return N <= 8192 ? GEMM_MAX_SPLITS : 1; }
 
 size_t clover_op_scratch_bytes(int32_t dtype, int32_t M, int32_t N, int32_t K) {
   if ((dtype != 0 && dtype != 1) || M < 1 || N < 16 || N % 16 || K < 1 || K % kc_of(dtype)) return 0;
-  GemmPlan pl = plan_gemm(dtype, M, N / 16, K / kc_of(dtype), false);
-  return align_up(4 * pl.part_floats) + align_up(4 * (size_t)pl.ngroups * pl.mchunks);
+  GemmPlan pl = plan_gemm(dtype, M, N / 16, K / kc_of(dtype), false, op_linear_splits(N));
+  return align_up(4 * pl.part_floats) + ALIGN;
 }
 
 size_t clover_packed_matrix_bytes(int32_t dtype, int32_t rows, int32_t cols) {
@@ -993,7 +1076,7 @@ clover_status clover_pack_matrix(int32_t dtype, const void* src, int32_t rows, i
     set_global_err("pack_matrix: bad arguments");
     return CLOVER_ERR_INVALID_ARG;
   }
-  hipError_t e = launch_pack(dtype, src, rows, cols, dst, (hipStream_t)hip_stream);
+  hipError_t e = launch_pack(dtype, src, rows, cols, dst, false, (hipStream_t)hip_stream);
   if (e != hipSuccess) {
     set_global_err("pack_matrix: %s", hipGetErrorString(e));
     return CLOVER_ERR_DEVICE;
@@ -1014,15 +1097,19 @@ clover_status clover_op_linear(int32_t dtype, const void* X, int32_t M, int32_t 
     return CLOVER_ERR_CAPACITY;
   }
   hipStream_t st = (hipStream_t)hip_stream;
-  GemmPlan pl = plan_gemm(dtype, M, N / 16, K / kc_of(dtype), false);
   GemmParams p{};
   p.X = X; p.ldx = K; p.M = M; p.K = K; p.nchunks = K / kc_of(dtype);
   p.seg[0] = GemmSeg{Wp, N / 16}; p.nseg = 1; p.ntiles = N / 16; p.N = N;
-  p.part = (float*)scratch;
-  p.sem = (int*)((char*)scratch + align_up(4 * pl.part_floats));
-  p.mode = EP_F32; p.out_f = Y; p.ldo = N;
-  hipError_t e = hipMemsetAsync(p.sem, 0, 4 * (size_t)pl.ngroups * pl.mchunks, st);
-  if (e == hipSuccess) e = launch_gemm(dtype, p, st);
+  p.mode = EP_PARTIAL;
+  p.max_splits = op_linear_splits(N);
+  p.part = p.max_splits == 1 ? Y : (float*)scratch;
+  hipError_t e = launch_gemm(dtype, p, st);
+  if (e == hipSuccess && p.max_splits > 1) {
+    RowFixParams rf{};
+    rf.M = M; rf.d = N; rf.part = (float*)scratch; rf.S = p.S; rf.ldp = N;
+    rf.out_f = Y; rf.ldo = N;
+    e = launch_rowfix(dtype, rf, st);
+  }
   if (e != hipSuccess) {
     set_global_err("op_linear: %s", hipGetErrorString(e));
     return CLOVER_ERR_DEVICE;
@@ -1043,9 +1130,7 @@ size_t clover_op_attention_scratch_bytes(int32_t dtype, int32_t L, int32_t T, in
   b += align_up((size_t)nblocks * n_kv * 16 * head_dim * es_of(dtype)) * 2;  // K and V pools
   b += align_up(4 * (size_t)nblocks);                                          // block table
   b += align_up(8 * (size_t)T * ((T + 63) / 64));                              // mask
-  b += align_up(4 * 2);                                                        // seq id, prefix
-  b += align_up(4 * attention_part_floats(1, a.qtiles, n_heads, a.splits, head_dim));
-  b += align_up(4 * (size_t)a.qtiles * n_heads);
+  b += align_up(4 * 2);                                                        // seq id
   return b;
 }
 
@@ -1075,9 +1160,6 @@ clover_status clover_op_attention(int32_t dtype, const void* Q, const void* Kpre
   int* ids = (int*)p; p += align_up(8);
   AttnParams a{};
   a.nbatch = 1; a.nq = T; a.n_heads = n_heads;
-  plan_attention(a, L + T);
-  float* part = (float*)p; p += align_up(4 * attention_part_floats(1, a.qtiles, n_heads, a.splits, head_dim));
-  int* sem = (int*)p;
   std::vector<int> hbt(nblocks);
   for (int i = 0; i < nblocks; ++i) hbt[i] = nblocks - 1 - i;  // reversed pages: exercises the table
   std::vector<uint64_t> hm((size_t)T * W, 0);
@@ -1097,7 +1179,6 @@ clover_status clover_op_attention(int32_t dtype, const void* Q, const void* Kpre
   if (!e) e = hipMemcpyAsync(bt, hbt.data(), 4 * nblocks, hipMemcpyHostToDevice, st);
   if (!e) e = hipMemcpyAsync(mask, hm.data(), 8 * hm.size(), hipMemcpyHostToDevice, st);
   if (!e) e = hipMemcpyAsync(ids, &zero, 4, hipMemcpyHostToDevice, st);
-  if (!e) e = hipMemsetAsync(sem, 0, 4 * (size_t)a.qtiles * n_heads, st);
   if (!e && L > 0) e = launch_kv_write(dtype, Kpre, Vpre, L, 0, 0, kp, vp, bt, nblocks, n_kv, head_dim, st);
   if (!e) e = launch_kv_write(dtype, Ktree, Vtree, T, L, 0, kp, vp, bt, nblocks, n_kv, head_dim, st);
   a.Q = Q; a.ldq = n_heads * head_dim; a.O = O; a.ldo = n_heads * head_dim;
@@ -1105,7 +1186,7 @@ clover_status clover_op_attention(int32_t dtype, const void* Q, const void* Kpre
   a.seq_ids = ids; a.prefix_dev = nullptr; a.prefix_host = L;
   a.rows_per_seq = T; a.n_tail = T; a.causal = causal ? 1 : 0;
   a.mask = mask; a.mask_words = W; a.mask_seq_stride = T * W;
-  a.n_kv = n_kv; a.hd = head_dim; a.part = part; a.sem = sem;
+  a.n_kv = n_kv; a.hd = head_dim;
   if (!e) e = launch_attention(dtype, a, L + T, st);
   if (!e) e = hipStreamSynchronize(st);  // host staging vectors die with this call
   if (e != hipSuccess) {
@@ -1115,12 +1196,13 @@ clover_status clover_op_attention(int32_t dtype, const void* Q, const void* Kpre
   return CLOVER_OK;
 }
 
-clover_status clover_op_argmax(const float* logits, int32_t M, int32_t V, int32_t* out, void* hip_stream) {
-  if (!logits || !out || M < 1 || V < 1) {
+clover_status clover_op_argmax(const float* logits, int32_t M, int32_t V, int32_t* out, void* scratch,
+                               void* hip_stream) {
+  if (!logits || !out || !scratch || M < 1 || V < 1) {
     set_global_err("op_argmax: bad arguments");
     return CLOVER_ERR_INVALID_ARG;
   }
-  hipError_t e = launch_argmax(logits, M, V, out, (hipStream_t)hip_stream);
+  hipError_t e = launch_argmax(logits, M, V, out, (unsigned long long*)scratch, false, (hipStream_t)hip_stream);
   if (e != hipSuccess) {
     set_global_err("op_argmax: %s", hipGetErrorString(e));
     return CLOVER_ERR_DEVICE;
@@ -1128,14 +1210,20 @@ clover_status clover_op_argmax(const float* logits, int32_t M, int32_t V, int32_
   return CLOVER_OK;
 }
 
+size_t clover_op_topk_scratch_bytes(int32_t M, int32_t V, int32_t k) {
+  if (M < 1 || V < 1 || k < 1 || k > 16 || V < k) return 0;
+  return 4 * topk_scratch_floats(M, V, k);
+}
+
 clover_status clover_op_topk(const float* logits, int32_t M, int32_t V, int32_t k, int32_t* tok,
-                             float* logp, void* hip_stream) {
-  if (!logits || !tok || !logp || M < 1 || k < 1 || k > 16 || V < k) {
+                             float* logp, void* scratch, void* hip_stream) {
+  if (!logits || !tok || !logp || !scratch || !clover_op_topk_scratch_bytes(M, V, k)) {
     set_global_err("op_topk: bad arguments");
     return CLOVER_ERR_INVALID_ARG;
   }
   TopkParams p{};
   p.logits = logits; p.M = M; p.V = V; p.k = k; p.tok = tok; p.logp = logp;
+  p.scratch = (float*)scratch;
   hipError_t e = launch_topk(p, (hipStream_t)hip_stream);
   if (e != hipSuccess) {
     set_global_err("op_topk: %s", hipGetErrorString(e));

@@ -7,8 +7,7 @@
 // transposed (S^T = K Q^T) so the matrix-core accumulator already holds, per lane,
 // four consecutive keys of one query row: exactly the operand layout the P*V product
 // needs, with no shuffles.  Softmax is online in the log2 domain.  Keys are split over
-// workgroups (split-KV); the last split of a (sequence, head, query tile) combines the
-// partial results in split order.
+// the waves of a workgroup, whose states merge in LDS in wave order.
 #include "common.h"
 #include "kernels.h"
 
@@ -16,8 +15,8 @@
 
 namespace clover {
 
-static constexpr int ATT_THREADS = 256;  // 4 waves x 16 query rows
-static constexpr int ATT_TARGET_WGS = 512;
+static constexpr int ATT_WAVES = 8;              // key splits inside a workgroup
+static constexpr int ATT_THREADS = ATT_WAVES * 64;
 
 __device__ __forceinline__ f32x4_t mma_pv(u32x2_t v, const float p[4], f32x4_t c, bf16_t) {
   u32x2_t pb;
@@ -39,18 +38,42 @@ template <> struct VFrag<bf16_t> { typedef u32x2_t type; };
 template <> struct VFrag<float> { typedef u32x4_t type; };
 
 template <typename S, int HD>
+struct KVBlock {
+  static constexpr int EPL = St<S>::EPL, NQC = HD / (4 * EPL), NT = HD / 16;
+  u32x4_t k[NQC];
+  typename VFrag<S>::type v[NT];
+  __device__ __forceinline__ void load(const S* kc, const S* vc, size_t base, int lane) {
+#pragma unroll
+    for (int c = 0; c < NQC; ++c)
+      k[c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(kc + base + (size_t)(c * 64 + lane) * EPL));
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+      v[t] = __builtin_nontemporal_load(
+          reinterpret_cast<const typename VFrag<S>::type*>(vc + base + (size_t)(t * 64 + lane) * 4));
+  }
+};
+
+// One workgroup = one 16-row query tile of one (sequence, head); its 8 waves take
+// interleaved 16-key blocks and merge their online-softmax states through LDS.
+// Workgroup ids are laid out so all query tiles of one (sequence, head) land on the
+// same XCD (ids are dealt to the 8 XCDs round-robin) and share its L2 copy of K/V.
+template <typename S, int HD>
 __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(const AttnParams p) {
   using T = St<S>;
-  using VT = typename VFrag<S>::type;
   constexpr int EPL = T::EPL, KC = 4 * EPL, NQC = HD / KC, NT = HD / 16;
+  __shared__ float s_m[ATT_WAVES][16], s_l[ATT_WAVES][16];
+  __shared__ float s_o[ATT_WAVES][16][HD + 4];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, j = lane & 15;
-  const int split = blockIdx.x, h = blockIdx.y, bq = blockIdx.z;
-  const int b = bq / p.qtiles, qt = bq % p.qtiles;
+  const int id = blockIdx.x, xcd = id & 7, slotx = id >> 3;
+  const int item = (slotx / p.qtiles) * 8 + xcd, qt = slotx % p.qtiles;
+  if (item >= p.nbatch * p.n_heads) return;
+  const int b = item / p.n_heads, h = item % p.n_heads;
   const int slot = p.seq_ids[b];
   const int P = p.prefix_dev ? p.prefix_dev[slot] : p.prefix_host;
-  const int nkeys = P + p.n_tail;
+  const int tail = p.causal ? min(p.n_tail, qt * 16 + 16) : p.n_tail;
+  const int nkeys = P + tail;
   const int kvh = h / (p.n_heads / p.n_kv);
-  const int row = qt * 64 + wave * 16 + j;
+  const int row = qt * 16 + j;
   const bool valid = row < p.nq;
   const S* Q = reinterpret_cast<const S*>(p.Q);
 
@@ -70,8 +93,6 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(const AttnParams p) {
   }
 
   const int nblocks = (nkeys + 15) >> 4;
-  const int kb0 = split * p.blocks_per_split;
-  const int kb1 = min(nblocks, kb0 + p.blocks_per_split);
   const float scale2 = rsqrtf((float)HD) * 1.4426950408889634f;
   float m_i = -INFINITY, l_i = 0.f;
   f32x4_t o[NT];
@@ -80,21 +101,17 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(const AttnParams p) {
 
   const S* kc = reinterpret_cast<const S*>(p.kcache);
   const S* vc = reinterpret_cast<const S*>(p.vcache);
-  for (int kb = kb0; kb < kb1; ++kb) {
-    const int blk = p.block_table[(size_t)slot * p.max_blocks + kb];
-    const size_t base = ((size_t)blk * p.n_kv + kvh) * (size_t)(16 * HD);
+  const int* bt = p.block_table + (size_t)slot * p.max_blocks;
+  auto base_of = [&](int kb) { return ((size_t)bt[kb] * p.n_kv + kvh) * (size_t)(16 * HD); };
+  KVBlock<S, HD> cur, nxt;
+  int kb = wave;
+  if (kb < nblocks) cur.load(kc, vc, base_of(kb), lane);
+  for (; kb < nblocks; kb += ATT_WAVES) {
+    if (kb + ATT_WAVES < nblocks) nxt.load(kc, vc, base_of(kb + ATT_WAVES), lane);
     f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int c = 0; c < NQC; ++c) {
-      const u32x4_t a = __builtin_nontemporal_load(
-          reinterpret_cast<const u32x4_t*>(kc + base + (size_t)(c * 64 + lane) * EPL));
-      s = mma_frag(a, qf[c], s, S{});
-    }
-    VT vf[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t)
-      vf[t] = __builtin_nontemporal_load(reinterpret_cast<const VT*>(vc + base + (size_t)(t * 64 + lane) * 4));
-
+    for (int c = 0; c < NQC; ++c) s = mma_frag(cur.k[c], qf[c], s, S{});
+    // s[r] = score of key kb*16 + 4g + r for query row j
     float s2[4];
     float mloc = -INFINITY;
 #pragma unroll
@@ -128,80 +145,53 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(const AttnParams p) {
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
       o[t] *= alpha;
-      o[t] = mma_pv(vf[t], pr, o[t], S{});
+      o[t] = mma_pv(cur.v[t], pr, o[t], S{});
     }
+    cur = nxt;
   }
-
-  S* O = reinterpret_cast<S*>(p.O);
-  const int rt = wave * 16 + j;
-  if (p.splits == 1) {
-    if (valid) {
-      const float inv = l_i > 0.f ? 1.f / l_i : 0.f;
-      S* orow = O + (size_t)(b * p.rows_per_seq + row) * p.ldo + h * HD;
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) orow[t * 16 + 4 * g + r] = T::from_f(o[t][r] * inv);
-    }
-    return;
+  // merge the waves' states
+  if (g == 0) {
+    s_m[wave][j] = m_i;
+    s_l[wave][j] = l_i;
   }
-  const size_t pstride = (size_t)64 * (HD + 2);
-  const size_t item = (size_t)bq * p.n_heads + h;
-  float* pp = p.part + (item * p.splits + split) * pstride;
 #pragma unroll
   for (int t = 0; t < NT; ++t)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) pp[(size_t)rt * HD + t * 16 + 4 * g + r] = o[t][r];
-  if (g == 0) {
-    pp[64 * HD + rt] = m_i;
-    pp[64 * HD + 64 + rt] = l_i;
-  }
-  __threadfence();
+    for (int r = 0; r < 4; ++r) s_o[wave][j][t * 16 + 4 * g + r] = o[t][r];
   __syncthreads();
-  __shared__ int last;
-  if (threadIdx.x == 0) {
-    const int old = atomicAdd(p.sem + item, 1);
-    last = (old == p.splits - 1);
-    if (last) atomicExch(p.sem + item, 0);
-  }
-  __syncthreads();
-  if (!last) return;
-  __threadfence();
-  const float* base = p.part + item * p.splits * pstride;
-  for (int e = threadIdx.x; e < 64 * HD; e += ATT_THREADS) {
+  S* O = reinterpret_cast<S*>(p.O);
+  for (int e = threadIdx.x; e < 16 * HD; e += ATT_THREADS) {
     const int r2 = e / HD, dim = e % HD;
-    const int row2 = qt * 64 + r2;
+    const int row2 = qt * 16 + r2;
     if (row2 >= p.nq) continue;
     float M = -INFINITY;
-    for (int s2 = 0; s2 < p.splits; ++s2)
-      M = fmaxf(M, __builtin_nontemporal_load(base + s2 * pstride + 64 * HD + r2));
+#pragma unroll
+    for (int w = 0; w < ATT_WAVES; ++w) M = fmaxf(M, s_m[w][r2]);
     float num = 0.f, den = 0.f;
-    for (int s2 = 0; s2 < p.splits; ++s2) {
-      const float ms = __builtin_nontemporal_load(base + s2 * pstride + 64 * HD + r2);
-      const float w = (ms == -INFINITY) ? 0.f : exp2f(ms - M);
-      num += w * __builtin_nontemporal_load(base + s2 * pstride + (size_t)r2 * HD + dim);
-      den += w * __builtin_nontemporal_load(base + s2 * pstride + 64 * HD + 64 + r2);
+#pragma unroll
+    for (int w = 0; w < ATT_WAVES; ++w) {
+      const float ms = s_m[w][r2];
+      const float wt = (ms == -INFINITY) ? 0.f : exp2f(ms - M);
+      num += wt * s_o[w][r2][dim];
+      den += wt * s_l[w][r2];
     }
     O[(size_t)(b * p.rows_per_seq + row2) * p.ldo + h * HD + dim] = T::from_f(den > 0.f ? num / den : 0.f);
   }
 }
 
 void plan_attention(AttnParams& p, int max_keys) {
-  p.qtiles = (p.nq + 63) / 64;
-  const int nblocks = std::max(1, (max_keys + 15) / 16);
-  const int base = p.nbatch * p.qtiles * p.n_heads;
-  int splits = std::max(1, std::min(nblocks, (ATT_TARGET_WGS + base - 1) / base));
-  p.blocks_per_split = (nblocks + splits - 1) / splits;
-  p.splits = (nblocks + p.blocks_per_split - 1) / p.blocks_per_split;
+  (void)max_keys;
+  p.qtiles = (p.nq + 15) / 16;
+  p.splits = 1;
+  p.blocks_per_split = 0;
 }
 
-size_t attention_part_floats(int nbatch, int qtiles, int n_heads, int splits, int hd) {
-  return splits > 1 ? (size_t)nbatch * qtiles * n_heads * splits * 64 * (hd + 2) : 0;
-}
+size_t attention_part_floats(int, int, int, int, int) { return 0; }
 
 template <typename S>
 static hipError_t launch_attn_t(AttnParams& p, hipStream_t st) {
-  dim3 grid(p.splits, p.n_heads, p.nbatch * p.qtiles), block(ATT_THREADS);
+  const int items = p.nbatch * p.n_heads;
+  dim3 grid(8 * ((items + 7) / 8) * p.qtiles), block(ATT_THREADS);
   switch (p.hd) {
     case 32: hipLaunchKernelGGL((attn_kernel<S, 32>), grid, block, 0, st, p); break;
     case 64: hipLaunchKernelGGL((attn_kernel<S, 64>), grid, block, 0, st, p); break;

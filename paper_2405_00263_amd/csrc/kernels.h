@@ -8,11 +8,9 @@ namespace clover {
 
 // ---- weight-streaming GEMM ------------------------------------------------------------
 enum GemmEpilogue : int {
-  EP_F32 = 0,     // out_f[m][n] = y
-  EP_RESID = 1,   // out_f[m][n] = resid[m][n] + y ; out_s (optional) = storage copy
-  EP_QKV = 2,     // rotary on q/k, q -> qbuf, k/v -> paged KV cache
-  EP_SWIGLU = 3,  // out_s[m][j] = silu(gate) * up  (gate/up tiles paired per group)
-  EP_HEAD = 4,    // out_f[m][n] = resid[m][n] + silu(y + bias[n]); out_s optional copy
+  EP_PARTIAL = 0,  // part[split][m][n] = partial y (fp32); S = 1 gives y itself
+  EP_QKV = 2,      // rotary on q/k, q -> qbuf, k/v -> paged KV cache (unsplit)
+  EP_SWIGLU = 3,   // out_s[m][j] = silu(gate) * up, gate/up tiles paired per group (unsplit)
 };
 
 struct GemmSeg {
@@ -26,13 +24,10 @@ struct GemmParams {
   GemmSeg seg[3];
   int nseg, ntiles, N;
   int ngroups, mchunks, S, cps;
-  float* part;
-  int* sem;
+  int max_splits;  // EP_PARTIAL: upper bound on K splits (1 = unsplit)
+  float* part;     // EP_PARTIAL output [S][M][N]
   int mode;
-  float* out_f; int ldo;
   void* out_s; int ldos;
-  const float* resid; int ldr;
-  const void* bias;
   // EP_QKV
   void* qbuf; int ldq;
   void* kcache; void* vcache;
@@ -49,10 +44,12 @@ struct GemmPlan {
   size_t part_floats;
 };
 
-GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu);
+GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int max_splits);
 // Fills plan fields of p and launches; returns hipSuccess or an error.
 hipError_t launch_gemm(int dtype, GemmParams& p, hipStream_t st);
-hipError_t launch_pack(int dtype, const void* src, int rows, int cols, void* dst, hipStream_t st);
+// rope_interleave: Q/K weights of 128-wide heads, rotary halves interleaved by 16-row tiles
+hipError_t launch_pack(int dtype, const void* src, int rows, int cols, void* dst, bool rope_interleave,
+                       hipStream_t st);
 size_t packed_matrix_bytes(int dtype, int rows, int cols);
 
 // ---- attention -------------------------------------------------------------------------
@@ -71,7 +68,6 @@ struct AttnParams {
   const uint64_t* mask; int mask_words; int mask_seq_stride;  // per slot [T][words]
   int n_heads, n_kv, hd;
   int nbatch, qtiles, splits, blocks_per_split;
-  float* part; int* sem;
 };
 hipError_t launch_attention(int dtype, AttnParams& p, int max_keys, hipStream_t st);
 // write rows [n][n_kv*hd] (storage) of K and V into the paged cache at slots slot0.. of seq
@@ -84,9 +80,9 @@ void plan_attention(AttnParams& p, int max_keys);
 // ---- row kernels -------------------------------------------------------------------------
 hipError_t launch_embed(int dtype, const void* emb, const int* tok, int M, int d, float* x,
                         hipStream_t st);
-hipError_t launch_rmsnorm(int dtype, const float* x, int ldx, int M, int d, const void* g,
-                          float eps, void* out, int ldo, float* copy, hipStream_t st);
-hipError_t launch_argmax(const float* logits, int M, int V, int* out, hipStream_t st);
+// keys: M u64 scratch; keys_zeroed: a previous kernel already cleared them
+hipError_t launch_argmax(const float* logits, int M, int V, int* out, unsigned long long* keys,
+                         bool keys_zeroed, hipStream_t st);
 // top-k of rows with log-softmax; writes either plain (tok/logp [M][k]) or candidate
 // records (children of frontier rows).
 struct TopkParams {
@@ -96,8 +92,25 @@ struct TopkParams {
   const int* seq_ids; int F;
   int* cand_token; int* cand_parent; int* cand_depth; float* cand_lp; int cand_stride;
   int base_parent, base_child, depth;
+  float* scratch;  // topk_scratch_floats(M, k)
 };
+size_t topk_scratch_floats(int M, int V, int k);
 hipError_t launch_topk(TopkParams& p, hipStream_t st);
+
+struct RowFixParams {
+  int M, d;
+  const float* part; int S; int ldp;   // split-K partials [S][M][ldp] (S = 0: none)
+  const float* resid; int ldr;         // residual input (null: 0)
+  int act;                             // 0: y = sum; 1: y = silu(sum + bias)
+  const void* bias;                    // storage [d]
+  float* out_f; int ldo;               // resid + y (may alias resid)
+  float* out_copy_f;                   // optional fp32 copy [M][d]
+  void* out_copy_s;                    // optional storage copy [M][d]
+  const void* gain; float eps;         // RMSNorm gain (storage)
+  void* out_norm; int ldn;             // optional RMSNorm(result) * gain, storage
+  unsigned long long* zero_keys; int zero_n;  // optional: clear argmax keys
+};
+hipError_t launch_rowfix(int dtype, RowFixParams& p, hipStream_t st);
 
 struct AdPrepParams {
   // frontier row f = b*F + fl of depth j; parent state row = prev[b*Fprev + fl/kprev]
@@ -110,8 +123,8 @@ struct AdPrepParams {
   float* hin; void* a_out; void* e_out;
 };
 hipError_t launch_ad_prep(int dtype, AdPrepParams& p, hipStream_t st);
-hipError_t launch_ad_attn(int dtype, const float* q, const float* kv, int M, int n_heads, int hd,
-                          void* out, hipStream_t st);
+hipError_t launch_ad_attn(int dtype, const float* q, int Sq, const float* kv, int Skv, int M,
+                          int n_heads, int hd, void* out, hipStream_t st);
 
 // ---- tree, acceptance, compaction -----------------------------------------------------------
 struct TreeParams {

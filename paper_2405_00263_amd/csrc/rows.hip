@@ -38,153 +38,203 @@ __device__ __forceinline__ float block_sum256(float v, float* red) {
   return red[0] + red[1] + red[2] + red[3];
 }
 
-// ---- RMSNorm: out[m] = x[m] / sqrt(mean(x^2) + eps) * g, stored in the storage type ---------
-template <typename S>
-__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ x, int ldx, int d,
-                                                      const S* __restrict__ gain, float eps,
-                                                      S* __restrict__ out, int ldo,
-                                                      float* __restrict__ copy) {
-  __shared__ float red[4];
-  const int m = blockIdx.x;
-  const float* xr = x + (size_t)m * ldx;
-  float ss = 0.f;
-  for (int k = threadIdx.x; k < d; k += 256) ss += xr[k] * xr[k];
-  ss = block_sum256(ss, red);
-  const float rinv = 1.0f / sqrtf(ss / (float)d + eps);
-  for (int k = threadIdx.x; k < d; k += 256) {
-    const float v = xr[k];
-    out[(size_t)m * ldo + k] = St<S>::from_f(v * rinv * St<S>::to_f(gain[k]));
-    if (copy) copy[(size_t)m * d + k] = v;
-  }
-}
-
-hipError_t launch_rmsnorm(int dtype, const float* x, int ldx, int M, int d, const void* g,
-                          float eps, void* out, int ldo, float* copy, hipStream_t st) {
-  if (M <= 0) return hipSuccess;
-  if (dtype == 1)
-    hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(M), dim3(256), 0, st, x, ldx, d,
-                       (const bf16_t*)g, eps, (bf16_t*)out, ldo, copy);
-  else
-    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(M), dim3(256), 0, st, x, ldx, d,
-                       (const float*)g, eps, (float*)out, ldo, copy);
-  return hipGetLastError();
-}
-
 // ---- argmax (lowest index on ties) ---------------------------------------------------------
+// Every element maps to a 64-bit key whose order is (value ascending, index descending):
+// the maximum key is the largest value with the lowest index.  Chunks of a row reduce
+// to one key each and combine with a 64-bit atomic max, which is exact and
+// order-independent, so the result is deterministic.
 __device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
   return va > vb || (va == vb && ia < ib);
 }
-
-static constexpr int RED_THREADS = 512;
-
-__global__ __launch_bounds__(RED_THREADS) void argmax_kernel(const float* __restrict__ logits, int V,
-                                                             int* __restrict__ out) {
-  __shared__ float sv[RED_THREADS / 64];
-  __shared__ int si[RED_THREADS / 64];
-  const int m = blockIdx.x;
-  const float* row = logits + (size_t)m * V;
-  float bv = -INFINITY;
-  int bi = 0x7fffffff;
-  for (int k = threadIdx.x; k < V; k += RED_THREADS) {
-    const float v = row[k];
-    if (better(v, k, bv, bi)) { bv = v; bi = k; }
-  }
-  for (int o = 32; o > 0; o >>= 1) {
-    const float ov = __shfl_xor(bv, o);
-    const int oi = __shfl_xor(bi, o);
-    if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-  }
-  const int w = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) { sv[w] = bv; si[w] = bi; }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    for (int i = 1; i < RED_THREADS / 64; ++i)
-      if (better(sv[i], si[i], bv, bi)) { bv = sv[i]; bi = si[i]; }
-    out[m] = bi;
-  }
+__device__ __forceinline__ unsigned long long amax_key(float v, int i) {
+  uint32_t u = __float_as_uint(v);
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((unsigned long long)u << 32) | (uint32_t)(0x7fffffff - i);
+}
+__device__ __forceinline__ unsigned long long umax64(unsigned long long a, unsigned long long b) {
+  return a > b ? a : b;
 }
 
-hipError_t launch_argmax(const float* logits, int M, int V, int* out, hipStream_t st) {
+static constexpr int RED_THREADS = 256;
+static constexpr int AMAX_CHUNKS = 32;
+
+__global__ __launch_bounds__(RED_THREADS) void argmax_kernel(const float* __restrict__ logits, int V,
+                                                             unsigned long long* __restrict__ keys) {
+  const int m = blockIdx.x, ch = blockIdx.y;
+  const int per = (V + AMAX_CHUNKS - 1) / AMAX_CHUNKS;
+  const int c0 = ch * per, c1 = min(V, c0 + per);
+  const float* row = logits + (size_t)m * V;
+  unsigned long long best = 0ull;
+  constexpr int U = 8;
+  for (int c = c0 + threadIdx.x; c < c1; c += RED_THREADS * U) {
+    float v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = c + u * RED_THREADS;
+      v[u] = i < c1 ? row[i] : -INFINITY;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = c + u * RED_THREADS;
+      if (i < c1) best = umax64(best, amax_key(v[u], i));
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    const unsigned long long ob = ((unsigned long long)__shfl_xor((int)(best >> 32), o) << 32) |
+                                  (uint32_t)__shfl_xor((int)(best & 0xffffffffu), o);
+    best = umax64(best, ob);
+  }
+  if ((threadIdx.x & 63) == 0) atomicMax(keys + m, best);
+}
+
+__global__ void argmax_finish_kernel(const unsigned long long* __restrict__ keys, int M, int* __restrict__ out) {
+  const int m = blockIdx.x * blockDim.x + threadIdx.x;
+  if (m < M) out[m] = 0x7fffffff - (int)(keys[m] & 0xffffffffu);
+}
+
+__global__ void zero_u64_kernel(unsigned long long* p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0ull;
+}
+
+hipError_t launch_argmax(const float* logits, int M, int V, int* out, unsigned long long* keys,
+                         bool keys_zeroed, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  hipLaunchKernelGGL(argmax_kernel, dim3(M), dim3(RED_THREADS), 0, st, logits, V, out);
+  if (!keys_zeroed) hipLaunchKernelGGL(zero_u64_kernel, dim3((M + 255) / 256), dim3(256), 0, st, keys, M);
+  hipLaunchKernelGGL(argmax_kernel, dim3(M, AMAX_CHUNKS), dim3(RED_THREADS), 0, st, logits, V, keys);
+  hipLaunchKernelGGL(argmax_finish_kernel, dim3((M + 255) / 256), dim3(256), 0, st, keys, M, out);
   return hipGetLastError();
 }
 
-// ---- top-k with log-softmax ----------------------------------------------------------------
+// ---- top-k with log-softmax, two stages ---------------------------------------------------
+// Stage 1: each (row, chunk) workgroup finds its chunk's k best (value desc, index asc)
+// by k rounds of block argmax over register-resident elements, and the chunk's
+// (max, sum exp(x - max)).  Stage 2: one workgroup per row merges the chunk lists the
+// same way and combines the chunk sums in chunk order into the log-sum-exp.
 static constexpr int KMAX = 16;
+static constexpr int TOPK_EPT = 16;  // elements per thread in stage 1
+static constexpr int TOPK_S2 = 4;    // candidates per thread in stage 2
 
-__global__ __launch_bounds__(RED_THREADS) void topk_kernel(const TopkParams p) {
-  __shared__ float sv[RED_THREADS / 64];
-  __shared__ int si[RED_THREADS / 64];
-  __shared__ float sm[RED_THREADS / 64], ss[RED_THREADS / 64];
-  __shared__ float res_v[KMAX];
-  __shared__ int res_i[KMAX];
-  const int m = blockIdx.x;
-  const float* row = p.logits + (size_t)m * p.V;
-  const int k = p.k;  // 1..KMAX; each thread keeps its KMAX best, a superset of its k best
-  float lv[KMAX];
-  int li[KMAX];
-#pragma unroll
-  for (int i = 0; i < KMAX; ++i) { lv[i] = -INFINITY; li[i] = 0x7fffffff; }
-  float mx = -INFINITY, se = 0.f;
-  for (int c = threadIdx.x; c < p.V; c += RED_THREADS) {
-    float v = row[c];
-    // running log-sum-exp
-    if (v > mx) { se = se * expf(mx - v) + 1.f; mx = v; }
-    else se += expf(v - mx);
-    // sorted insertion into the thread's list (static indices only)
-    if (better(v, c, lv[KMAX - 1], li[KMAX - 1])) {
-      int ci = c;
-#pragma unroll
-      for (int i = 0; i < KMAX; ++i) {
-        if (better(v, ci, lv[i], li[i])) {
-          const float tv = lv[i]; const int ti = li[i];
-          lv[i] = v; li[i] = ci; v = tv; ci = ti;
-        }
-      }
-    }
-  }
-  // block log-sum-exp
+__device__ void block_best(float& v, int& i, float* sv, int* si) {
   for (int o = 32; o > 0; o >>= 1) {
-    const float om = __shfl_xor(mx, o), os = __shfl_xor(se, o);
-    const float nm = fmaxf(mx, om);
-    se = (mx == -INFINITY ? 0.f : se * expf(mx - nm)) + (om == -INFINITY ? 0.f : os * expf(om - nm));
-    mx = nm;
+    const float ov = __shfl_xor(v, o);
+    const int oi = __shfl_xor(i, o);
+    if (better(ov, oi, v, i)) { v = ov; i = oi; }
   }
   const int w = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) { sm[w] = mx; ss[w] = se; }
   __syncthreads();
-  float M = sm[0];
-  for (int i = 1; i < RED_THREADS / 64; ++i) M = fmaxf(M, sm[i]);
-  float S = 0.f;
-  for (int i = 0; i < RED_THREADS / 64; ++i) S += ss[i] * expf(sm[i] - M);
-  const float lse = M + logf(S);
-  // merge: k rounds of block-wide best over list heads
-  for (int r = 0; r < k; ++r) {
-    float bv = lv[0];
-    int bi = li[0];
-    for (int o = 32; o > 0; o >>= 1) {
-      const float ov = __shfl_xor(bv, o);
-      const int oi = __shfl_xor(bi, o);
-      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-    }
-    __syncthreads();
-    if ((threadIdx.x & 63) == 0) { sv[w] = bv; si[w] = bi; }
-    __syncthreads();
-    bv = sv[0]; bi = si[0];
-    for (int i = 1; i < RED_THREADS / 64; ++i)
-      if (better(sv[i], si[i], bv, bi)) { bv = sv[i]; bi = si[i]; }
-    if (threadIdx.x == 0) { res_v[r] = bv; res_i[r] = bi; }
-    if (li[0] == bi) {  // the owner pops its head
+  if ((threadIdx.x & 63) == 0) { sv[w] = v; si[w] = i; }
+  __syncthreads();
+  v = sv[0]; i = si[0];
+  for (int q = 1; q < RED_THREADS / 64; ++q)
+    if (better(sv[q], si[q], v, i)) { v = sv[q]; i = si[q]; }
+}
+
+__global__ __launch_bounds__(RED_THREADS) void topk_stage1_kernel(const float* __restrict__ logits, int V, int k,
+                                                                   int nch, float* __restrict__ pv,
+                                                                   int* __restrict__ pi, float* __restrict__ pms) {
+  __shared__ float sv[RED_THREADS / 64], sred[RED_THREADS / 64];
+  __shared__ int si[RED_THREADS / 64];
+  const int m = blockIdx.x, ch = blockIdx.y;
+  const int per = (V + nch - 1) / nch;
+  const int c0 = ch * per, c1 = min(V, c0 + per);
+  const float* row = logits + (size_t)m * V;
+  float v[TOPK_EPT];
+  uint32_t taken = 0u;
+  float mx = -INFINITY;
 #pragma unroll
-      for (int i = 0; i < KMAX - 1; ++i) { lv[i] = lv[i + 1]; li[i] = li[i + 1]; }
-      lv[KMAX - 1] = -INFINITY; li[KMAX - 1] = 0x7fffffff;
+  for (int u = 0; u < TOPK_EPT; ++u) {
+    const int i = c0 + threadIdx.x + u * RED_THREADS;
+    v[u] = i < c1 ? row[i] : -INFINITY;
+  }
+#pragma unroll
+  for (int u = 0; u < TOPK_EPT; ++u) mx = fmaxf(mx, v[u]);
+  // chunk max and sum of exponentials
+  float bm = mx;
+  for (int o = 32; o > 0; o >>= 1) bm = fmaxf(bm, __shfl_xor(bm, o));
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) sred[w] = bm;
+  __syncthreads();
+  float cmax = sred[0];
+  for (int q = 1; q < RED_THREADS / 64; ++q) cmax = fmaxf(cmax, sred[q]);
+  float se = 0.f;
+#pragma unroll
+  for (int u = 0; u < TOPK_EPT; ++u) se += (v[u] == -INFINITY) ? 0.f : expf(v[u] - cmax);
+  se = warp_sum(se);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sred[w] = se;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float tot = 0.f;
+    for (int q = 0; q < RED_THREADS / 64; ++q) tot += sred[q];
+    pms[((size_t)m * nch + ch) * 2] = cmax;
+    pms[((size_t)m * nch + ch) * 2 + 1] = tot;
+  }
+  // k rounds of block argmax; the owner of the winner masks it out
+  for (int r = 0; r < k; ++r) {
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+#pragma unroll
+    for (int u = 0; u < TOPK_EPT; ++u) {
+      const int i = c0 + threadIdx.x + u * RED_THREADS;
+      if (i < c1 && !((taken >> u) & 1u) && better(v[u], i, bv, bi)) { bv = v[u]; bi = i; }
     }
+    block_best(bv, bi, sv, si);  // bi == INT_MAX: the chunk has fewer than k elements
+    if (threadIdx.x == 0) {
+      pv[((size_t)m * nch + ch) * k + r] = bv;
+      pi[((size_t)m * nch + ch) * k + r] = bi;
+    }
+#pragma unroll
+    for (int u = 0; u < TOPK_EPT; ++u)
+      if (c0 + (int)threadIdx.x + u * RED_THREADS == bi) taken |= 1u << u;
+  }
+}
+
+__global__ __launch_bounds__(RED_THREADS) void topk_stage2_kernel(const TopkParams p, int nch,
+                                                                   const float* __restrict__ pv,
+                                                                   const int* __restrict__ pi,
+                                                                   const float* __restrict__ pms) {
+  __shared__ float sv[RED_THREADS / 64];
+  __shared__ int si[RED_THREADS / 64];
+  __shared__ float res_v[KMAX];
+  __shared__ int res_i[KMAX];
+  __shared__ float s_lse;
+  const int m = blockIdx.x, k = p.k;
+  const int ncand = nch * k;  // <= TOPK_S2 * RED_THREADS
+  float cv[TOPK_S2];
+  int ci[TOPK_S2];
+#pragma unroll
+  for (int u = 0; u < TOPK_S2; ++u) {
+    const int c = threadIdx.x + u * RED_THREADS;
+    cv[u] = c < ncand ? pv[(size_t)m * ncand + c] : -INFINITY;
+    ci[u] = c < ncand ? pi[(size_t)m * ncand + c] : 0x7fffffff;
+  }
+  if (threadIdx.x == 0) {
+    float M = -INFINITY;
+    for (int c = 0; c < nch; ++c) M = fmaxf(M, pms[((size_t)m * nch + c) * 2]);
+    float S = 0.f;
+    for (int c = 0; c < nch; ++c) {
+      const float cm = pms[((size_t)m * nch + c) * 2];
+      if (cm != -INFINITY) S += pms[((size_t)m * nch + c) * 2 + 1] * expf(cm - M);
+    }
+    s_lse = M + logf(S);
+  }
+  for (int r = 0; r < k; ++r) {
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+#pragma unroll
+    for (int u = 0; u < TOPK_S2; ++u)
+      if (better(cv[u], ci[u], bv, bi)) { bv = cv[u]; bi = ci[u]; }
+    block_best(bv, bi, sv, si);
+    if (threadIdx.x == 0) { res_v[r] = bv; res_i[r] = bi; }
+#pragma unroll
+    for (int u = 0; u < TOPK_S2; ++u)
+      if (ci[u] == bi) { cv[u] = -INFINITY; ci[u] = 0x7fffffff; }
   }
   __syncthreads();
   if (threadIdx.x < k) {
     const int r = threadIdx.x;
-    const float logp = res_v[r] - lse;
+    const float logp = res_v[r] - s_lse;
     if (p.tok) {
       p.tok[(size_t)m * k + r] = res_i[r];
       p.logp[(size_t)m * k + r] = logp;
@@ -203,10 +253,111 @@ __global__ __launch_bounds__(RED_THREADS) void topk_kernel(const TopkParams p) {
   }
 }
 
+// chunks per row: enough that one chunk fits the stage-1 registers, at most what the
+// stage-2 merge holds
+static int topk_chunks(int V, int k) {
+  const int need = (V + TOPK_EPT * RED_THREADS - 1) / (TOPK_EPT * RED_THREADS);
+  return std::max(need, std::min(32, TOPK_S2 * RED_THREADS / k));
+}
+
+size_t topk_scratch_floats(int M, int V, int k) { return (size_t)M * topk_chunks(V, k) * (2 * k + 2); }
+
 hipError_t launch_topk(TopkParams& p, hipStream_t st) {
   if (p.M <= 0) return hipSuccess;
   if (p.k < 1 || p.k > KMAX) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(topk_kernel, dim3(p.M), dim3(RED_THREADS), 0, st, p);
+  const int nch = topk_chunks(p.V, p.k);
+  if (nch * p.k > TOPK_S2 * RED_THREADS) return hipErrorInvalidValue;
+  float* pv = p.scratch;
+  int* pi = reinterpret_cast<int*>(p.scratch + (size_t)p.M * nch * p.k);
+  float* pms = p.scratch + (size_t)p.M * nch * 2 * p.k;
+  hipLaunchKernelGGL(topk_stage1_kernel, dim3(p.M, nch), dim3(RED_THREADS), 0, st, p.logits, p.V, p.k, nch,
+                     pv, pi, pms);
+  hipLaunchKernelGGL(topk_stage2_kernel, dim3(p.M), dim3(RED_THREADS), 0, st, p, nch, pv, pi, pms);
+  return hipGetLastError();
+}
+
+// ---- reduce split-K partials, residual, activation, RMSNorm ---------------------------------
+// One workgroup per row.  result = resid + y with y = sum_s part[s] (act 0) or
+// silu(sum_s part[s] + bias) (act 1), summed in split order; then optional copies and
+// out_norm = RMSNorm(result) * gain in the storage type.
+static constexpr int FIX_THREADS = 1024;
+static constexpr int FIX_MAXS = 8;
+static constexpr int FIX_VEC = 2;  // float4 per thread: d <= 8192
+
+template <typename S>
+__global__ __launch_bounds__(FIX_THREADS) void rowfix_kernel(const RowFixParams p) {
+  using T = St<S>;
+  __shared__ float red[FIX_THREADS / 64];
+  const int m = blockIdx.x, d = p.d;
+  if (p.zero_keys && m == 0)
+    for (int i = threadIdx.x; i < p.zero_n; i += FIX_THREADS) p.zero_keys[i] = 0ull;
+  float4 acc[FIX_VEC];
+  float4 part[FIX_MAXS][FIX_VEC];
+  float4 res[FIX_VEC];
+#pragma unroll
+  for (int i = 0; i < FIX_VEC; ++i) {
+    const int e = threadIdx.x * 4 + i * FIX_THREADS * 4;
+    res[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (e < d && p.resid) res[i] = *reinterpret_cast<const float4*>(p.resid + (size_t)m * p.ldr + e);
+#pragma unroll
+    for (int s = 0; s < FIX_MAXS; ++s) {
+      part[s][i] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (s < p.S && e < d)
+        part[s][i] = *reinterpret_cast<const float4*>(p.part + ((size_t)s * p.M + m) * p.ldp + e);
+    }
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < FIX_VEC; ++i) {
+    const int e = threadIdx.x * 4 + i * FIX_THREADS * 4;
+    float4 y = part[0][i];
+#pragma unroll
+    for (int s = 1; s < FIX_MAXS; ++s)
+      if (s < p.S) { y.x += part[s][i].x; y.y += part[s][i].y; y.z += part[s][i].z; y.w += part[s][i].w; }
+    if (p.act == 1 && e < d) {
+      const S* b = reinterpret_cast<const S*>(p.bias) + e;
+      y.x = silu_f(y.x + T::to_f(b[0])); y.y = silu_f(y.y + T::to_f(b[1]));
+      y.z = silu_f(y.z + T::to_f(b[2])); y.w = silu_f(y.w + T::to_f(b[3]));
+    }
+    float4 o = make_float4(res[i].x + y.x, res[i].y + y.y, res[i].z + y.z, res[i].w + y.w);
+    acc[i] = o;
+    if (e < d) {
+      if (p.out_f) *reinterpret_cast<float4*>(p.out_f + (size_t)m * p.ldo + e) = o;
+      if (p.out_copy_f) *reinterpret_cast<float4*>(p.out_copy_f + (size_t)m * d + e) = o;
+      if (p.out_copy_s) {
+        S* cs = reinterpret_cast<S*>(p.out_copy_s) + (size_t)m * d + e;
+        cs[0] = T::from_f(o.x); cs[1] = T::from_f(o.y); cs[2] = T::from_f(o.z); cs[3] = T::from_f(o.w);
+      }
+      ss += o.x * o.x + o.y * o.y + o.z * o.z + o.w * o.w;
+    }
+  }
+  if (!p.out_norm) return;
+  ss = warp_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+  for (int q = 0; q < FIX_THREADS / 64; ++q) tot += red[q];
+  const float rinv = 1.0f / sqrtf(tot / (float)d + p.eps);
+  const S* gain = reinterpret_cast<const S*>(p.gain);
+#pragma unroll
+  for (int i = 0; i < FIX_VEC; ++i) {
+    const int e = threadIdx.x * 4 + i * FIX_THREADS * 4;
+    if (e >= d) continue;
+    S* on = reinterpret_cast<S*>(p.out_norm) + (size_t)m * p.ldn + e;
+    on[0] = T::from_f(acc[i].x * rinv * T::to_f(gain[e]));
+    on[1] = T::from_f(acc[i].y * rinv * T::to_f(gain[e + 1]));
+    on[2] = T::from_f(acc[i].z * rinv * T::to_f(gain[e + 2]));
+    on[3] = T::from_f(acc[i].w * rinv * T::to_f(gain[e + 3]));
+  }
+}
+
+hipError_t launch_rowfix(int dtype, RowFixParams& p, hipStream_t st) {
+  if (p.M <= 0) return hipSuccess;
+  if (p.S > FIX_MAXS || p.d > FIX_VEC * FIX_THREADS * 4 || p.d % 4) return hipErrorInvalidValue;
+  if (dtype == 1)
+    hipLaunchKernelGGL(rowfix_kernel<bf16_t>, dim3(p.M), dim3(FIX_THREADS), 0, st, p);
+  else
+    hipLaunchKernelGGL(rowfix_kernel<float>, dim3(p.M), dim3(FIX_THREADS), 0, st, p);
   return hipGetLastError();
 }
 
@@ -256,36 +407,42 @@ hipError_t launch_ad_prep(int dtype, AdPrepParams& p, hipStream_t st) {
 }
 
 // ---- Attention Decoder attention (Eq. 1-2): one key per frontier row ----------------------
-// q: [M][H*hd] f32, kv: [M][2*H*hd] f32 (keys then values).  The softmax is taken over
-// the key set of the row, which holds the single embedding e_{i-1}.
+// q: split-K partials [Sq][M][H*hd], kv: partials [Skv][M][2*H*hd] (keys then values), f32.
+// The softmax is taken over the key set of the row, which holds the single embedding
+// e_{i-1}.
 template <typename S>
-__global__ __launch_bounds__(64) void ad_attn_kernel(const float* __restrict__ q,
-                                                     const float* __restrict__ kv, int H, int hd,
-                                                     S* __restrict__ out) {
+__global__ __launch_bounds__(64) void ad_attn_kernel(const float* __restrict__ q, int Sq,
+                                                     const float* __restrict__ kv, int Skv, int M, int H,
+                                                     int hd, S* __restrict__ out) {
   const int f = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
   const int qd = H * hd;
-  const float* qr = q + (size_t)f * qd + h * hd;
-  const float* kr = kv + (size_t)f * 2 * qd + h * hd;
-  const float* vr = kv + (size_t)f * 2 * qd + qd + h * hd;
   float dot = 0.f;
-  for (int i = lane; i < hd; i += 64) dot += qr[i] * kr[i];
+  for (int i = lane; i < hd; i += 64) {
+    float qv = 0.f, kk = 0.f;
+    for (int s = 0; s < Sq; ++s) qv += q[((size_t)s * M + f) * qd + h * hd + i];
+    for (int s = 0; s < Skv; ++s) kk += kv[((size_t)s * M + f) * 2 * qd + h * hd + i];
+    dot += qv * kk;
+  }
   dot = warp_sum(dot);
-  const float s = dot * rsqrtf((float)hd);
-  const float mx = s;                 // max over the single key
-  const float pw = expf(s - mx);      // = 1
+  const float sc = dot * rsqrtf((float)hd);
+  const float mx = sc;               // max over the single key
+  const float pw = expf(sc - mx);    // = 1
   const float l = pw;
-  for (int i = lane; i < hd; i += 64)
-    out[(size_t)f * qd + h * hd + i] = St<S>::from_f(pw * vr[i] / l);
+  for (int i = lane; i < hd; i += 64) {
+    float vv = 0.f;
+    for (int s = 0; s < Skv; ++s) vv += kv[((size_t)s * M + f) * 2 * qd + qd + h * hd + i];
+    out[(size_t)f * qd + h * hd + i] = St<S>::from_f(pw * vv / l);
+  }
 }
 
-hipError_t launch_ad_attn(int dtype, const float* q, const float* kv, int M, int n_heads, int hd,
-                          void* out, hipStream_t st) {
+hipError_t launch_ad_attn(int dtype, const float* q, int Sq, const float* kv, int Skv, int M, int n_heads,
+                          int hd, void* out, hipStream_t st) {
   if (M <= 0) return hipSuccess;
   dim3 grid(M, n_heads);
   if (dtype == 1)
-    hipLaunchKernelGGL(ad_attn_kernel<bf16_t>, grid, dim3(64), 0, st, q, kv, n_heads, hd, (bf16_t*)out);
+    hipLaunchKernelGGL(ad_attn_kernel<bf16_t>, grid, dim3(64), 0, st, q, Sq, kv, Skv, M, n_heads, hd, (bf16_t*)out);
   else
-    hipLaunchKernelGGL(ad_attn_kernel<float>, grid, dim3(64), 0, st, q, kv, n_heads, hd, (float*)out);
+    hipLaunchKernelGGL(ad_attn_kernel<float>, grid, dim3(64), 0, st, q, Sq, kv, Skv, M, n_heads, hd, (float*)out);
   return hipGetLastError();
 }
 

@@ -101,4 +101,6 @@ def test_op_entry_points_validate():
     assert L.clover_packed_matrix_bytes(0, 32, 48) == 32 * 48 * 4
     assert L.clover_op_attention_scratch_bytes(1, 100, 64, 32, 8, 128) > 0
     assert L.clover_op_attention_scratch_bytes(1, 100, 64, 32, 7, 128) == 0
-    assert L.clover_op_topk(None, 1, 10, 3, None, None, None) == 1
+    assert L.clover_op_topk(None, 1, 10, 3, None, None, None, None) == 1
+    assert L.clover_op_topk_scratch_bytes(4, 125696, 16) > 0
+    assert L.clover_op_topk_scratch_bytes(4, 125696, 17) == 0
