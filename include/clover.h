@@ -69,7 +69,10 @@ typedef struct {
 } clover_config;
 
 #define CLOVER_FLAG_KEEP_LOGITS 1 /* keep draft and verify logits of the last step readable */
-#define CLOVER_FLAG_PROFILE 2     /* time every kernel launch with HIP events (clover_kernel_stats) */
+#define CLOVER_FLAG_PROFILE 2     /* time every kernel launch with HIP events (clover_kernel_stats);
+                                     implies CLOVER_FLAG_EAGER */
+#define CLOVER_FLAG_EAGER 4       /* launch the step's kernels one by one instead of replaying the
+                                     HIP graphs captured per batch size on first use */
 
 typedef struct clover_ctx clover_ctx;
 
@@ -191,6 +194,9 @@ typedef struct {
 } clover_kernel_stats;
 clover_status clover_kernel_stats_get(clover_ctx* ctx, int32_t kind, clover_kernel_stats* out);
 clover_status clover_kernel_stats_reset(clover_ctx* ctx);
+/* Replace the context's CLOVER_FLAG_* bits (e.g. switch per-launch profiling on for a
+ * measured pass and off again for graph replay). */
+clover_status clover_set_flags(clover_ctx* ctx, int32_t flags);
 
 /* ---- single-kernel entry points (parity tests at full size) ---------------------------
  * Each runs one hot-path kernel on caller buffers.  scratch: device memory of at least

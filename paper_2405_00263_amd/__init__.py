@@ -17,6 +17,7 @@ MAX_HEADS = 8
 STATUS = {0: "OK", 1: "INVALID_ARG", 2: "CAPACITY", 3: "STATE", 4: "BAD_TREE", 5: "DEVICE"}
 FLAG_KEEP_LOGITS = 1
 FLAG_PROFILE = 2
+FLAG_EAGER = 4
 KSTAT = {"gemm_verify": 0, "gemm_draft": 1, "attention": 2, "other": 3}
 
 
@@ -73,6 +74,7 @@ EXPORTS = {
     "clover_get_timings": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p]),
     "clover_kernel_stats_get": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p]),
     "clover_kernel_stats_reset": (ctypes.c_int, [ctypes.c_void_p]),
+    "clover_set_flags": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32]),
     "clover_op_scratch_bytes": (ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
     "clover_op_linear": (ctypes.c_int, [ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "clover_packed_matrix_bytes": (ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
@@ -268,6 +270,9 @@ class CloverEngine:
             _check(lib().clover_kernel_stats_get(self.ctx, k, ctypes.byref(st)), self.ctx)
             out[name] = dict(launches=st.launches, total_ms=st.total_ms, bytes=st.bytes, flops=st.flops)
         return out
+
+    def set_flags(self, flags: int):
+        _check(lib().clover_set_flags(self.ctx, int(flags)), self.ctx)
 
     def reset_kernel_stats(self):
         _check(lib().clover_kernel_stats_reset(self.ctx), self.ctx)

@@ -272,6 +272,12 @@ struct clover_ctx {
   struct Pending { int kind; size_t ev; double bytes, flops; };
   std::vector<Pending> pend;
   clover_kernel_stats kst[CLOVER_KSTAT_COUNT]{};
+  // captured step phases per batch size
+  struct StepGraphs { hipGraphExec_t draft = nullptr, verify = nullptr, accept = nullptr; };
+  std::vector<StepGraphs> graphs;
+  bool use_graphs = true;
+  hipStream_t cap_st = nullptr;  // private stream the phases are captured on (the caller's
+                                 // stream may be the legacy default stream, which cannot be)
 
   template <typename T> T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
 };
@@ -300,11 +306,11 @@ struct ProfScope {
       if (hipEventCreate(&e) != hipSuccess) { on = false; return; }
       c->pev.push_back(e);
     }
-    hipEventRecord(c->pev[i], c->st);
+    (void)hipEventRecord(c->pev[i], c->st);
     c->pend.push_back({kind, i, bytes, flops});
   }
   ~ProfScope() {
-    if (on) hipEventRecord(c->pev[c->pend.back().ev + 1], c->st);
+    if (on) (void)hipEventRecord(c->pev[c->pend.back().ev + 1], c->st);
   }
 };
 
@@ -437,14 +443,22 @@ clover_status ensure_blocks(clover_ctx* c, int slot, int upto) {
   return CLOVER_OK;
 }
 
-// verify + accept + commit for the batch in seq_ids (tree already in device buffers)
-clover_status verify_accept(clover_ctx* c, int B, int* out_tokens, int* out_count, int max_keys) {
+#define HE(expr)                        \
+  do {                                  \
+    hipError_t e_ = (expr);             \
+    if (e_ != hipSuccess) return e_;    \
+  } while (0)
+
+// Verify forward for the batch in seq_ids (tree already in device buffers): all target
+// layers over the tree, final norm, LM head, greedy argmax, then the Augmenting Block
+// over the tree.
+hipError_t enq_verify(clover_ctx* c, int B, int max_keys) {
   const clover_config& cf = c->cfg;
   const Layout& L = c->L;
-  const int T = L.T, M = B * T, d = cf.d_model, H = L.H;
+  const int T = L.T, M = B * T, d = cf.d_model;
   float* x = c->at<float>(L.x);
   float* xa = c->at<float>(L.xa);
-  HIPCK(c, launch_embed(cf.dtype, c->emb, c->at<int>(L.row_tok), M, d, x, c->st));
+  HE(launch_embed(cf.dtype, c->emb, c->at<int>(L.row_tok), M, d, x, c->st));
   AttnParams att{};
   att.seq_ids = c->at<int>(L.seq_ids);
   att.prefix_dev = c->at<int>(L.seq_len);
@@ -452,38 +466,47 @@ clover_status verify_accept(clover_ctx* c, int B, int* out_tokens, int* out_coun
   att.mask = c->at<uint64_t>(L.tree_mask); att.mask_words = L.W; att.mask_seq_stride = T * L.W;
   att.nbatch = B;
   int pend = 0;
-  for (int l = 0; l < cf.n_layers; ++l) HIPCK(c, run_layer(c, c->layers[l], l, x, M, att, max_keys, pend, &pend));
+  for (int l = 0; l < cf.n_layers; ++l) HE(run_layer(c, c->layers[l], l, x, M, att, max_keys, pend, &pend));
   // x_N = x + last partials; kept in xa for the Augmenting Block; final norm; LM head; argmax
   RowFixParams rf{};
   rf.M = M; rf.d = d; rf.part = c->at<float>(L.gpart); rf.S = pend; rf.ldp = d;
   rf.resid = x; rf.ldr = d; rf.out_f = x; rf.ldo = d; rf.out_copy_f = xa;
   rf.gain = c->final_norm; rf.eps = cf.rms_eps; rf.out_norm = c->at<void>(L.xn); rf.ldn = d;
   rf.zero_keys = c->at<unsigned long long>(L.amax_keys); rf.zero_n = M;
-  HIPCK(c, run_rowfix(c, rf));
+  HE(run_rowfix(c, rf));
   GemmParams lm{};
   lm.X = c->at<void>(L.xn); lm.ldx = d; lm.mode = EP_PARTIAL; lm.max_splits = 1;
   lm.part = c->at<float>(L.vlogits);
-  HIPCK(c, run_gemm(c, lm, M, d, {{c->lm_head, cf.vocab}}));
+  HE(run_gemm(c, lm, M, d, {{c->lm_head, cf.vocab}}));
   {
     ProfScope ps(c, CLOVER_KSTAT_OTHER, 0, 0);
-    HIPCK(c, launch_argmax(c->at<float>(L.vlogits), M, cf.vocab, c->at<int>(L.target),
-                           c->at<unsigned long long>(L.amax_keys), true, c->st));
+    HE(launch_argmax(c->at<float>(L.vlogits), M, cf.vocab, c->at<int>(L.target),
+                     c->at<unsigned long long>(L.amax_keys), true, c->st));
   }
   // Augmenting Block over the tree (tree mask, its own KV cache)
-  HIPCK(c, run_layer(c, c->layers[cf.n_layers], cf.n_layers, xa, M, att, max_keys, 0, &pend));
+  HE(run_layer(c, c->layers[cf.n_layers], cf.n_layers, xa, M, att, max_keys, 0, &pend));
   RowFixParams ra{};
   ra.M = M; ra.d = d; ra.part = c->at<float>(L.gpart); ra.S = pend; ra.ldp = d;
   ra.resid = xa; ra.ldr = d; ra.out_f = xa; ra.ldo = d;
-  HIPCK(c, run_rowfix(c, ra));
-  HIPCK(c, hipEventRecord(c->ev[2], c->st));
+  return run_rowfix(c, ra);
+}
+
+// Greedy acceptance, bonus token, h_0 for the next draft, KV compaction of every layer.
+hipError_t enq_accept(clover_ctx* c, int B) {
+  const clover_config& cf = c->cfg;
+  const Layout& L = c->L;
+  const int T = L.T, d = cf.d_model, H = L.H;
   AcceptParams ap{};
   ap.seq_ids = c->at<int>(L.seq_ids); ap.nbatch = B; ap.T = T; ap.H = H;
   ap.tree_token = c->at<int>(L.tree_token); ap.tree_parent = c->at<int>(L.tree_parent);
   ap.target = c->at<int>(L.target);
   ap.acc = c->at<int>(L.acc); ap.acc_len = c->at<int>(L.acc_len);
   ap.out_tokens = c->at<int>(L.out_tokens); ap.t0 = c->at<int>(L.t0);
-  ap.ab_out = xa; ap.d = d; ap.h0 = c->at<float>(L.h0);
-  HIPCK(c, launch_accept(ap, c->st));
+  ap.ab_out = c->at<float>(L.xa); ap.d = d; ap.h0 = c->at<float>(L.h0);
+  {
+    ProfScope ps(c, CLOVER_KSTAT_OTHER, 0, 0);
+    HE(launch_accept(ap, c->st));
+  }
   CompactParams cp{};
   cp.seq_ids = c->at<int>(L.seq_ids); cp.nbatch = B; cp.H = H;
   cp.acc = c->at<int>(L.acc); cp.acc_len = c->at<int>(L.acc_len); cp.seq_len = c->at<int>(L.seq_len);
@@ -491,7 +514,14 @@ clover_status verify_accept(clover_ctx* c, int B, int* out_tokens, int* out_coun
   cp.nlayers = cf.n_layers + 1;
   cp.block_table = c->at<int>(L.block_table); cp.max_blocks = L.mbps;
   cp.n_kv = cf.n_kv_heads; cp.hd = cf.head_dim;
-  HIPCK(c, launch_compact(cf.dtype, cp, c->st));
+  ProfScope ps(c, CLOVER_KSTAT_OTHER, 0, 0);
+  return launch_compact(cf.dtype, cp, c->st);
+}
+
+// Emitted tokens to the host, one stream sync, host mirrors and phase timings.
+clover_status finish_step(clover_ctx* c, int B, int* out_tokens, int* out_count) {
+  const Layout& L = c->L;
+  const int H = L.H;
   c->host_out.resize((size_t)B * (H + 1));
   HIPCK(c, hipMemcpyAsync(c->host_out.data(), c->at<int>(L.out_tokens), sizeof(int) * B * (H + 1),
                           hipMemcpyDeviceToHost, c->st));
@@ -515,6 +545,112 @@ clover_status verify_accept(clover_ctx* c, int B, int* out_tokens, int* out_coun
   if (hipEventElapsedTime(&ms, c->ev[0], c->ev[3]) == hipSuccess) c->tim.total_ms = ms;
   c->tim.steps++;
   return CLOVER_OK;
+}
+
+// Run one phase of the step: eagerly, or through a HIP graph captured on first use for
+// this batch size (the phase's launches depend only on the batch size; everything that
+// changes between steps is read from device memory).
+template <typename Fn>
+hipError_t run_phase(clover_ctx* c, hipGraphExec_t* slot, bool graph, Fn&& fn) {
+  if (!graph) return fn();
+  if (!*slot) {
+    hipError_t e = hipStreamBeginCapture(c->cap_st, hipStreamCaptureModeRelaxed);
+    if (e != hipSuccess) return e;
+    hipStream_t user = c->st;
+    c->st = c->cap_st;  // the phase enqueues on c->st
+    const hipError_t e2 = fn();
+    c->st = user;
+    hipGraph_t g = nullptr;
+    e = hipStreamEndCapture(c->cap_st, &g);
+    if (e2 != hipSuccess || e != hipSuccess) {
+      if (g) (void)hipGraphDestroy(g);
+      return e2 != hipSuccess ? e2 : e;
+    }
+    e = hipGraphInstantiate(slot, g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    if (e != hipSuccess) {
+      *slot = nullptr;
+      return e;
+    }
+  }
+  return hipGraphLaunch(*slot, c->st);
+}
+
+// Draft (Sec. 3): per depth, Attention Decoder on the frontier (Eq. 1-2), head MLP,
+// shared final norm + LM head, top-k children; then truncation into the verify tree.
+hipError_t enq_draft(clover_ctx* c, int B) {
+  const clover_config& cf = c->cfg;
+  const Layout& L = c->L;
+  const int d = cf.d_model, qd = cf.n_heads * cf.head_dim, H = L.H;
+  int* ids = c->at<int>(L.seq_ids);
+  int *ct = c->at<int>(L.cand_token), *cpar = c->at<int>(L.cand_parent), *cd = c->at<int>(L.cand_depth);
+  float* clp = c->at<float>(L.cand_lp);
+  HE(launch_set_root(ids, B, c->at<int>(L.t0), ct, cpar, cd, clp, L.NC, c->st));
+  for (int j = 1; j <= H; ++j) {
+    const int F = frontier(cf, j), M = B * F;
+    AdPrepParams ap{};
+    ap.use_slot_state = (j == 1);
+    ap.prev = (j == 1) ? c->at<float>(L.h0) : c->at<float>(L.dstate[j - 2]);
+    ap.Fprev = (j == 1) ? 1 : frontier(cf, j - 1);
+    ap.kprev = (j == 1) ? 1 : cf.topk[j - 2];
+    ap.seq_ids = ids; ap.nbatch = B; ap.F = F;
+    ap.cand_token = ct; ap.cand_stride = L.NC; ap.base_node = depth_base(cf, j - 1);
+    ap.lm_packed = c->lm_head; ap.lm_nchunks = d / kc_of(cf.dtype);
+    ap.ad_norm = c->ad_norm; ap.eps = cf.rms_eps; ap.d = d;
+    ap.hin = c->at<float>(L.d_hin); ap.a_out = c->at<void>(L.d_a); ap.e_out = c->at<void>(L.d_e);
+    HE(launch_ad_prep(cf.dtype, ap, c->st));
+    float* part = c->at<float>(L.gpart);
+    float* part2 = c->at<float>(L.gpart2);
+    int sq = 0, skv = 0, so = 0, sh = 0;
+    GemmParams q{};
+    q.X = c->at<void>(L.d_a); q.ldx = d; q.mode = EP_PARTIAL; q.max_splits = GEMM_MAX_SPLITS; q.part = part;
+    HE(run_gemm(c, q, M, d, {{c->ad_wq, qd}}, &sq));
+    GemmParams kv{};
+    kv.X = c->at<void>(L.d_e); kv.ldx = d; kv.mode = EP_PARTIAL; kv.max_splits = GEMM_MAX_SPLITS; kv.part = part2;
+    HE(run_gemm(c, kv, M, d, {{c->ad_wk, qd}, {c->ad_wv, qd}}, &skv));
+    HE(launch_ad_attn(cf.dtype, part, sq, part2, skv, M, cf.n_heads, cf.head_dim,
+                            c->at<void>(L.d_o), c->st));
+    GemmParams o{};
+    o.X = c->at<void>(L.d_o); o.ldx = qd; o.mode = EP_PARTIAL; o.max_splits = GEMM_MAX_SPLITS; o.part = part;
+    HE(run_gemm(c, o, M, qd, {{c->ad_wo, d}}, &so));
+    RowFixParams rs{};  // s = h + W_O attn (Eq. 2): fp32 state and storage copy for the MLP
+    rs.M = M; rs.d = d; rs.part = part; rs.S = so; rs.ldp = d;
+    rs.resid = c->at<float>(L.d_hin); rs.ldr = d;
+    rs.out_f = c->at<float>(L.dstate[j - 1]); rs.ldo = d; rs.out_copy_s = c->at<void>(L.d_sst);
+    HE(run_rowfix(c, rs));
+    GemmParams hm{};
+    hm.X = c->at<void>(L.d_sst); hm.ldx = d; hm.mode = EP_PARTIAL; hm.max_splits = GEMM_MAX_SPLITS; hm.part = part;
+    HE(run_gemm(c, hm, M, d, {{c->head_w1[j - 1], d}}, &sh));
+    RowFixParams rh{};  // r = s + SiLU(W1 s + b1), then the shared final norm
+    rh.M = M; rh.d = d; rh.part = part; rh.S = sh; rh.ldp = d;
+    rh.resid = c->at<float>(L.dstate[j - 1]); rh.ldr = d; rh.act = 1; rh.bias = c->head_b1[j - 1];
+    rh.out_f = c->at<float>(L.d_r); rh.ldo = d;
+    rh.gain = c->final_norm; rh.eps = cf.rms_eps; rh.out_norm = c->at<void>(L.d_rn); rh.ldn = d;
+    HE(run_rowfix(c, rh));
+    GemmParams lm{};
+    lm.X = c->at<void>(L.d_rn); lm.ldx = d; lm.mode = EP_PARTIAL; lm.max_splits = 1;
+    lm.part = c->at<float>(L.dlogits[j - 1]);
+    HE(run_gemm(c, lm, M, d, {{c->lm_head, cf.vocab}}));
+    TopkParams tp{};
+    tp.logits = c->at<float>(L.dlogits[j - 1]); tp.M = M; tp.V = cf.vocab; tp.k = cf.topk[j - 1];
+    tp.seq_ids = ids; tp.F = F;
+    tp.cand_token = ct; tp.cand_parent = cpar; tp.cand_depth = cd; tp.cand_lp = clp; tp.cand_stride = L.NC;
+    tp.base_parent = depth_base(cf, j - 1); tp.base_child = depth_base(cf, j); tp.depth = j;
+    tp.scratch = c->at<float>(L.topk_scratch);
+    HE(launch_topk(tp, c->st));
+  }
+  TreeParams tr{};
+  tr.seq_ids = ids; tr.nbatch = B;
+  tr.cand_token = ct; tr.cand_parent = cpar; tr.cand_depth = cd; tr.cand_lp = clp;
+  tr.cand_stride = L.NC; tr.n_cand = L.NC; tr.T = L.T; tr.mask_words = L.W;
+  tr.seq_len = c->at<int>(L.seq_len);
+  tr.tree_token = c->at<int>(L.tree_token); tr.tree_parent = c->at<int>(L.tree_parent);
+  tr.tree_depth = c->at<int>(L.tree_depth); tr.tree_pos = c->at<int>(L.tree_pos);
+  tr.tree_mask = c->at<uint64_t>(L.tree_mask);
+  tr.row_tok = c->at<int>(L.row_tok); tr.row_pos = c->at<int>(L.row_pos);
+  tr.row_slot = c->at<int>(L.row_slot); tr.row_seq = c->at<int>(L.row_seq);
+  HE(launch_tree_build(tr, c->st));
+  return hipSuccess;
 }
 
 clover_status check_ctx(clover_ctx* c) {
@@ -679,6 +815,8 @@ clover_status clover_init(const clover_config* cfg, void* const* weights, void* 
     c->head_b1.push_back(c->w[k++]);
   }
   c->profile = (cfg->flags & CLOVER_FLAG_PROFILE) != 0;
+  c->use_graphs = !c->profile && !(cfg->flags & CLOVER_FLAG_EAGER);
+  c->graphs.resize(cfg->max_batch + 1);
   c->seq_len.assign(cfg->max_batch, -1);
   c->seq_blocks.assign(cfg->max_batch, {});
   for (int b = L.nblocks - 1; b >= 0; --b) c->free_blocks.push_back(b);
@@ -691,6 +829,7 @@ clover_status clover_init(const clover_config* cfg, void* const* weights, void* 
   hipError_t e;
   for (int i = 0; i < 4; ++i)
     if ((e = hipEventCreate(&c->ev[i])) != hipSuccess) return fail(e, "event");
+  if ((e = hipStreamCreateWithFlags(&c->cap_st, hipStreamNonBlocking)) != hipSuccess) return fail(e, "capture stream");
   // zero the KV pools (attention reads whole 16-key blocks), counters and state
   if ((e = hipMemsetAsync(c->ws, 0, L.pool_ptrs, c->st)) != hipSuccess) return fail(e, "memset pools");
   if ((e = hipMemsetAsync(c->ws + L.block_table, 0, L.x - L.block_table, c->st)) != hipSuccess) return fail(e, "memset state");
@@ -709,9 +848,13 @@ clover_status clover_init(const clover_config* cfg, void* const* weights, void* 
 
 void clover_destroy(clover_ctx* ctx) {
   if (!ctx) return;
-  hipStreamSynchronize(ctx->st);
-  for (int i = 0; i < 4; ++i) hipEventDestroy(ctx->ev[i]);
-  for (auto e : ctx->pev) hipEventDestroy(e);
+  (void)hipStreamSynchronize(ctx->st);
+  for (int i = 0; i < 4; ++i) (void)hipEventDestroy(ctx->ev[i]);
+  for (auto e : ctx->pev) (void)hipEventDestroy(e);
+  for (auto& g : ctx->graphs)
+    for (hipGraphExec_t x : {g.draft, g.verify, g.accept})
+      if (x) (void)hipGraphExecDestroy(x);
+  if (ctx->cap_st) (void)hipStreamDestroy(ctx->cap_st);
   delete ctx;
 }
 
@@ -814,81 +957,18 @@ clover_status clover_step(clover_ctx* c, const int32_t* seqs, int32_t n_seqs, in
   const int B = n_seqs, d = cf.d_model, qd = cf.n_heads * cf.head_dim, H = L.H;
   int max_keys = 0;
   if ((s = begin_batch(c, seqs, B, max_keys))) return s;
+  const bool graph = c->use_graphs;
   HIPCK(c, hipEventRecord(c->ev[0], c->st));
   c->in_step = true;
   c->phase = CLOVER_KSTAT_GEMM_DRAFT;
-  int* ids = c->at<int>(L.seq_ids);
-  int *ct = c->at<int>(L.cand_token), *cpar = c->at<int>(L.cand_parent), *cd = c->at<int>(L.cand_depth);
-  float* clp = c->at<float>(L.cand_lp);
-  HIPCK(c, launch_set_root(ids, B, c->at<int>(L.t0), ct, cpar, cd, clp, L.NC, c->st));
-  for (int j = 1; j <= H; ++j) {
-    const int F = frontier(cf, j), M = B * F;
-    AdPrepParams ap{};
-    ap.use_slot_state = (j == 1);
-    ap.prev = (j == 1) ? c->at<float>(L.h0) : c->at<float>(L.dstate[j - 2]);
-    ap.Fprev = (j == 1) ? 1 : frontier(cf, j - 1);
-    ap.kprev = (j == 1) ? 1 : cf.topk[j - 2];
-    ap.seq_ids = ids; ap.nbatch = B; ap.F = F;
-    ap.cand_token = ct; ap.cand_stride = L.NC; ap.base_node = depth_base(cf, j - 1);
-    ap.lm_packed = c->lm_head; ap.lm_nchunks = d / kc_of(cf.dtype);
-    ap.ad_norm = c->ad_norm; ap.eps = cf.rms_eps; ap.d = d;
-    ap.hin = c->at<float>(L.d_hin); ap.a_out = c->at<void>(L.d_a); ap.e_out = c->at<void>(L.d_e);
-    HIPCK(c, launch_ad_prep(cf.dtype, ap, c->st));
-    float* part = c->at<float>(L.gpart);
-    float* part2 = c->at<float>(L.gpart2);
-    int sq = 0, skv = 0, so = 0, sh = 0;
-    GemmParams q{};
-    q.X = c->at<void>(L.d_a); q.ldx = d; q.mode = EP_PARTIAL; q.max_splits = GEMM_MAX_SPLITS; q.part = part;
-    HIPCK(c, run_gemm(c, q, M, d, {{c->ad_wq, qd}}, &sq));
-    GemmParams kv{};
-    kv.X = c->at<void>(L.d_e); kv.ldx = d; kv.mode = EP_PARTIAL; kv.max_splits = GEMM_MAX_SPLITS; kv.part = part2;
-    HIPCK(c, run_gemm(c, kv, M, d, {{c->ad_wk, qd}, {c->ad_wv, qd}}, &skv));
-    HIPCK(c, launch_ad_attn(cf.dtype, part, sq, part2, skv, M, cf.n_heads, cf.head_dim,
-                            c->at<void>(L.d_o), c->st));
-    GemmParams o{};
-    o.X = c->at<void>(L.d_o); o.ldx = qd; o.mode = EP_PARTIAL; o.max_splits = GEMM_MAX_SPLITS; o.part = part;
-    HIPCK(c, run_gemm(c, o, M, qd, {{c->ad_wo, d}}, &so));
-    RowFixParams rs{};  // s = h + W_O attn (Eq. 2): fp32 state and storage copy for the MLP
-    rs.M = M; rs.d = d; rs.part = part; rs.S = so; rs.ldp = d;
-    rs.resid = c->at<float>(L.d_hin); rs.ldr = d;
-    rs.out_f = c->at<float>(L.dstate[j - 1]); rs.ldo = d; rs.out_copy_s = c->at<void>(L.d_sst);
-    HIPCK(c, run_rowfix(c, rs));
-    GemmParams hm{};
-    hm.X = c->at<void>(L.d_sst); hm.ldx = d; hm.mode = EP_PARTIAL; hm.max_splits = GEMM_MAX_SPLITS; hm.part = part;
-    HIPCK(c, run_gemm(c, hm, M, d, {{c->head_w1[j - 1], d}}, &sh));
-    RowFixParams rh{};  // r = s + SiLU(W1 s + b1), then the shared final norm
-    rh.M = M; rh.d = d; rh.part = part; rh.S = sh; rh.ldp = d;
-    rh.resid = c->at<float>(L.dstate[j - 1]); rh.ldr = d; rh.act = 1; rh.bias = c->head_b1[j - 1];
-    rh.out_f = c->at<float>(L.d_r); rh.ldo = d;
-    rh.gain = c->final_norm; rh.eps = cf.rms_eps; rh.out_norm = c->at<void>(L.d_rn); rh.ldn = d;
-    HIPCK(c, run_rowfix(c, rh));
-    GemmParams lm{};
-    lm.X = c->at<void>(L.d_rn); lm.ldx = d; lm.mode = EP_PARTIAL; lm.max_splits = 1;
-    lm.part = c->at<float>(L.dlogits[j - 1]);
-    HIPCK(c, run_gemm(c, lm, M, d, {{c->lm_head, cf.vocab}}));
-    TopkParams tp{};
-    tp.logits = c->at<float>(L.dlogits[j - 1]); tp.M = M; tp.V = cf.vocab; tp.k = cf.topk[j - 1];
-    tp.seq_ids = ids; tp.F = F;
-    tp.cand_token = ct; tp.cand_parent = cpar; tp.cand_depth = cd; tp.cand_lp = clp; tp.cand_stride = L.NC;
-    tp.base_parent = depth_base(cf, j - 1); tp.base_child = depth_base(cf, j); tp.depth = j;
-    tp.scratch = c->at<float>(L.topk_scratch);
-    HIPCK(c, launch_topk(tp, c->st));
-  }
-  TreeParams tr{};
-  tr.seq_ids = ids; tr.nbatch = B;
-  tr.cand_token = ct; tr.cand_parent = cpar; tr.cand_depth = cd; tr.cand_lp = clp;
-  tr.cand_stride = L.NC; tr.n_cand = L.NC; tr.T = L.T; tr.mask_words = L.W;
-  tr.seq_len = c->at<int>(L.seq_len);
-  tr.tree_token = c->at<int>(L.tree_token); tr.tree_parent = c->at<int>(L.tree_parent);
-  tr.tree_depth = c->at<int>(L.tree_depth); tr.tree_pos = c->at<int>(L.tree_pos);
-  tr.tree_mask = c->at<uint64_t>(L.tree_mask);
-  tr.row_tok = c->at<int>(L.row_tok); tr.row_pos = c->at<int>(L.row_pos);
-  tr.row_slot = c->at<int>(L.row_slot); tr.row_seq = c->at<int>(L.row_seq);
-  HIPCK(c, launch_tree_build(tr, c->st));
+  HIPCK(c, run_phase(c, &c->graphs[B].draft, graph, [&] { return enq_draft(c, B); }));
   HIPCK(c, hipEventRecord(c->ev[1], c->st));
-  c->last_nbatch = B;
   c->phase = CLOVER_KSTAT_GEMM_VERIFY;
-  s = verify_accept(c, B, out_tokens, out_count, max_keys);
+  HIPCK(c, run_phase(c, &c->graphs[B].verify, graph, [&] { return enq_verify(c, B, max_keys); }));
+  HIPCK(c, hipEventRecord(c->ev[2], c->st));
+  HIPCK(c, run_phase(c, &c->graphs[B].accept, graph, [&] { return enq_accept(c, B); }));
+  c->last_nbatch = B;
+  s = finish_step(c, B, out_tokens, out_count);
   c->in_step = false;
   return s;
 }
@@ -955,7 +1035,10 @@ clover_status clover_verify_tree(clover_ctx* c, int32_t seq, const int32_t* toke
   c->last_nbatch = 1;
   c->in_step = true;
   c->phase = CLOVER_KSTAT_GEMM_VERIFY;
-  s = verify_accept(c, 1, out_tokens, out_count, max_keys);
+  HIPCK(c, enq_verify(c, 1, max_keys));
+  HIPCK(c, hipEventRecord(c->ev[2], c->st));
+  HIPCK(c, enq_accept(c, 1));
+  s = finish_step(c, 1, out_tokens, out_count);
   c->in_step = false;
   return s;
 }
@@ -1043,6 +1126,17 @@ clover_status clover_kernel_stats_get(clover_ctx* c, int32_t kind, clover_kernel
   if (s) return s;
   if (!out || kind < 0 || kind >= CLOVER_KSTAT_COUNT) return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "bad kernel class");
   *out = c->kst[kind];
+  return CLOVER_OK;
+}
+
+clover_status clover_set_flags(clover_ctx* c, int32_t flags) {
+  clover_status s = check_ctx(c);
+  if (s) return s;
+  if (flags & ~(CLOVER_FLAG_KEEP_LOGITS | CLOVER_FLAG_PROFILE | CLOVER_FLAG_EAGER))
+    return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
+  c->cfg.flags = flags;
+  c->profile = (flags & CLOVER_FLAG_PROFILE) != 0;
+  c->use_graphs = !c->profile && !(flags & CLOVER_FLAG_EAGER);
   return CLOVER_OK;
 }
 

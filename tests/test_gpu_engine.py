@@ -224,3 +224,31 @@ def test_bf16_small_model_within_tolerance():
         if np.min(top2[:, 1] - top2[:, 0]) < 2 * tol:
             break
         assert ours == ref, step
+
+
+def test_graph_replay_matches_eager_launches():
+    """The step's phases replay as HIP graphs captured per batch size; every replay,
+    with host work and batch-size changes in between, matches eager launches bit for bit."""
+    P = need_gpu()
+    note("engine graph vs eager")
+    cfg, w = _tiny(batch=2)
+    prompts = [synth.make_prompt(cfg, seq=s, n=100 + 30 * s) for s in range(2)]
+    g = _engine(P, cfg, w)
+    e = _engine(P, cfg, w, flags=P.FLAG_EAGER)
+    for s in range(2):
+        assert g.prefill(s, prompts[s]) == e.prefill(s, prompts[s])
+    schedule = [[0], [0, 1], [1], [0, 1], [0], [1, 0], [0, 1]]
+    for i, seqs in enumerate(schedule):
+        if i == 3:
+            g.set_flags(P.FLAG_EAGER)      # eager in the middle, graphs again after
+        if i == 5:
+            g.set_flags(0)
+        a, b = g.step(seqs), e.step(seqs)
+        assert a == b, (i, seqs, a, b)
+        rows = len(seqs) * cfg.tree_tokens
+        va = g.debug("verify_logits", np.float32, (rows, cfg.vocab))
+        vb = e.debug("verify_logits", np.float32, (rows, cfg.vocab))
+        assert np.array_equal(va, vb), i
+        assert np.array_equal(g.debug("h0", np.float32, (2, cfg.d_model)), e.debug("h0", np.float32, (2, cfg.d_model)))
+        torch.cuda.synchronize()
+    assert g.seq_len(0) == e.seq_len(0) and g.seq_len(1) == e.seq_len(1)
