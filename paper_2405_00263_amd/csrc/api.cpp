@@ -129,6 +129,7 @@ bool check_config(const clover_config* c, std::string& why) {
   if (c->max_batch < 1 || c->max_batch > 256) return fail("max_batch must be 1..256");
   if (c->kv_block != 16) return fail("kv_block must be 16");
   if (c->max_context < c->tree_tokens + 1) return fail("max_context must exceed tree_tokens");
+  if (c->max_context > 65536) return fail("max_context must be at most 65536");
   if (c->prefill_chunk < 0 || c->prefill_chunk % 64) return fail("prefill_chunk must be a multiple of 64");
   if ((int64_t)c->max_batch * frontier(*c, c->n_spec_heads) > 4096) return fail("draft frontier too large");
   (void)buf;
@@ -1213,7 +1214,7 @@ clover_status clover_op_linear(int32_t dtype, const void* X, int32_t M, int32_t 
 
 size_t clover_op_attention_scratch_bytes(int32_t dtype, int32_t L, int32_t T, int32_t n_heads,
                                          int32_t n_kv, int32_t head_dim) {
-  if ((dtype != 0 && dtype != 1) || L < 0 || T < 1 || n_heads < 1 || n_kv < 1 || n_heads % n_kv ||
+  if ((dtype != 0 && dtype != 1) || L < 0 || T < 1 || L + T > 65536 || n_heads < 1 || n_kv < 1 || n_heads % n_kv ||
       (head_dim != 32 && head_dim != 64 && head_dim != 128))
     return 0;
   const int nblocks = (L + T + 15) / 16;

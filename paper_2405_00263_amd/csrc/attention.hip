@@ -17,6 +17,7 @@ namespace clover {
 
 static constexpr int ATT_WAVES = 8;              // key splits inside a workgroup
 static constexpr int ATT_THREADS = ATT_WAVES * 64;
+static constexpr int ATT_MAX_BLOCKS = 4096;    // 65536 keys
 
 __device__ __forceinline__ f32x4_t mma_pv(u32x2_t v, const float p[4], f32x4_t c, bf16_t) {
   u32x2_t pb;
@@ -61,6 +62,7 @@ template <typename S, int HD>
 __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(const AttnParams p) {
   using T = St<S>;
   constexpr int EPL = T::EPL, KC = 4 * EPL, NQC = HD / KC, NT = HD / 16;
+  constexpr int ATT_RING = sizeof(S) == 2 ? 3 : 2;  // 16-key blocks in flight per wave
   __shared__ float s_m[ATT_WAVES][16], s_l[ATT_WAVES][16];
   __shared__ float s_o[ATT_WAVES][16][HD + 4];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, j = lane & 15;
@@ -101,13 +103,18 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(const AttnParams p) {
 
   const S* kc = reinterpret_cast<const S*>(p.kcache);
   const S* vc = reinterpret_cast<const S*>(p.vcache);
+  // the sequence's block-table row, staged in LDS so no K/V load waits on a table load
+  __shared__ int s_bt[ATT_MAX_BLOCKS];
   const int* bt = p.block_table + (size_t)slot * p.max_blocks;
-  auto base_of = [&](int kb) { return ((size_t)bt[kb] * p.n_kv + kvh) * (size_t)(16 * HD); };
-  KVBlock<S, HD> cur, nxt;
-  int kb = wave;
-  if (kb < nblocks) cur.load(kc, vc, base_of(kb), lane);
-  for (; kb < nblocks; kb += ATT_WAVES) {
-    if (kb + ATT_WAVES < nblocks) nxt.load(kc, vc, base_of(kb + ATT_WAVES), lane);
+  for (int i = threadIdx.x; i < nblocks; i += ATT_THREADS) s_bt[i] = bt[i];
+  __syncthreads();
+  auto base_of = [&](int kb) { return ((size_t)s_bt[kb] * p.n_kv + kvh) * (size_t)(16 * HD); };
+
+  // this wave's blocks: kb = wave + ATT_WAVES * i, i < nmine; a ring of RB blocks in
+  // flight, each slot reloaded (clamped, unconditionally) right after it is consumed
+  const int nmine = wave < nblocks ? (nblocks - wave + ATT_WAVES - 1) / ATT_WAVES : 0;
+  auto blk = [&](int i) { return wave + ATT_WAVES * min(i, nmine - 1); };
+  auto consume = [&](const KVBlock<S, HD>& cur, int kb) {
     f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int c = 0; c < NQC; ++c) s = mma_frag(cur.k[c], qf[c], s, S{});
@@ -147,7 +154,22 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(const AttnParams p) {
       o[t] *= alpha;
       o[t] = mma_pv(cur.v[t], pr, o[t], S{});
     }
-    cur = nxt;
+  };
+  if (nmine > 0) {
+    KVBlock<S, HD> ring[ATT_RING];
+#pragma unroll
+    for (int r = 0; r < ATT_RING; ++r) ring[r].load(kc, vc, base_of(blk(r)), lane);
+    const int nfull = nmine / ATT_RING;
+    for (int i0 = 0; i0 < nfull * ATT_RING; i0 += ATT_RING) {  // branch-free steady state
+#pragma unroll
+      for (int r = 0; r < ATT_RING; ++r) {
+        consume(ring[r], wave + ATT_WAVES * (i0 + r));
+        ring[r].load(kc, vc, base_of(blk(i0 + r + ATT_RING)), lane);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < ATT_RING; ++r)  // tail
+      if (nfull * ATT_RING + r < nmine) consume(ring[r], wave + ATT_WAVES * (nfull * ATT_RING + r));
   }
   // merge the waves' states
   if (g == 0) {

@@ -63,7 +63,8 @@ __host__ __device__ __forceinline__ int rope_tile(int p) {
 }
 
 template <typename S>
-__device__ void gemm_epilogue(const GemmParams& p, const float* tile, int g, int m0, int mrows) {
+__device__ void gemm_epilogue(const GemmParams& p, const float* tile, int g, int m0, int mrows,
+                              const int* s_pos, const int* s_kvbase) {
   using T = St<S>;
   const int tid = threadIdx.x;
   constexpr int COLS = GEMM_WAVES * 16;
@@ -103,7 +104,7 @@ __device__ void gemm_epilogue(const GemmParams& p, const float* tile, int g, int
     float v = tile[r * TILE_STRIDE + col];
     if (rot) {
       const float partner = tile[r * TILE_STRIDE + pc];
-      double ang = (double)p.row_pos[m] * inv;
+      double ang = (double)s_pos[r] * inv;
       ang -= 6.283185307179586 * rint(ang * 0.15915494309189535);
       float sn, cs;
       sincosf((float)ang, &sn, &cs);
@@ -114,9 +115,9 @@ __device__ void gemm_epilogue(const GemmParams& p, const float* tile, int g, int
     } else {
       const bool isk = n < qd + kvd;
       const int kvh = (isk ? n - qd : n - qd - kvd) / hd;
-      const int seq = p.row_seq[m], slot = p.row_slot[m];
-      const size_t base = kv_block_base(p.block_table, p.max_blocks, seq, slot, kvh, p.n_kv, hd);
-      const int key = slot & 15;
+      const int kb = s_kvbase[r];  // physical block * 16 + key
+      const size_t base = ((size_t)(kb >> 4) * p.n_kv + kvh) * (size_t)(16 * hd);
+      const int key = kb & 15;
       if (isk)
         reinterpret_cast<S*>(p.kcache)[base + kblk_off(key, d, T::EPL)] = T::from_f(v);
       else
@@ -143,6 +144,16 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(const GemmParams p) 
   const int c1 = min(p.nchunks, c0 + p.cps);
   const int nk = c1 - c0;
   const int nst = (nk + STAGE_CHUNKS - 1) / STAGE_CHUNKS;
+
+  // row metadata of the fused rotary + KV-append epilogue, loaded once up front so the
+  // epilogue's row loop has no dependent global loads
+  __shared__ int s_pos[MROWS], s_kvbase[MROWS];
+  if (p.mode == EP_QKV && threadIdx.x < MROWS) {
+    const int m = min(m0 + (int)threadIdx.x, p.M - 1);
+    const int slot = p.row_slot[m];
+    s_pos[threadIdx.x] = p.row_pos[m];
+    s_kvbase[threadIdx.x] = p.block_table[(size_t)p.row_seq[m] * p.max_blocks + (slot >> 4)] * 16 + (slot & 15);
+  }
 
   bool active;
   const u32x4_t* wp = wave_weight_ptr<S>(p, g, wave, active);
@@ -258,7 +269,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(const GemmParams p) 
 #pragma unroll
     for (int r = 0; r < 4; ++r) tile[(t * 16 + 4 * (lane >> 4) + r) * TILE_STRIDE + col] = acc[t][r];
   __syncthreads();
-  gemm_epilogue<S>(p, tile, g, m0, MROWS);
+  gemm_epilogue<S>(p, tile, g, m0, MROWS, s_pos, s_kvbase);
 }
 
 // ---- host side ------------------------------------------------------------------------
