@@ -296,10 +296,14 @@ clover_status ctx_fail(clover_ctx* c, clover_status s, const char* fmt, ...) {
 }
 
 // ---- per-launch timing ---------------------------------------------------------------
+// Marker events around the scope's launches; with `kernel_events` the scope holds a single
+// launch that records the pair itself from the kernel's own start and end (see timing()).
 struct ProfScope {
   clover_ctx* c;
-  bool on;
-  ProfScope(clover_ctx* c_, int kind, double bytes, double flops) : c(c_), on(c_->profile && c_->in_step) {
+  bool on, kev;
+  LaunchTiming lt{};
+  ProfScope(clover_ctx* c_, int kind, double bytes, double flops, bool kernel_events = false)
+      : c(c_), on(c_->profile && c_->in_step), kev(kernel_events) {
     if (!on) return;
     const size_t i = c->pend.size() * 2;
     while (c->pev.size() < i + 2) {
@@ -307,11 +311,13 @@ struct ProfScope {
       if (hipEventCreate(&e) != hipSuccess) { on = false; return; }
       c->pev.push_back(e);
     }
-    (void)hipEventRecord(c->pev[i], c->st);
+    lt = {c->pev[i], c->pev[i + 1]};
+    if (!kev) (void)hipEventRecord(lt.start, c->st);
     c->pend.push_back({kind, i, bytes, flops});
   }
+  const LaunchTiming* timing() const { return on && kev ? &lt : nullptr; }
   ~ProfScope() {
-    if (on) (void)hipEventRecord(c->pev[c->pend.back().ev + 1], c->st);
+    if (on && !kev) (void)hipEventRecord(lt.stop, c->st);
   }
 };
 
@@ -356,8 +362,8 @@ hipError_t run_gemm(clover_ctx* c, GemmParams p, int M, int K,
   const double ybytes = (p.mode == EP_PARTIAL ? 4.0 : es) * M * p.N;
   hipError_t e;
   {
-    ProfScope ps(c, c->phase, rows * K * es + es * M * K + ybytes, 2.0 * M * rows * K);
-    e = launch_gemm(c->cfg.dtype, p, c->st);
+    ProfScope ps(c, c->phase, rows * K * es + es * M * K + ybytes, 2.0 * M * rows * K, true);
+    e = launch_gemm(c->cfg.dtype, p, c->st, ps.timing());
   }
   if (splits) *splits = p.S;
   return e;
@@ -406,8 +412,8 @@ hipError_t run_layer(clover_ctx* c, const LayerPtrs& lw, int layer_idx, float* x
     const double keys = (double)max_keys;  // upper bound over the batch
     ProfScope ps(c, CLOVER_KSTAT_ATTENTION,
                  att.nbatch * (2.0 * keys * kvd * es + 2.0 * att.nq * qd * es),
-                 att.nbatch * 4.0 * att.nq * keys * hd * cf.n_heads);
-    if ((e = launch_attention(cf.dtype, att, max_keys, c->st))) return e;
+                 att.nbatch * 4.0 * att.nq * keys * hd * cf.n_heads, true);
+    if ((e = launch_attention(cf.dtype, att, max_keys, c->st, ps.timing()))) return e;
   }
   GemmParams o{};
   o.X = c->at<void>(L.obuf); o.ldx = qd; o.mode = EP_PARTIAL; o.max_splits = GEMM_MAX_SPLITS; o.part = part;
@@ -757,7 +763,7 @@ clover_status clover_pack_weight(const clover_config* cfg, size_t i, const void*
   const bool qk = nm.rfind("ad.", 0) != 0 && nm.size() > 3 &&
                   (nm.compare(nm.size() - 3, 3, ".wq") == 0 || nm.compare(nm.size() - 3, 3, ".wk") == 0);
   if (s[i].matrix)
-    e = launch_pack(cfg->dtype, src, (int)s[i].rows, (int)s[i].cols, dst, qk && cfg->head_dim == 128, st);
+    e = launch_pack(cfg->dtype, src, (int)s[i].rows, (int)s[i].cols, dst, qk ? cfg->head_dim : 0, st);
   else
     e = hipMemcpyAsync(dst, src, clover_packed_bytes(cfg, i), hipMemcpyDeviceToDevice, st);
   if (e != hipSuccess) {
@@ -1171,7 +1177,7 @@ clover_status clover_pack_matrix(int32_t dtype, const void* src, int32_t rows, i
     set_global_err("pack_matrix: bad arguments");
     return CLOVER_ERR_INVALID_ARG;
   }
-  hipError_t e = launch_pack(dtype, src, rows, cols, dst, false, (hipStream_t)hip_stream);
+  hipError_t e = launch_pack(dtype, src, rows, cols, dst, 0, (hipStream_t)hip_stream);
   if (e != hipSuccess) {
     set_global_err("pack_matrix: %s", hipGetErrorString(e));
     return CLOVER_ERR_DEVICE;

@@ -11,6 +11,8 @@
 #include "common.h"
 #include "kernels.h"
 
+#include <hip/hip_ext.h>
+
 #include <algorithm>
 
 namespace clover {
@@ -211,22 +213,32 @@ void plan_attention(AttnParams& p, int max_keys) {
 size_t attention_part_floats(int, int, int, int, int) { return 0; }
 
 template <typename S>
-static hipError_t launch_attn_t(AttnParams& p, hipStream_t st) {
+static hipError_t launch_attn_t(AttnParams& p, hipStream_t st, const LaunchTiming* lt) {
   const int items = p.nbatch * p.n_heads;
   dim3 grid(8 * ((items + 7) / 8) * p.qtiles), block(ATT_THREADS);
+  auto go = [&](auto kern) {
+    if (lt) hipExtLaunchKernelGGL(kern, grid, block, 0, st, lt->start, lt->stop, 0, p);
+    else hipLaunchKernelGGL(kern, grid, block, 0, st, p);
+  };
   switch (p.hd) {
-    case 32: hipLaunchKernelGGL((attn_kernel<S, 32>), grid, block, 0, st, p); break;
-    case 64: hipLaunchKernelGGL((attn_kernel<S, 64>), grid, block, 0, st, p); break;
-    case 128: hipLaunchKernelGGL((attn_kernel<S, 128>), grid, block, 0, st, p); break;
+    case 32: go(attn_kernel<S, 32>); break;
+    case 64: go(attn_kernel<S, 64>); break;
+    case 128: go(attn_kernel<S, 128>); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_attention(int dtype, AttnParams& p, int max_keys, hipStream_t st) {
+hipError_t launch_attention(int dtype, AttnParams& p, int max_keys, hipStream_t st, const LaunchTiming* lt) {
   plan_attention(p, max_keys);
-  if (p.nq <= 0 || p.nbatch <= 0) return hipSuccess;
-  return dtype == 1 ? launch_attn_t<bf16_t>(p, st) : launch_attn_t<float>(p, st);
+  if (p.nq <= 0 || p.nbatch <= 0) {  // nothing to launch: an empty timed interval
+    if (lt) {
+      (void)hipEventRecord(lt->start, st);
+      (void)hipEventRecord(lt->stop, st);
+    }
+    return hipSuccess;
+  }
+  return dtype == 1 ? launch_attn_t<bf16_t>(p, st, lt) : launch_attn_t<float>(p, st, lt);
 }
 
 }  // namespace clover

@@ -1,7 +1,7 @@
 // Weight-streaming GEMM for small M on gfx950 matrix cores.
 //
-//   Y[M][N] = X[M][K] * W[N][K]^T, fused epilogues (residual, rotary + KV append,
-//   SwiGLU, head MLP).
+//   Y[M][N] = X[M][K] * W[N][K]^T, fused epilogues (rotary + KV append, SwiGLU) or
+//   fp32 split-K partials.
 //
 // Decoding streams every weight once per forward while only M (= tree tokens) rows
 // use it, so the kernel is bound by HBM bandwidth (Sec. 1 of the paper: decoding is
@@ -9,12 +9,16 @@
 //  * weights are pre-tiled (packed_index) so one wave's 16-byte-per-lane load of a
 //    16 x KC fragment is 1 KB of contiguous memory, streamed with non-temporal loads
 //    and a register prefetch ring;
-//  * a workgroup is 4 waves, one 16-row weight tile each (64 output columns), all
-//    sharing the X tile, which is staged through LDS in double-buffered stages; X is
-//    prefetched into registers as many stages ahead as the weight ring, so waiting for
-//    an X load never forces younger weight loads to land (loads complete in order);
-//  * Q/K weights of 128-wide heads are packed with their rotary halves interleaved by
-//    16-row tiles, so a 64-row group holds complete rotary pairs;
+//  * a workgroup is NW waves (2..8), one 16-row weight tile each, all sharing the X
+//    tile, which is staged through LDS in double-buffered stages; X is prefetched into
+//    registers as many stages ahead as the weight ring, so waiting for an X load never
+//    forces younger weight loads to land (loads complete in order);
+//  * on gfx950 a compute unit moves roughly 40-50 GB/s of weight plus X bytes in this
+//    loop, so the planner picks NW and the K split per shape to keep every CU busy with
+//    one workgroup while keeping the X bytes per weight byte low (plan_gemm);
+//  * Q/K weights are packed so that each 16-row tile holds 8 rows of the first rotary
+//    half and their 8 partners of the second half: the rotary epilogue is tile-local and
+//    any NW works;
 //  * K may be split over workgroups (EP_PARTIAL): each split writes its own fp32
 //    partial [split][M][N] and the consumer kernel sums them in split order, so the
 //    result does not depend on scheduling and no cross-workgroup synchronisation (and
@@ -24,28 +28,36 @@
 #include "common.h"
 #include "kernels.h"
 
+#include <hip/hip_ext.h>
+
 #include <algorithm>
+#include <cmath>
 
 namespace clover {
 
-static constexpr int GEMM_WAVES = 4;
-static constexpr int GEMM_THREADS = GEMM_WAVES * 64;
 static constexpr int STAGE_CHUNKS = 4;   // chunks of X per LDS stage
 static constexpr int PF = 16;            // weight fragments in flight per wave (16 KB)
-static constexpr int TILE_STRIDE = 68;   // floats per row of the 64-column epilogue tile
-static constexpr int TARGET_WGS = 256;
 static constexpr int RING = PF / STAGE_CHUNKS;  // stages covered by the prefetch ring
+static_assert(RING % 2 == 0, "stages alternate between two LDS buffers inside a superstage");
 
-template <typename S>
+// source row of row r of physical tile t in a Q/K weight packed with tile-local rotary
+// pairs: rows 0..7 are dims q*8.. of the first half of a head, rows 8..15 their partners
+__host__ __device__ __forceinline__ int rope_row(int t, int r, int hd) {
+  const int tph = hd / 16, h = t / tph, q = t % tph;
+  return h * hd + (r < 8 ? q * 8 + r : hd / 2 + q * 8 + (r - 8));
+}
+
+template <int NW>
 __device__ __forceinline__ const u32x4_t* wave_weight_ptr(const GemmParams& p, int g, int wave,
                                                           bool& active) {
   int seg = 0, t;
-  if (p.mode == EP_SWIGLU) {
-    seg = wave >> 1;
-    t = g * 2 + (wave & 1);
+  if (p.mode == EP_SWIGLU) {  // waves [0, NW/2) gate tiles, [NW/2, NW) the matching up tiles
+    constexpr int H = NW / 2;
+    seg = wave >= H ? 1 : 0;
+    t = g * H + wave - seg * H;
     active = t < p.seg[seg].tiles;
   } else {
-    t = g * GEMM_WAVES + wave;
+    t = g * NW + wave;
     active = t < p.ntiles;
     while (active && seg < p.nseg - 1 && t >= p.seg[seg].tiles) {
       t -= p.seg[seg].tiles;
@@ -56,59 +68,52 @@ __device__ __forceinline__ const u32x4_t* wave_weight_ptr(const GemmParams& p, i
   return reinterpret_cast<const u32x4_t*>(p.seg[seg].w) + (size_t)t * p.nchunks * 64;
 }
 
-// logical 16-row tile of physical tile p in a rotary-interleaved Q/K weight (128-wide heads)
-__host__ __device__ __forceinline__ int rope_tile(int p) {
-  const int q = p & 7;
-  return (p & ~7) + ((q & 1) ? 4 + (q >> 1) : (q >> 1));
-}
-
-template <typename S>
+template <typename S, int NW>
 __device__ void gemm_epilogue(const GemmParams& p, const float* tile, int g, int m0, int mrows,
                               const int* s_pos, const int* s_kvbase) {
   using T = St<S>;
+  constexpr int THREADS = NW * 64, COLS = NW * 16, TSTRIDE = COLS + 4;
   const int tid = threadIdx.x;
-  constexpr int COLS = GEMM_WAVES * 16;
   if (p.mode == EP_SWIGLU) {
+    constexpr int HC = COLS / 2;  // SwiGLU outputs per group
     const int F = p.N;
-    for (int e = tid; e < mrows * 32; e += GEMM_THREADS) {
-      const int r = e >> 5, j = e & 31, m = m0 + r, n = g * 32 + j;
+    for (int e = tid; e < mrows * HC; e += THREADS) {
+      const int r = e / HC, j = e % HC, m = m0 + r, n = g * HC + j;
       if (m >= p.M || n >= F) continue;
-      const float gt = tile[r * TILE_STRIDE + j], up = tile[r * TILE_STRIDE + 32 + j];
+      const float gt = tile[r * TSTRIDE + j], up = tile[r * TSTRIDE + HC + j];
       reinterpret_cast<S*>(p.out_s)[(size_t)m * p.ldos + n] = T::from_f(silu_f(gt) * up);
     }
     return;
   }
-  // EP_QKV.  Each thread owns one column of the 64-wide tile (GEMM_THREADS % 64 == 0).
-  const int col = tid & (COLS - 1), w = col >> 4, jj = col & 15;
+  // EP_QKV.  Each thread owns one column of the tile (THREADS / COLS == 4 rows at a time).
+  const int col = tid % COLS, w = col >> 4, jj = col & 15;
   const int hd = p.hd, half = hd >> 1, qd = p.n_heads * hd, kvd = p.n_kv * hd;
-  const int pt = g * GEMM_WAVES + w;  // physical tile over [q; k; v]
+  const int pt = g * NW + w;  // physical tile over [q; k; v]
   const int qt = qd / 16, kt = kvd / 16;
   if (pt >= qt + 2 * kt) return;
-  int n, pc;  // logical output column, partner column in the tile
-  if (hd == 128 && pt < qt + kt) {  // interleaved rotary halves
+  const bool rot = pt < qt + kt;
+  int n, d;  // logical output column and its dimension within the head
+  if (rot) {
     const int seg0 = pt < qt ? 0 : qt;
-    n = seg0 * 16 + rope_tile(pt - seg0) * 16 + jj;
-    pc = ((w ^ 1) << 4) + jj;
+    n = seg0 * 16 + rope_row(pt - seg0, jj, hd);
+    d = n % hd;
   } else {
     n = pt * 16 + jj;
-    const int dd = n % hd;
-    pc = dd < half ? col + half : col - half;
+    d = n % hd;
   }
-  const int d = n % hd;
-  const bool rot = n < qd + kvd;
   double inv = 0.0;
   if (rot) inv = pow((double)p.theta, -2.0 * (double)((d < half) ? d : d - half) / (double)hd);
-  for (int r = tid / COLS; r < mrows; r += GEMM_THREADS / COLS) {
+  for (int r = tid / COLS; r < mrows; r += THREADS / COLS) {
     const int m = m0 + r;
     if (m >= p.M) break;
-    float v = tile[r * TILE_STRIDE + col];
+    float v = tile[r * TSTRIDE + col];
     if (rot) {
-      const float partner = tile[r * TILE_STRIDE + pc];
+      const float partner = tile[r * TSTRIDE + (col ^ 8)];
       double ang = (double)s_pos[r] * inv;
       ang -= 6.283185307179586 * rint(ang * 0.15915494309189535);
       float sn, cs;
       sincosf((float)ang, &sn, &cs);
-      v = (d < half) ? (v * cs - partner * sn) : (v * cs + partner * sn);
+      v = (jj < 8) ? (v * cs - partner * sn) : (v * cs + partner * sn);
     }
     if (n < qd) {
       reinterpret_cast<S*>(p.qbuf)[(size_t)m * p.ldq + n] = T::from_f(v);
@@ -126,14 +131,15 @@ __device__ void gemm_epilogue(const GemmParams& p, const float* tile, int g, int
   }
 }
 
-template <typename S, int MT>
-__global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(const GemmParams p) {
+template <typename S, int MT, int NW>
+__global__ __launch_bounds__(NW * 64) void gemm_kernel(const GemmParams p) {
   using T = St<S>;
+  constexpr int THREADS = NW * 64, COLS = NW * 16, TSTRIDE = COLS + 4;
   constexpr int EPL = T::EPL, KC = 4 * EPL, MROWS = 16 * MT;
   constexpr int XSTRIDE = STAGE_CHUNKS * KC + EPL;          // elements per LDS row
   constexpr int XBUF = MROWS * XSTRIDE;                      // elements per stage buffer
   constexpr int VEC_PER_ROW = STAGE_CHUNKS * 4;              // 16-byte vectors per row per stage
-  constexpr int XVEC = (MROWS * VEC_PER_ROW + GEMM_THREADS - 1) / GEMM_THREADS;
+  constexpr int XVEC = (MROWS * VEC_PER_ROW + THREADS - 1) / THREADS;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   S* xs = reinterpret_cast<S*>(smem);
 
@@ -156,7 +162,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(const GemmParams p) 
   }
 
   bool active;
-  const u32x4_t* wp = wave_weight_ptr<S>(p, g, wave, active);
+  const u32x4_t* wp = wave_weight_ptr<NW>(p, g, wave, active);
   // Inactive waves (past the last tile) stream a valid tile and discard the result, so no
   // load sits behind a branch.
   if (!active) wp = reinterpret_cast<const u32x4_t*>(p.seg[0].w);
@@ -172,7 +178,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(const GemmParams p) 
   auto load_x = [&](int st, u32x4_t* regs) {
 #pragma unroll
     for (int i = 0; i < XVEC; ++i) {
-      const int v = min(threadIdx.x + i * GEMM_THREADS, MROWS * VEC_PER_ROW - 1);
+      const int v = min((int)threadIdx.x + i * THREADS, MROWS * VEC_PER_ROW - 1);
       const int r = min(v / VEC_PER_ROW, p.M - 1 - m0), cv = v % VEC_PER_ROW;
       const int cchunk = min(st * STAGE_CHUNKS + cv / 4, nk - 1);
       regs[i] = *reinterpret_cast<const u32x4_t*>(X + (size_t)(m0 + r) * p.ldx +
@@ -182,7 +188,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(const GemmParams p) 
   auto store_x = [&](int buf, const u32x4_t* regs) {
 #pragma unroll
     for (int i = 0; i < XVEC; ++i) {
-      const int v = threadIdx.x + i * GEMM_THREADS;
+      const int v = threadIdx.x + i * THREADS;
       if (v < MROWS * VEC_PER_ROW) {
         const int r = v / VEC_PER_ROW, cv = v % VEC_PER_ROW;
         const u32x4_t zero = {0u, 0u, 0u, 0u};
@@ -214,7 +220,6 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(const GemmParams p) 
   // register), stage X(st + 1) into the other LDS buffer.  Stages alternate between
   // the two buffers; walking them RING at a time keeps the ring slot (chunk % PF) and
   // the buffer a compile-time index.
-  static_assert(PF == RING * STAGE_CHUNKS, "ring covers whole stages");
   auto stage = [&](int st, int par, bool guard) {
     load_x(st + RING, xr[par]);
     const S* xb = xs + (par & 1) * XBUF + (lane & 15) * XSTRIDE + (lane >> 4) * EPL;
@@ -248,11 +253,10 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(const GemmParams p) 
     if (st < nst) stage(st, par, true);
   }
 
-  const int col = wave * 16 + (lane & 15);
   if (p.mode == EP_PARTIAL) {
     // split `split` writes rows m0.. of its own [M][N] fp32 slice
     if (!active) return;
-    const int n = (g * GEMM_WAVES + wave) * 16 + (lane & 15);  // segments are contiguous in N
+    const int n = (g * NW + wave) * 16 + (lane & 15);  // segments are contiguous in N
     float* out = p.part + (size_t)split * p.M * p.N;
 #pragma unroll
     for (int t = 0; t < MT; ++t)
@@ -263,69 +267,118 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(const GemmParams p) 
       }
     return;
   }
+  const int col = wave * 16 + (lane & 15);
   float* tile = reinterpret_cast<float*>(smem);
 #pragma unroll
   for (int t = 0; t < MT; ++t)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) tile[(t * 16 + 4 * (lane >> 4) + r) * TILE_STRIDE + col] = acc[t][r];
+    for (int r = 0; r < 4; ++r) tile[(t * 16 + 4 * (lane >> 4) + r) * TSTRIDE + col] = acc[t][r];
   __syncthreads();
-  gemm_epilogue<S>(p, tile, g, m0, MROWS, s_pos, s_kvbase);
+  gemm_epilogue<S, NW>(p, tile, g, m0, MROWS, s_pos, s_kvbase);
 }
 
 // ---- host side ------------------------------------------------------------------------
 
 static int es_of(int dtype) { return dtype == 1 ? 2 : 4; }
 
+// Cost model of one launch (microseconds), from per-workgroup timings on MI355X: a CU
+// streams weight + X bytes at about CU_GBS while the whole chip reads HBM at about
+// HBM_GBS; fp32 partials are written once and read once by the consumer.
+static constexpr double CU_GBS = 45.0, HBM_GBS = 6500.0;
+static constexpr int N_CU = 256, N_XCD = 8;
+
+static double plan_cost(const GemmPlan& pl, int es, int M, int ntiles, int nchunks) {
+  const int KC = 64 / es;
+  const long wgs = (long)pl.ngroups * pl.S * pl.mchunks;
+  const long per_xcd = (wgs + N_XCD - 1) / N_XCD;
+  const long rounds = (per_xcd + N_CU / N_XCD - 1) / (N_CU / N_XCD);
+  const double wg_bytes = (double)pl.nw * pl.cps * 1024.0 + 16.0 * pl.mt * pl.cps * KC * es;
+  const double t_cu = rounds * wg_bytes / (CU_GBS * 1e3);
+  const double part = pl.S > 1 ? 2.0 * pl.S * M * ntiles * 16.0 * 4.0 : 0.0;
+  const double t_hbm = ((double)ntiles * nchunks * 1024.0 + part) / (HBM_GBS * 1e3);
+  return std::max(t_cu, t_hbm) + 0.1 * std::min(t_cu, t_hbm);
+}
+
 GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int max_splits) {
-  GemmPlan pl{};
-  pl.mt = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
-  const int mrows = 16 * pl.mt;
-  pl.mchunks = (M + mrows - 1) / mrows;
-  pl.ngroups = swiglu ? ((ntiles / 2) + 1) / 2 : (ntiles + GEMM_WAVES - 1) / GEMM_WAVES;
-  const int base = pl.ngroups * pl.mchunks;
-  int S = 1;
-  if (max_splits > 1) {
-    S = (TARGET_WGS + base - 1) / base;
-    S = std::max(1, std::min({S, max_splits, nchunks / (2 * STAGE_CHUNKS)}));
-  }
-  int cps = (nchunks + S - 1) / S;
-  S = (nchunks + cps - 1) / cps;
-  pl.S = S;
-  pl.cps = cps;
   const int es = es_of(dtype), EPL = 16 / es, KC = 4 * EPL;
+  GemmPlan best{};
+  double best_cost = 1e30;
+  for (int nw : {4, 2, 3, 6, 8}) {
+    if (swiglu && (nw & 1)) continue;
+    GemmPlan pl{};
+    pl.nw = nw;
+    pl.mt = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+    const int mrows = 16 * pl.mt;
+    pl.mchunks = (std::max(M, 1) + mrows - 1) / mrows;
+    pl.ngroups = swiglu ? ((ntiles / 2) + nw / 2 - 1) / (nw / 2) : (ntiles + nw - 1) / nw;
+    const int smax = std::max(1, std::min(max_splits, nchunks / (2 * STAGE_CHUNKS)));
+    for (int S0 = 1; S0 <= smax; ++S0) {
+      const int cps = (nchunks + S0 - 1) / S0;
+      pl.cps = cps;
+      pl.S = (nchunks + cps - 1) / cps;
+      if (pl.S != S0) continue;
+      const double c = plan_cost(pl, es, M, ntiles, nchunks);
+      if (c < best_cost) {
+        best_cost = c;
+        best = pl;
+      }
+    }
+  }
+  const int mrows = 16 * best.mt;
   const size_t xbytes = 2ull * mrows * (STAGE_CHUNKS * KC + EPL) * es;
-  const size_t tbytes = (size_t)mrows * TILE_STRIDE * 4;
-  pl.lds_bytes = std::max(xbytes, tbytes);
-  pl.part_floats = (size_t)S * M * ntiles * 16;
-  return pl;
+  const size_t tbytes = (size_t)mrows * (best.nw * 16 + 4) * 4;
+  best.lds_bytes = std::max(xbytes, tbytes);
+  best.part_floats = (size_t)best.S * M * ntiles * 16;
+  return best;
+}
+
+template <typename S, int MT>
+static void launch_nw(const GemmPlan& pl, GemmParams& p, hipStream_t st, const LaunchTiming* lt) {
+  dim3 grid(pl.ngroups, pl.S, pl.mchunks), block(pl.nw * 64);
+  auto go = [&](auto kern) {
+    if (lt) hipExtLaunchKernelGGL(kern, grid, block, (uint32_t)pl.lds_bytes, st, lt->start, lt->stop, 0, p);
+    else hipLaunchKernelGGL(kern, grid, block, pl.lds_bytes, st, p);
+  };
+  switch (pl.nw) {
+    case 2: go(gemm_kernel<S, MT, 2>); break;
+    case 3: go(gemm_kernel<S, MT, 3>); break;
+    case 6: go(gemm_kernel<S, MT, 6>); break;
+    case 8: go(gemm_kernel<S, MT, 8>); break;
+    default: go(gemm_kernel<S, MT, 4>); break;
+  }
 }
 
 template <typename S>
-static hipError_t launch_gemm_t(GemmParams& p, const GemmPlan& pl, hipStream_t st) {
-  dim3 grid(pl.ngroups, pl.S, pl.mchunks), block(GEMM_THREADS);
+static hipError_t launch_gemm_t(GemmParams& p, const GemmPlan& pl, hipStream_t st, const LaunchTiming* lt) {
   switch (pl.mt) {
-    case 1: hipLaunchKernelGGL((gemm_kernel<S, 1>), grid, block, pl.lds_bytes, st, p); break;
-    case 2: hipLaunchKernelGGL((gemm_kernel<S, 2>), grid, block, pl.lds_bytes, st, p); break;
-    default: hipLaunchKernelGGL((gemm_kernel<S, 4>), grid, block, pl.lds_bytes, st, p); break;
+    case 1: launch_nw<S, 1>(pl, p, st, lt); break;
+    case 2: launch_nw<S, 2>(pl, p, st, lt); break;
+    default: launch_nw<S, 4>(pl, p, st, lt); break;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_gemm(int dtype, GemmParams& p, hipStream_t st) {
+hipError_t launch_gemm(int dtype, GemmParams& p, hipStream_t st, const LaunchTiming* lt) {
   const int maxs = p.mode == EP_PARTIAL ? std::max(1, p.max_splits) : 1;
   const GemmPlan pl = plan_gemm(dtype, p.M, p.ntiles, p.nchunks, p.mode == EP_SWIGLU, maxs);
   p.ngroups = pl.ngroups;
   p.mchunks = pl.mchunks;
   p.S = pl.S;
   p.cps = pl.cps;
-  if (p.M <= 0) return hipSuccess;
-  return dtype == 1 ? launch_gemm_t<bf16_t>(p, pl, st) : launch_gemm_t<float>(p, pl, st);
+  if (p.M <= 0) {  // nothing to launch: an empty timed interval
+    if (lt) {
+      (void)hipEventRecord(lt->start, st);
+      (void)hipEventRecord(lt->stop, st);
+    }
+    return hipSuccess;
+  }
+  return dtype == 1 ? launch_gemm_t<bf16_t>(p, pl, st, lt) : launch_gemm_t<float>(p, pl, st, lt);
 }
 
 // ---- packing ------------------------------------------------------------------------------
 
 template <typename S>
-__global__ void pack_kernel(const S* __restrict__ src, int rows, int cols, S* __restrict__ dst, int rope) {
+__global__ void pack_kernel(const S* __restrict__ src, int rows, int cols, S* __restrict__ dst, int rope_hd) {
   constexpr int EPL = St<S>::EPL, KC = 4 * EPL;
   const int nchunks = cols / KC;
   const size_t nvec = (size_t)(rows / 16) * nchunks * 64;
@@ -335,7 +388,7 @@ __global__ void pack_kernel(const S* __restrict__ src, int rows, int cols, S* __
     const size_t tc = v / 64;
     const int c = (int)(tc % nchunks);
     const int t = (int)(tc / nchunks);
-    const int n = (rope ? rope_tile(t) : t) * 16 + (lane & 15);
+    const int n = rope_hd ? rope_row(t, lane & 15, rope_hd) : t * 16 + (lane & 15);
     const int k = c * KC + (lane >> 4) * EPL;
     *reinterpret_cast<u32x4_t*>(dst + v * EPL) =
         *reinterpret_cast<const u32x4_t*>(src + (size_t)n * cols + k);
@@ -346,10 +399,10 @@ size_t packed_matrix_bytes(int dtype, int rows, int cols) {
   return (size_t)rows * cols * es_of(dtype);
 }
 
-hipError_t launch_pack(int dtype, const void* src, int rows, int cols, void* dst, bool rope_interleave,
+hipError_t launch_pack(int dtype, const void* src, int rows, int cols, void* dst, int rope_hd,
                        hipStream_t st) {
-  const int rope = rope_interleave ? 1 : 0;
-  if (rope && rows % 128) return hipErrorInvalidValue;
+  const int rope = rope_hd;
+  if (rope && (rope % 16 || rows % rope)) return hipErrorInvalidValue;
   const size_t nvec = (size_t)rows * cols * es_of(dtype) / 16;
   const int grid = (int)std::min<size_t>((nvec + 255) / 256, 65536);
   if (dtype == 1)

@@ -6,6 +6,12 @@
 
 namespace clover {
 
+// Optional events filled with a kernel's own start and end times (hipExtLaunchKernel), so
+// that per-launch timing excludes the dispatch gaps that marker events would include.
+struct LaunchTiming {
+  hipEvent_t start, stop;
+};
+
 // ---- weight-streaming GEMM ------------------------------------------------------------
 enum GemmEpilogue : int {
   EP_PARTIAL = 0,  // part[split][m][n] = partial y (fp32); S = 1 gives y itself
@@ -38,6 +44,7 @@ struct GemmParams {
 };
 
 struct GemmPlan {
+  int nw;        // waves per workgroup, one 16-row weight tile each (2, 3, 4, 6 or 8)
   int mt;        // m-tiles of 16 rows per chunk (1, 2 or 4)
   int mchunks, ngroups, S, cps;
   size_t lds_bytes;
@@ -46,9 +53,10 @@ struct GemmPlan {
 
 GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int max_splits);
 // Fills plan fields of p and launches; returns hipSuccess or an error.
-hipError_t launch_gemm(int dtype, GemmParams& p, hipStream_t st);
-// rope_interleave: Q/K weights of 128-wide heads, rotary halves interleaved by 16-row tiles
-hipError_t launch_pack(int dtype, const void* src, int rows, int cols, void* dst, bool rope_interleave,
+hipError_t launch_gemm(int dtype, GemmParams& p, hipStream_t st, const LaunchTiming* lt = nullptr);
+// rope_hd > 0: a Q/K weight of heads rope_hd wide, packed so that each 16-row tile holds
+// 8 dims of a head's first rotary half and their 8 partners (tile-local rotary epilogue)
+hipError_t launch_pack(int dtype, const void* src, int rows, int cols, void* dst, int rope_hd,
                        hipStream_t st);
 size_t packed_matrix_bytes(int dtype, int rows, int cols);
 
@@ -69,7 +77,8 @@ struct AttnParams {
   int n_heads, n_kv, hd;
   int nbatch, qtiles, splits, blocks_per_split;
 };
-hipError_t launch_attention(int dtype, AttnParams& p, int max_keys, hipStream_t st);
+hipError_t launch_attention(int dtype, AttnParams& p, int max_keys, hipStream_t st,
+                            const LaunchTiming* lt = nullptr);
 // write rows [n][n_kv*hd] (storage) of K and V into the paged cache at slots slot0.. of seq
 hipError_t launch_kv_write(int dtype, const void* K, const void* V, int n, int slot0, int seq,
                            void* kcache, void* vcache, const int* block_table, int max_blocks,
