@@ -147,6 +147,7 @@ struct Layout {
   size_t dstate[CLOVER_MAX_HEADS], dlogits[CLOVER_MAX_HEADS];
   size_t d_hin, d_a, d_e, d_q, d_kv, d_o, d_sst, d_r, d_rn;
   size_t gpart, gpart2, amax_keys, topk_scratch;
+  size_t apart, apart_floats;  // attention split partials
   size_t gpart_floats, gpart2_floats;
   size_t total;
 };
@@ -234,6 +235,24 @@ Layout make_layout(const clover_config& c) {
   L.gpart2 = take(4 * L.gpart2_floats);
   L.amax_keys = take(8 * (size_t)L.Mv);
   L.topk_scratch = take(4 * topk_scratch_floats(L.Fmaxrows, (int)V, 16));
+  // attention split partials: the largest of the verify launches (every batch size) and
+  // the prefill chunks (every chunk length)
+  {
+    AttnParams a{};
+    a.n_heads = c.n_heads; a.n_kv = c.n_kv_heads; a.hd = c.head_dim;
+    size_t af = 0;
+    for (int b = 1; b <= c.max_batch; ++b) {
+      a.nbatch = b; a.nq = L.T;
+      af = std::max(af, attention_part_floats(a));
+    }
+    a.nbatch = 1;
+    for (int rows = 16; rows < L.Mp + 16; rows += 16) {
+      a.nq = std::min(rows, L.Mp);
+      af = std::max(af, attention_part_floats(a));
+    }
+    L.apart_floats = af;
+    L.apart = take(4 * std::max<size_t>(af, 1));
+  }
   L.total = off;
   return L;
 }
@@ -472,6 +491,7 @@ hipError_t enq_verify(clover_ctx* c, int B, int max_keys) {
   att.rows_per_seq = T; att.nq = T; att.n_tail = T; att.causal = 0;
   att.mask = c->at<uint64_t>(L.tree_mask); att.mask_words = L.W; att.mask_seq_stride = T * L.W;
   att.nbatch = B;
+  att.part = c->at<float>(L.apart); att.part_cap = L.apart_floats;
   int pend = 0;
   for (int l = 0; l < cf.n_layers; ++l) HE(run_layer(c, c->layers[l], l, x, M, att, max_keys, pend, &pend));
   // x_N = x + last partials; kept in xa for the Augmenting Block; final norm; LM head; argmax
@@ -918,6 +938,7 @@ clover_status clover_prefill(clover_ctx* c, int32_t seq, const int32_t* tokens, 
     att.prefix_dev = nullptr; att.prefix_host = c0;
     att.rows_per_seq = rows; att.nq = rows; att.n_tail = rows; att.causal = 1;
     att.nbatch = 1;
+    att.part = c->at<float>(L.apart); att.part_cap = L.apart_floats;
     int pend = 0;
     for (int l = 0; l < cf.n_layers; ++l)
       HIPCK(c, run_layer(c, c->layers[l], l, x, rows, att, c0 + rows, pend, &pend));
@@ -1225,9 +1246,9 @@ size_t clover_op_attention_scratch_bytes(int32_t dtype, int32_t L, int32_t T, in
     return 0;
   const int nblocks = (L + T + 15) / 16;
   AttnParams a{};
-  a.nbatch = 1; a.nq = T; a.n_heads = n_heads;
-  plan_attention(a, L + T);
+  a.nbatch = 1; a.nq = T; a.n_heads = n_heads; a.n_kv = n_kv; a.hd = head_dim;
   size_t b = 0;
+  b += align_up(4 * attention_part_floats(a));                                 // split partials
   b += align_up((size_t)nblocks * n_kv * 16 * head_dim * es_of(dtype)) * 2;  // K and V pools
   b += align_up(4 * (size_t)nblocks);                                          // block table
   b += align_up(8 * (size_t)T * ((T + 63) / 64));                              // mask
@@ -1254,13 +1275,15 @@ clover_status clover_op_attention(int32_t dtype, const void* Q, const void* Kpre
   const int nblocks = (L + T + 15) / 16, W = (T + 63) / 64;
   const int es = es_of(dtype);
   char* p = (char*)scratch;
+  AttnParams a{};
+  a.nbatch = 1; a.nq = T; a.n_heads = n_heads; a.n_kv = n_kv; a.hd = head_dim;
+  a.part_cap = attention_part_floats(a);
+  a.part = (float*)p; p += align_up(4 * a.part_cap);
   char* kp = p; p += align_up((size_t)nblocks * n_kv * 16 * head_dim * es);
   char* vp = p; p += align_up((size_t)nblocks * n_kv * 16 * head_dim * es);
   int* bt = (int*)p; p += align_up(4 * (size_t)nblocks);
   uint64_t* mask = (uint64_t*)p; p += align_up(8 * (size_t)T * W);
   int* ids = (int*)p; p += align_up(8);
-  AttnParams a{};
-  a.nbatch = 1; a.nq = T; a.n_heads = n_heads;
   std::vector<int> hbt(nblocks);
   for (int i = 0; i < nblocks; ++i) hbt[i] = nblocks - 1 - i;  // reversed pages: exercises the table
   std::vector<uint64_t> hm((size_t)T * W, 0);

@@ -3,11 +3,23 @@
 //
 // Each query row attends to every committed key (slots 0..P-1) and to the tail keys
 // P..P+n_tail-1 its mask row admits: the tree's ancestor-or-self bits during verify,
-// or the causal rule during chunked prefill.  The score product is computed
-// transposed (S^T = K Q^T) so the matrix-core accumulator already holds, per lane,
-// four consecutive keys of one query row: exactly the operand layout the P*V product
-// needs, with no shuffles.  Softmax is online in the log2 domain.  Keys are split over
-// the waves of a workgroup, whose states merge in LDS in wave order.
+// or the causal rule during chunked prefill.
+//
+// Work split.  One workgroup takes one (sequence, KV head), up to four 16-row query
+// tiles of the query heads sharing that KV head, and one contiguous range of the keys.
+// Its K/V blocks are staged once through LDS and shared by the tiles, so each CU reads
+// every key it needs exactly once; the key range is split over enough workgroups
+// (attention "splits") to give every CU of the chip one workgroup.  Splits of one
+// (sequence, KV head) run on the same XCD and leave fp32 partial states (unnormalised
+// output, running max, running sum) that a small merge kernel combines in split order;
+// with one split the output is written directly.
+//
+// Inside a workgroup, waves w and w + 4 take one query tile and the even / odd key
+// blocks of each chunk, merging their states through LDS at the end.  The score
+// product is computed transposed (S^T = K Q^T) so the matrix-core accumulator already
+// holds, per lane, four consecutive keys of one query row: exactly the operand layout
+// the P*V product needs.  Softmax is online in the log2 domain.  The next chunk's K/V
+// loads are in flight while the current chunk is computed from LDS.
 #include "common.h"
 #include "kernels.h"
 
@@ -17,18 +29,27 @@
 
 namespace clover {
 
-static constexpr int ATT_WAVES = 8;              // key splits inside a workgroup
-static constexpr int ATT_THREADS = ATT_WAVES * 64;
-static constexpr int ATT_MAX_BLOCKS = 4096;    // 65536 keys
+static constexpr int AT_WAVES = 8;               // 4 query tiles x 2 key halves
+static constexpr int AT_THREADS = AT_WAVES * 64;
+static constexpr int AT_QT = 4;                  // query tiles per workgroup
+static constexpr int AT_MAX_BLOCKS = 4096;       // 65536 keys
+static constexpr int AT_MAX_SPLITS = 16;
+static constexpr int AT_TARGET_WGS = 256;        // one workgroup per CU
+static constexpr int AT_CHUNK_BYTES = 128 * 1024;  // K + V bytes of one LDS chunk
 
-__device__ __forceinline__ f32x4_t mma_pv(u32x2_t v, const float p[4], f32x4_t c, bf16_t) {
-  u32x2_t pb;
-  pb[0] = (uint32_t)f2bf(p[0]) | ((uint32_t)f2bf(p[1]) << 16);
-  pb[1] = (uint32_t)f2bf(p[2]) | ((uint32_t)f2bf(p[3]) << 16);
+// probabilities of one lane's 4 keys as the bf16 B operand of the P*V product
+__device__ __forceinline__ u32x2_t pack_p(const float p[4], bf16_t) {
+  typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+  const bf16x4_t v = {(__bf16)p[0], (__bf16)p[1], (__bf16)p[2], (__bf16)p[3]};
+  return __builtin_bit_cast(u32x2_t, v);
+}
+__device__ __forceinline__ u32x2_t pack_p(const float*, float) { return u32x2_t{0u, 0u}; }
+
+__device__ __forceinline__ f32x4_t mma_pv(u32x2_t v, u32x2_t pb, const float*, f32x4_t c, bf16_t) {
   return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, v),
                                                    __builtin_bit_cast(s16x4_t, pb), c, 0, 0, 0);
 }
-__device__ __forceinline__ f32x4_t mma_pv(u32x4_t v, const float p[4], f32x4_t c, float) {
+__device__ __forceinline__ f32x4_t mma_pv(u32x4_t v, u32x2_t, const float p[4], f32x4_t c, float) {
   c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(v[0]), p[0], c, 0, 0, 0);
   c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(v[1]), p[1], c, 0, 0, 0);
   c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(v[2]), p[2], c, 0, 0, 0);
@@ -41,46 +62,69 @@ template <> struct VFrag<bf16_t> { typedef u32x2_t type; };
 template <> struct VFrag<float> { typedef u32x4_t type; };
 
 template <typename S, int HD>
-struct KVBlock {
-  static constexpr int EPL = St<S>::EPL, NQC = HD / (4 * EPL), NT = HD / 16;
-  u32x4_t k[NQC];
-  typename VFrag<S>::type v[NT];
-  __device__ __forceinline__ void load(const S* kc, const S* vc, size_t base, int lane) {
-#pragma unroll
-    for (int c = 0; c < NQC; ++c)
-      k[c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(kc + base + (size_t)(c * 64 + lane) * EPL));
-#pragma unroll
-    for (int t = 0; t < NT; ++t)
-      v[t] = __builtin_nontemporal_load(
-          reinterpret_cast<const typename VFrag<S>::type*>(vc + base + (size_t)(t * 64 + lane) * 4));
-  }
+struct AttnShape {
+  static constexpr int BLK_BYTES = 16 * HD * (int)sizeof(S);                // K (or V) of a block
+  static constexpr int CB = std::min(16, AT_CHUNK_BYTES / (2 * BLK_BYTES));  // blocks per chunk
+  static constexpr int CH_VEC = 2 * CB * BLK_BYTES / 16;                    // 16-byte vectors
+  static constexpr int LVEC = CH_VEC / AT_THREADS;                          // per thread
+  static_assert(CH_VEC % AT_THREADS == 0, "chunk splits evenly over the threads");
+  static constexpr size_t LDS = (size_t)CH_VEC * 16;
 };
 
-// One workgroup = one 16-row query tile of one (sequence, head); its 8 waves take
-// interleaved 16-key blocks and merge their online-softmax states through LDS.
-// Workgroup ids are laid out so all query tiles of one (sequence, head) land on the
-// same XCD (ids are dealt to the 8 XCDs round-robin) and share its L2 copy of K/V.
+// record of one (item, split, query tile, row): o[HD] then m, l
+__device__ __forceinline__ size_t part_rec(const AttnParams& p, int item, int split, int qi, int j, int hd) {
+  return ((((size_t)item * p.splits + split) * p.qt_item + qi) * 16 + j) * (size_t)(hd + 2);
+}
+
 template <typename S, int HD>
-__global__ __launch_bounds__(ATT_THREADS) void attn_kernel(const AttnParams p) {
+__global__ __launch_bounds__(AT_THREADS) void attn_kernel(const AttnParams p) {
   using T = St<S>;
+  using SH = AttnShape<S, HD>;
   constexpr int EPL = T::EPL, KC = 4 * EPL, NQC = HD / KC, NT = HD / 16;
-  constexpr int ATT_RING = sizeof(S) == 2 ? 3 : 2;  // 16-key blocks in flight per wave
-  __shared__ float s_m[ATT_WAVES][16], s_l[ATT_WAVES][16];
-  __shared__ float s_o[ATT_WAVES][16][HD + 4];
+  constexpr int CB = SH::CB, LVEC = SH::LVEC, BVEC = SH::BLK_BYTES / 16;
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  u32x4_t* lds = reinterpret_cast<u32x4_t*>(smem);  // [K blocks 0..CB-1][V blocks 0..CB-1]
+  __shared__ int s_bt[AT_MAX_BLOCKS];
+
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, j = lane & 15;
+  const int half = wave >> 2;  // key-block parity this wave takes
+  // workgroup -> (item, query group, split); all splits and query groups of an item on
+  // one XCD (workgroup ids are dealt to the 8 XCDs round-robin)
+  const int per_item = p.qgroups * p.splits;
   const int id = blockIdx.x, xcd = id & 7, slotx = id >> 3;
-  const int item = (slotx / p.qtiles) * 8 + xcd, qt = slotx % p.qtiles;
-  if (item >= p.nbatch * p.n_heads) return;
-  const int b = item / p.n_heads, h = item % p.n_heads;
+  const int item = (slotx / per_item) * 8 + xcd, rem = slotx % per_item;
+  const int qg = rem / p.splits, split = rem % p.splits;
+  if (item >= p.nbatch * p.n_kv) return;
+  const int b = item / p.n_kv, kvh = item % p.n_kv;
+  const int G = p.n_heads / p.n_kv;
   const int slot = p.seq_ids[b];
   const int P = p.prefix_dev ? p.prefix_dev[slot] : p.prefix_host;
-  const int tail = p.causal ? min(p.n_tail, qt * 16 + 16) : p.n_tail;
-  const int nkeys = P + tail;
-  const int kvh = h / (p.n_heads / p.n_kv);
-  const int row = qt * 16 + j;
-  const bool valid = row < p.nq;
-  const S* Q = reinterpret_cast<const S*>(p.Q);
 
+  // this wave's query tile
+  const int qi = qg * AT_QT + (wave & 3);
+  const bool has_q = qi < p.qt_item;
+  const int h = kvh * G + (has_q ? qi / p.qph : 0), qt = has_q ? qi % p.qph : 0;
+  const int row = qt * 16 + j;
+  const bool valid = has_q && row < p.nq;
+  // keys the workgroup needs: the causal tail stops at its last query tile's rows
+  int tail = p.n_tail;
+  if (p.causal) {
+    int qmax = 0;
+    for (int w = 0; w < AT_QT; ++w) {
+      const int q2 = qg * AT_QT + w;
+      if (q2 < p.qt_item) qmax = max(qmax, q2 % p.qph);
+    }
+    tail = min(p.n_tail, qmax * 16 + 16);
+  }
+  const int nkeys = P + tail;
+  const int nblocks = (nkeys + 15) >> 4;
+  const int bps = (nblocks + p.splits - 1) / p.splits;
+  const int kb0 = min(nblocks, split * bps), nb = min(nblocks, kb0 + bps) - kb0;
+
+  const int* bt = p.block_table + (size_t)slot * p.max_blocks;
+  for (int i = threadIdx.x; i < nb; i += AT_THREADS) s_bt[i] = bt[kb0 + i];
+
+  const S* Q = reinterpret_cast<const S*>(p.Q);
   u32x4_t qf[NQC];
 #pragma unroll
   for (int c = 0; c < NQC; ++c) {
@@ -95,142 +139,283 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(const AttnParams p) {
     mw0 = mr[0];
     if (p.mask_words > 1) mw1 = mr[1];
   }
+  __syncthreads();  // s_bt
 
-  const int nblocks = (nkeys + 15) >> 4;
+  const S* kc = reinterpret_cast<const S*>(p.kcache);
+  const S* vc = reinterpret_cast<const S*>(p.vcache);
+  const int nch = (nb + CB - 1) / CB;
+  // chunk loader: vector v of the chunk is K (v < CB*BVEC) or V of block v / BVEC; blocks
+  // past the range are clamped to its last block (unconditional loads, never consumed)
+  u32x4_t stg[LVEC];
+  auto load_chunk = [&](int ch) {
+#pragma unroll
+    for (int i = 0; i < LVEC; ++i) {
+      const int v = threadIdx.x + i * AT_THREADS;
+      const int isv = v >= CB * BVEC;
+      const int vv = v - isv * CB * BVEC;
+      const int kbl = min(ch * CB + vv / BVEC, nb - 1);
+      const size_t base = ((size_t)s_bt[kbl] * p.n_kv + kvh) * (size_t)(16 * HD);
+      const S* src = (isv ? vc : kc) + base + (size_t)(vv % BVEC) * (16 / sizeof(S));
+      stg[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(src));
+    }
+  };
+  auto store_chunk = [&]() {
+#pragma unroll
+    for (int i = 0; i < LVEC; ++i) lds[threadIdx.x + i * AT_THREADS] = stg[i];
+  };
+
   const float scale2 = rsqrtf((float)HD) * 1.4426950408889634f;
   float m_i = -INFINITY, l_i = 0.f;
   f32x4_t o[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) o[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  const S* kc = reinterpret_cast<const S*>(p.kcache);
-  const S* vc = reinterpret_cast<const S*>(p.vcache);
-  // the sequence's block-table row, staged in LDS so no K/V load waits on a table load
-  __shared__ int s_bt[ATT_MAX_BLOCKS];
-  const int* bt = p.block_table + (size_t)slot * p.max_blocks;
-  for (int i = threadIdx.x; i < nblocks; i += ATT_THREADS) s_bt[i] = bt[i];
-  __syncthreads();
-  auto base_of = [&](int kb) { return ((size_t)s_bt[kb] * p.n_kv + kvh) * (size_t)(16 * HD); };
-
-  // this wave's blocks: kb = wave + ATT_WAVES * i, i < nmine; a ring of RB blocks in
-  // flight, each slot reloaded (clamped, unconditionally) right after it is consumed
-  const int nmine = wave < nblocks ? (nblocks - wave + ATT_WAVES - 1) / ATT_WAVES : 0;
-  auto blk = [&](int i) { return wave + ATT_WAVES * min(i, nmine - 1); };
-  auto consume = [&](const KVBlock<S, HD>& cur, int kb) {
-    f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // One online-softmax update over up to NG of this wave's blocks of the chunk (LDS
+  // blocks cb0, cb0 + 2, ...; key blocks kb0g, kb0g + 2, ...): the cross-lane max and
+  // sum reductions and the rescale of the output are paid once per NG blocks.  The
+  // running max m_i is kept in raw score units; the scale folds into one multiply-add
+  // per exponent.  Groups wholly inside the committed prefix skip the mask logic.
+  constexpr int NG = 4;
+  using VT = typename VFrag<S>::type;
+  // tail rule as data, so the score loop has no branch on the mode: causal rows see tail
+  // keys up to their own index, tree rows the keys whose mask bit is set
+  const bool causal_mode = p.causal != 0;
+  const int tail_lim = causal_mode ? row : 0x7fffffff;
+  auto consume = [&](int cb0, int kb0g, int nblk) {
+    f32x4_t s[NG];
 #pragma unroll
-    for (int c = 0; c < NQC; ++c) s = mma_frag(cur.k[c], qf[c], s, S{});
-    // s[r] = score of key kb*16 + 4g + r for query row j
-    float s2[4];
+    for (int i = 0; i < NG; ++i) {
+      s[i] = f32x4_t{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+      if (i < nblk) {
+        const u32x4_t* kblk = lds + (cb0 + 2 * i) * BVEC;
+        f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < NQC; ++c) acc = mma_frag(kblk[c * 64 + lane], qf[c], acc, S{});
+        s[i] = acc;
+      }
+    }
+    // s[i][r] = score of key (kb0g + 2i)*16 + 4g + r for query row j
+    const bool plain = (kb0g + 2 * (nblk - 1)) * 16 + 15 < P;  // all keys committed
+    if (!plain) {
+#pragma unroll
+      for (int i = 0; i < NG; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = (kb0g + 2 * i) * 16 + 4 * g + r;
+          const int tk = key - P;
+          const uint64_t word = tk < 64 ? mw0 : mw1;
+          const bool tree_ok = causal_mode | (((word >> (tk & 63)) & 1ull) != 0);
+          const bool vis = valid & (key < nkeys) & ((tk < 0) | (tree_ok & (tk <= tail_lim)));
+          s[i][r] = vis ? s[i][r] : -INFINITY;
+        }
+    }
     float mloc = -INFINITY;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int key = kb * 16 + 4 * g + r;
-      bool vis = valid && key < nkeys;
-      if (vis && key >= P) {
-        const int tk = key - P;
-        if (p.causal)
-          vis = tk <= row;
-        else
-          vis = ((tk < 64 ? mw0 >> tk : mw1 >> (tk - 64)) & 1ull) != 0;
-      }
-      s2[r] = vis ? s[r] * scale2 : -INFINITY;
-      mloc = fmaxf(mloc, s2[r]);
-    }
+    for (int i = 0; i < NG; ++i) mloc = fmaxf(mloc, fmaxf(fmaxf(s[i][0], s[i][1]), fmaxf(s[i][2], s[i][3])));
     mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
     const float m_new = fmaxf(m_i, mloc);
-    const float alpha = (m_new == -INFINITY) ? 1.f : exp2f(m_i - m_new);
-    float pr[4], lsum = 0.f;
+    // every exponent below is <= 0; exp2(-inf) = 0 removes masked keys
+    const float nm = (m_new == -INFINITY) ? 0.f : -m_new * scale2;
+    const float alpha = __builtin_amdgcn_exp2f(fmaf(m_i, scale2, nm));
+    float lsum = 0.f;
+    u32x2_t pb[NG];
+    float pr[NG][4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      pr[r] = (s2[r] == -INFINITY) ? 0.f : exp2f(s2[r] - m_new);
-      lsum += pr[r];
+    for (int i = 0; i < NG; ++i) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        pr[i][r] = __builtin_amdgcn_exp2f(fmaf(s[i][r], scale2, nm));
+        lsum += pr[i][r];
+      }
+      pb[i] = pack_p(pr[i], S{});
     }
     lsum += __shfl_xor(lsum, 16);
     lsum += __shfl_xor(lsum, 32);
     l_i = l_i * alpha + lsum;
     m_i = m_new;
+    if (!__all(alpha == 1.f)) {
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      o[t] *= alpha;
-      o[t] = mma_pv(cur.v[t], pr, o[t], S{});
+      for (int t = 0; t < NT; ++t) o[t] *= alpha;
     }
-  };
-  if (nmine > 0) {
-    KVBlock<S, HD> ring[ATT_RING];
 #pragma unroll
-    for (int r = 0; r < ATT_RING; ++r) ring[r].load(kc, vc, base_of(blk(r)), lane);
-    const int nfull = nmine / ATT_RING;
-    for (int i0 = 0; i0 < nfull * ATT_RING; i0 += ATT_RING) {  // branch-free steady state
+    for (int i = 0; i < NG; ++i) {
+      if (i < nblk) {
+        const VT* vblk = reinterpret_cast<const VT*>(lds + (CB + cb0 + 2 * i) * BVEC);
 #pragma unroll
-      for (int r = 0; r < ATT_RING; ++r) {
-        consume(ring[r], wave + ATT_WAVES * (i0 + r));
-        ring[r].load(kc, vc, base_of(blk(i0 + r + ATT_RING)), lane);
+        for (int t = 0; t < NT; ++t) o[t] = mma_pv(vblk[t * 64 + lane], pb[i], pr[i], o[t], S{});
       }
     }
+  };
+
+  if (nch > 0) {
+    load_chunk(0);
+    store_chunk();
+    __syncthreads();
+    for (int ch = 0; ch < nch; ++ch) {
+      const bool more = ch + 1 < nch;
+      if (more) load_chunk(ch + 1);  // in flight while this chunk is computed
+      if (has_q) {
+        const int nbc = min(CB, nb - ch * CB);
+        for (int cb0 = half; cb0 < nbc; cb0 += 2 * NG)
+          consume(cb0, kb0 + ch * CB + cb0, min(NG, (nbc - cb0 + 1) / 2));
+      }
+      __syncthreads();
+      if (more) {
+        store_chunk();
+        __syncthreads();
+      }
+    }
+  }
+
+  // from here on the running max is in log2-scaled units, as the merges expect
+  m_i = (m_i == -INFINITY) ? -INFINITY : m_i * scale2;
+  // merge the two key halves of each query tile through LDS (the chunk buffer is free)
+  float* mo = reinterpret_cast<float*>(smem);  // [AT_QT][16][HD + 2]
+  float* rec = mo + (size_t)((wave & 3) * 16 + j) * (HD + 2);
+  if (half == 1) {
 #pragma unroll
-    for (int r = 0; r < ATT_RING; ++r)  // tail
-      if (nfull * ATT_RING + r < nmine) consume(ring[r], wave + ATT_WAVES * (nfull * ATT_RING + r));
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) rec[t * 16 + 4 * g + r] = o[t][r];
+    if (g == 0) {
+      rec[HD] = m_i;
+      rec[HD + 1] = l_i;
+    }
   }
-  // merge the waves' states
-  if (g == 0) {
-    s_m[wave][j] = m_i;
-    s_l[wave][j] = l_i;
+  __syncthreads();
+  if (half == 1 || !has_q) return;
+  {
+    const float m1 = rec[HD], l1 = rec[HD + 1];
+    const float M = fmaxf(m_i, m1);
+    const float a0 = (m_i == -INFINITY) ? 0.f : exp2f(m_i - M);
+    const float a1 = (m1 == -INFINITY) ? 0.f : exp2f(m1 - M);
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) o[t][r] = a0 * o[t][r] + a1 * rec[t * 16 + 4 * g + r];
+    l_i = a0 * l_i + a1 * l1;
+    m_i = M;
   }
+  if (p.splits == 1) {
+    if (!valid) return;
+    const float inv = l_i > 0.f ? 1.f / l_i : 0.f;
+    S* O = reinterpret_cast<S*>(p.O) + (size_t)(b * p.rows_per_seq + row) * p.ldo + h * HD;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) O[t * 16 + 4 * g + r] = T::from_f(o[t][r] * inv);
+    return;
+  }
+  float* pr = p.part + part_rec(p, item, split, qi, j, HD);
 #pragma unroll
   for (int t = 0; t < NT; ++t)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) s_o[wave][j][t * 16 + 4 * g + r] = o[t][r];
-  __syncthreads();
-  S* O = reinterpret_cast<S*>(p.O);
-  for (int e = threadIdx.x; e < 16 * HD; e += ATT_THREADS) {
-    const int r2 = e / HD, dim = e % HD;
-    const int row2 = qt * 16 + r2;
-    if (row2 >= p.nq) continue;
-    float M = -INFINITY;
-#pragma unroll
-    for (int w = 0; w < ATT_WAVES; ++w) M = fmaxf(M, s_m[w][r2]);
-    float num = 0.f, den = 0.f;
-#pragma unroll
-    for (int w = 0; w < ATT_WAVES; ++w) {
-      const float ms = s_m[w][r2];
-      const float wt = (ms == -INFINITY) ? 0.f : exp2f(ms - M);
-      num += wt * s_o[w][r2][dim];
-      den += wt * s_l[w][r2];
-    }
-    O[(size_t)(b * p.rows_per_seq + row2) * p.ldo + h * HD + dim] = T::from_f(den > 0.f ? num / den : 0.f);
+    for (int r = 0; r < 4; ++r) pr[t * 16 + 4 * g + r] = o[t][r];
+  if (g == 0) {
+    pr[HD] = m_i;
+    pr[HD + 1] = l_i;
   }
 }
 
-void plan_attention(AttnParams& p, int max_keys) {
-  (void)max_keys;
-  p.qtiles = (p.nq + 15) / 16;
-  p.splits = 1;
-  p.blocks_per_split = 0;
+// Combine the splits of one (item, query tile) in split order; same XCD as its splits.
+// Every split's record is loaded up front (one memory latency, not one per split).
+template <typename S, int HD>
+__global__ __launch_bounds__(256) void attn_merge_kernel(const AttnParams p) {
+  using T = St<S>;
+  constexpr int DPT = HD / 16;  // dims per thread
+  const int id = blockIdx.x, xcd = id & 7, slotx = id >> 3;
+  const int item = (slotx / p.qt_item) * 8 + xcd, qi = slotx % p.qt_item;
+  if (item >= p.nbatch * p.n_kv) return;
+  const int b = item / p.n_kv, kvh = item % p.n_kv, G = p.n_heads / p.n_kv;
+  const int h = kvh * G + qi / p.qph, qt = qi % p.qph;
+  const int j = threadIdx.x >> 4, d0 = (threadIdx.x & 15) * DPT;
+  const int row = qt * 16 + j;
+  if (row >= p.nq) return;
+  float ms[AT_MAX_SPLITS], ls[AT_MAX_SPLITS], ov[AT_MAX_SPLITS][DPT];
+#pragma unroll
+  for (int s = 0; s < AT_MAX_SPLITS; ++s) {
+    const float* r = p.part + part_rec(p, item, min(s, p.splits - 1), qi, j, HD);
+    ms[s] = r[HD];
+    ls[s] = r[HD + 1];
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) ov[s][e] = r[d0 + e];
+  }
+  float M = -INFINITY;
+#pragma unroll
+  for (int s = 0; s < AT_MAX_SPLITS; ++s)
+    if (s < p.splits) M = fmaxf(M, ms[s]);
+  float acc[DPT], den = 0.f;
+#pragma unroll
+  for (int e = 0; e < DPT; ++e) acc[e] = 0.f;
+#pragma unroll
+  for (int s = 0; s < AT_MAX_SPLITS; ++s) {
+    const float wt = (s >= p.splits || ms[s] == -INFINITY) ? 0.f : exp2f(ms[s] - M);
+    den += wt * ls[s];
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) acc[e] += wt * ov[s][e];
+  }
+  const float inv = den > 0.f ? 1.f / den : 0.f;
+  S* O = reinterpret_cast<S*>(p.O) + (size_t)(b * p.rows_per_seq + row) * p.ldo + h * HD + d0;
+#pragma unroll
+  for (int e = 0; e < DPT; ++e) O[e] = T::from_f(acc[e] * inv);
 }
 
-size_t attention_part_floats(int, int, int, int, int) { return 0; }
+void plan_attention(AttnParams& p) {
+  const int G = std::max(1, p.n_heads / std::max(1, p.n_kv));
+  p.qph = (p.nq + 15) / 16;
+  p.qt_item = G * p.qph;
+  p.qgroups = (p.qt_item + AT_QT - 1) / AT_QT;
+  const int base = std::max(1, p.nbatch * p.n_kv * p.qgroups);
+  p.splits = std::max(1, std::min(AT_MAX_SPLITS, AT_TARGET_WGS / base));
+}
 
-template <typename S>
-static hipError_t launch_attn_t(AttnParams& p, hipStream_t st, const LaunchTiming* lt) {
-  const int items = p.nbatch * p.n_heads;
-  dim3 grid(8 * ((items + 7) / 8) * p.qtiles), block(ATT_THREADS);
-  auto go = [&](auto kern) {
-    if (lt) hipExtLaunchKernelGGL(kern, grid, block, 0, st, lt->start, lt->stop, 0, p);
-    else hipLaunchKernelGGL(kern, grid, block, 0, st, p);
-  };
-  switch (p.hd) {
-    case 32: go(attn_kernel<S, 32>); break;
-    case 64: go(attn_kernel<S, 64>); break;
-    case 128: go(attn_kernel<S, 128>); break;
-    default: return hipErrorInvalidValue;
+size_t attention_part_floats(const AttnParams& p0) {
+  AttnParams p = p0;
+  plan_attention(p);
+  if (p.splits == 1) return 0;
+  return (size_t)p.nbatch * p.n_kv * p.splits * p.qt_item * 16 * (size_t)(p.hd + 2);
+}
+
+template <typename S, int HD>
+static hipError_t launch_attn_hd(AttnParams& p, hipStream_t st, const LaunchTiming* lt) {
+  const int items = p.nbatch * p.n_kv;
+  const int per_xcd = (items + 7) / 8;
+  dim3 grid(8 * per_xcd * p.qgroups * p.splits), block(AT_THREADS);
+  const size_t lds = AttnShape<S, HD>::LDS;
+  static bool lds_attr = false;  // dynamic LDS above 64 KB is opted into once per kernel
+  if (!lds_attr) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<S, HD>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    lds_attr = true;
+  }
+  static_assert((size_t)AT_QT * 16 * (HD + 2) * 4 <= AttnShape<S, HD>::LDS, "merge records fit the chunk buffer");
+  // the merge kernel, if any, closes the timed interval
+  const bool merge = p.splits > 1;
+  if (lt) hipExtLaunchKernelGGL((attn_kernel<S, HD>), grid, block, (uint32_t)lds, st, lt->start,
+                                merge ? nullptr : lt->stop, 0, p);
+  else hipLaunchKernelGGL((attn_kernel<S, HD>), grid, block, lds, st, p);
+  if (merge) {
+    dim3 mgrid(8 * per_xcd * p.qt_item);
+    if (lt) hipExtLaunchKernelGGL((attn_merge_kernel<S, HD>), mgrid, dim3(256), 0, st, nullptr, lt->stop, 0, p);
+    else hipLaunchKernelGGL((attn_merge_kernel<S, HD>), mgrid, dim3(256), 0, st, p);
   }
   return hipGetLastError();
 }
 
+template <typename S>
+static hipError_t launch_attn_t(AttnParams& p, hipStream_t st, const LaunchTiming* lt) {
+  switch (p.hd) {
+    case 32: return launch_attn_hd<S, 32>(p, st, lt);
+    case 64: return launch_attn_hd<S, 64>(p, st, lt);
+    case 128: return launch_attn_hd<S, 128>(p, st, lt);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 hipError_t launch_attention(int dtype, AttnParams& p, int max_keys, hipStream_t st, const LaunchTiming* lt) {
-  plan_attention(p, max_keys);
+  plan_attention(p);
   if (p.nq <= 0 || p.nbatch <= 0) {  // nothing to launch: an empty timed interval
     if (lt) {
       (void)hipEventRecord(lt->start, st);
@@ -238,6 +423,8 @@ hipError_t launch_attention(int dtype, AttnParams& p, int max_keys, hipStream_t 
     }
     return hipSuccess;
   }
+  if (max_keys > AT_MAX_BLOCKS * 16 || p.n_kv <= 0 || p.n_heads % p.n_kv) return hipErrorInvalidValue;
+  if (p.splits > 1 && (!p.part || p.part_cap < attention_part_floats(p))) return hipErrorInvalidValue;
   return dtype == 1 ? launch_attn_t<bf16_t>(p, st, lt) : launch_attn_t<float>(p, st, lt);
 }
 

@@ -75,16 +75,23 @@ struct AttnParams {
   int causal;                      // tail mask: causal (1) or tree bitmask (0)
   const uint64_t* mask; int mask_words; int mask_seq_stride;  // per slot [T][words]
   int n_heads, n_kv, hd;
-  int nbatch, qtiles, splits, blocks_per_split;
+  int nbatch;
+  float* part; size_t part_cap;    // fp32 split partials (attention_part_floats), or null
+  // filled by plan_attention: query tiles per head, per (sequence, KV head), workgroups
+  // per (sequence, KV head) in the query direction, key splits
+  int qph, qt_item, qgroups, splits;
 };
+// Plans the launch (fields above) and runs it: the attention kernel and, with more than
+// one key split, the merge kernel.  max_keys bounds prefix + tail over the batch.
 hipError_t launch_attention(int dtype, AttnParams& p, int max_keys, hipStream_t st,
                             const LaunchTiming* lt = nullptr);
 // write rows [n][n_kv*hd] (storage) of K and V into the paged cache at slots slot0.. of seq
 hipError_t launch_kv_write(int dtype, const void* K, const void* V, int n, int slot0, int seq,
                            void* kcache, void* vcache, const int* block_table, int max_blocks,
                            int n_kv, int hd, hipStream_t st);
-size_t attention_part_floats(int nbatch, int qtiles, int n_heads, int splits, int hd);
-void plan_attention(AttnParams& p, int max_keys);
+// fp32 partial floats a launch with these shape fields needs (0 with one split)
+size_t attention_part_floats(const AttnParams& p);
+void plan_attention(AttnParams& p);
 
 // ---- row kernels -------------------------------------------------------------------------
 hipError_t launch_embed(int dtype, const void* emb, const int* tok, int M, int d, float* x,
