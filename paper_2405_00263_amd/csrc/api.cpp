@@ -142,6 +142,7 @@ struct Layout {
   size_t pool_bytes;
   size_t kpool, vpool, pool_ptrs, block_table, seq_len, seq_ids;
   size_t x, xa, xn, qbuf, obuf, act, vlogits, row_tok, row_pos, row_slot, row_seq, amax;
+  size_t rope_cs;  // [Mmax][hd/2] (cos, sin) of the current rows' positions
   size_t h0, t0, cand_token, cand_parent, cand_depth, cand_lp;
   size_t tree_token, tree_parent, tree_depth, tree_pos, tree_mask, target, acc, acc_len, out_tokens;
   size_t dstate[CLOVER_MAX_HEADS], dlogits[CLOVER_MAX_HEADS];
@@ -193,6 +194,7 @@ Layout make_layout(const clover_config& c) {
   L.row_pos = take(4 * (size_t)L.Mmax);
   L.row_slot = take(4 * (size_t)L.Mmax);
   L.row_seq = take(4 * (size_t)L.Mmax);
+  L.rope_cs = take(4 * (size_t)L.Mmax * c.head_dim);
   L.amax = take(4 * (size_t)L.Mv);
   L.h0 = take(4 * (size_t)c.max_batch * d);
   L.t0 = take(4 * (size_t)c.max_batch);
@@ -417,9 +419,9 @@ hipError_t run_layer(clover_ctx* c, const LayerPtrs& lw, int layer_idx, float* x
   g.X = xn; g.ldx = d; g.mode = EP_QKV;
   g.qbuf = c->at<void>(L.qbuf); g.ldq = qd;
   g.kcache = kp; g.vcache = vp;
-  g.row_seq = c->at<int>(L.row_seq); g.row_slot = c->at<int>(L.row_slot); g.row_pos = c->at<int>(L.row_pos);
+  g.row_seq = c->at<int>(L.row_seq); g.row_slot = c->at<int>(L.row_slot);
   g.block_table = c->at<int>(L.block_table); g.max_blocks = L.mbps;
-  g.n_heads = cf.n_heads; g.n_kv = cf.n_kv_heads; g.hd = hd; g.theta = cf.rope_theta;
+  g.n_heads = cf.n_heads; g.n_kv = cf.n_kv_heads; g.hd = hd; g.rope_cs = c->at<float>(L.rope_cs);
   if ((e = run_gemm(c, g, M, d, {{lw.wq, qd}, {lw.wk, kvd}, {lw.wv, kvd}}))) return e;
   att.Q = c->at<void>(L.qbuf); att.ldq = qd;
   att.O = c->at<void>(L.obuf); att.ldo = qd;
@@ -485,6 +487,7 @@ hipError_t enq_verify(clover_ctx* c, int B, int max_keys) {
   float* x = c->at<float>(L.x);
   float* xa = c->at<float>(L.xa);
   HE(launch_embed(cf.dtype, c->emb, c->at<int>(L.row_tok), M, d, x, c->st));
+  HE(launch_rope_table(c->at<int>(L.row_pos), M, cf.head_dim, cf.rope_theta, c->at<float>(L.rope_cs), c->st));
   AttnParams att{};
   att.seq_ids = c->at<int>(L.seq_ids);
   att.prefix_dev = c->at<int>(L.seq_len);
@@ -933,6 +936,7 @@ clover_status clover_prefill(clover_ctx* c, int32_t seq, const int32_t* tokens, 
     HIPCK(c, hipMemcpyAsync(c->at<int>(L.row_slot), meta.data() + 2 * C, sizeof(int) * rows, hipMemcpyHostToDevice, c->st));
     HIPCK(c, hipMemcpyAsync(c->at<int>(L.row_seq), meta.data() + 3 * C, sizeof(int) * rows, hipMemcpyHostToDevice, c->st));
     HIPCK(c, launch_embed(cf.dtype, c->emb, c->at<int>(L.row_tok), rows, d, x, c->st));
+    HIPCK(c, launch_rope_table(c->at<int>(L.row_pos), rows, cf.head_dim, cf.rope_theta, c->at<float>(L.rope_cs), c->st));
     AttnParams att{};
     att.seq_ids = c->at<int>(L.seq_ids);
     att.prefix_dev = nullptr; att.prefix_host = c0;

@@ -70,7 +70,7 @@ __device__ __forceinline__ const u32x4_t* wave_weight_ptr(const GemmParams& p, i
 
 template <typename S, int NW>
 __device__ void gemm_epilogue(const GemmParams& p, const float* tile, int g, int m0, int mrows,
-                              const int* s_pos, const int* s_kvbase) {
+                              const int* s_kvbase) {
   using T = St<S>;
   constexpr int THREADS = NW * 64, COLS = NW * 16, TSTRIDE = COLS + 4;
   const int tid = threadIdx.x;
@@ -101,19 +101,16 @@ __device__ void gemm_epilogue(const GemmParams& p, const float* tile, int g, int
     n = pt * 16 + jj;
     d = n % hd;
   }
-  double inv = 0.0;
-  if (rot) inv = pow((double)p.theta, -2.0 * (double)((d < half) ? d : d - half) / (double)hd);
+  const int dlo = (d < half) ? d : d - half;  // rotary frequency index
+  const float2* rcs = reinterpret_cast<const float2*>(p.rope_cs);
   for (int r = tid / COLS; r < mrows; r += THREADS / COLS) {
     const int m = m0 + r;
     if (m >= p.M) break;
     float v = tile[r * TSTRIDE + col];
     if (rot) {
       const float partner = tile[r * TSTRIDE + (col ^ 8)];
-      double ang = (double)s_pos[r] * inv;
-      ang -= 6.283185307179586 * rint(ang * 0.15915494309189535);
-      float sn, cs;
-      sincosf((float)ang, &sn, &cs);
-      v = (jj < 8) ? (v * cs - partner * sn) : (v * cs + partner * sn);
+      const float2 cs = rcs[(size_t)m * half + dlo];
+      v = (jj < 8) ? (v * cs.x - partner * cs.y) : (v * cs.x + partner * cs.y);
     }
     if (n < qd) {
       reinterpret_cast<S*>(p.qbuf)[(size_t)m * p.ldq + n] = T::from_f(v);
@@ -151,13 +148,12 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(const GemmParams p) {
   const int nk = c1 - c0;
   const int nst = (nk + STAGE_CHUNKS - 1) / STAGE_CHUNKS;
 
-  // row metadata of the fused rotary + KV-append epilogue, loaded once up front so the
-  // epilogue's row loop has no dependent global loads
-  __shared__ int s_pos[MROWS], s_kvbase[MROWS];
+  // KV-append targets of the fused epilogue, loaded once up front so the epilogue's row
+  // loop has no dependent global loads
+  __shared__ int s_kvbase[MROWS];
   if (p.mode == EP_QKV && threadIdx.x < MROWS) {
     const int m = min(m0 + (int)threadIdx.x, p.M - 1);
     const int slot = p.row_slot[m];
-    s_pos[threadIdx.x] = p.row_pos[m];
     s_kvbase[threadIdx.x] = p.block_table[(size_t)p.row_seq[m] * p.max_blocks + (slot >> 4)] * 16 + (slot & 15);
   }
 
@@ -274,7 +270,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(const GemmParams p) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) tile[(t * 16 + 4 * (lane >> 4) + r) * TSTRIDE + col] = acc[t][r];
   __syncthreads();
-  gemm_epilogue<S, NW>(p, tile, g, m0, MROWS, s_pos, s_kvbase);
+  gemm_epilogue<S, NW>(p, tile, g, m0, MROWS, s_kvbase);
 }
 
 // ---- host side ------------------------------------------------------------------------

@@ -37,10 +37,10 @@ struct GemmParams {
   // EP_QKV
   void* qbuf; int ldq;
   void* kcache; void* vcache;
-  const int* row_seq; const int* row_slot; const int* row_pos;
+  const int* row_seq; const int* row_slot;
   const int* block_table; int max_blocks;
   int n_heads, n_kv, hd;
-  float theta;
+  const float* rope_cs;  // [M][hd/2] (cos, sin) pairs of each row's position (launch_rope_table)
 };
 
 struct GemmPlan {
@@ -96,6 +96,8 @@ void plan_attention(AttnParams& p);
 // ---- row kernels -------------------------------------------------------------------------
 hipError_t launch_embed(int dtype, const void* emb, const int* tok, int M, int d, float* x,
                         hipStream_t st);
+// cs[m][i] = (cos, sin)(pos[m] * theta^(-2i/hd)), i < hd/2: the rotary factors of each row
+hipError_t launch_rope_table(const int* pos, int M, int hd, float theta, float* cs, hipStream_t st);
 // keys: M u64 scratch; keys_zeroed: a previous kernel already cleared them
 hipError_t launch_argmax(const float* logits, int M, int V, int* out, unsigned long long* keys,
                          bool keys_zeroed, hipStream_t st);

@@ -18,6 +18,30 @@ __global__ void embed_kernel(const S* __restrict__ emb, const int* __restrict__ 
   for (int k = threadIdx.x; k < d; k += blockDim.x) x[(size_t)m * d + k] = St<S>::to_f(row[k]);
 }
 
+// Rotary factors of each row's position (rotate-half pairing): the angle is formed and
+// reduced to [-pi, pi] in double precision, then sin/cos are taken in single precision.
+__global__ void rope_table_kernel(const int* __restrict__ pos, int M, int hd, float theta,
+                                  float* __restrict__ cs) {
+  const int half = hd / 2;
+  for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < M * half; e += gridDim.x * blockDim.x) {
+    const int m = e / half, i = e % half;
+    const double inv = pow((double)theta, -2.0 * (double)i / (double)hd);
+    double ang = (double)pos[m] * inv;
+    ang -= 6.283185307179586 * rint(ang * 0.15915494309189535);
+    float sn, c;
+    sincosf((float)ang, &sn, &c);
+    cs[2 * (size_t)e] = c;
+    cs[2 * (size_t)e + 1] = sn;
+  }
+}
+
+hipError_t launch_rope_table(const int* pos, int M, int hd, float theta, float* cs, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  const int n = M * (hd / 2);
+  hipLaunchKernelGGL(rope_table_kernel, dim3((n + 255) / 256), dim3(256), 0, st, pos, M, hd, theta, cs);
+  return hipGetLastError();
+}
+
 hipError_t launch_embed(int dtype, const void* emb, const int* tok, int M, int d, float* x,
                         hipStream_t st) {
   if (M <= 0) return hipSuccess;
