@@ -281,7 +281,10 @@ struct clover_ctx {
   std::vector<std::vector<int>> seq_blocks;  // physical KV blocks per slot
   std::vector<int> free_blocks;
   std::vector<int> bt_host;
-  std::vector<int> host_ids, host_len, host_out;
+  std::vector<int> host_ids, host_len;
+  int* pin_ids = nullptr;   // pinned host staging of the step's sequence ids [max_batch]
+  int* pin_len = nullptr;   // ... and of the committed lengths [max_batch]
+  int* pin_out = nullptr;   // ... and of the emitted tokens [max_batch][H+1]
   std::string err;
   bool dead = false;
   hipEvent_t ev[4];
@@ -552,16 +555,20 @@ hipError_t enq_accept(clover_ctx* c, int B) {
 clover_status finish_step(clover_ctx* c, int B, int* out_tokens, int* out_count) {
   const Layout& L = c->L;
   const int H = L.H;
-  c->host_out.resize((size_t)B * (H + 1));
-  HIPCK(c, hipMemcpyAsync(c->host_out.data(), c->at<int>(L.out_tokens), sizeof(int) * B * (H + 1),
+  HIPCK(c, hipMemcpyAsync(c->pin_out, c->at<int>(L.out_tokens), sizeof(int) * B * (H + 1),
                           hipMemcpyDeviceToHost, c->st));
   HIPCK(c, hipEventRecord(c->ev[3], c->st));
-  HIPCK(c, hipStreamSynchronize(c->st));
+  // poll rather than block: the step's end is the latency the caller sees
+  for (;;) {
+    const hipError_t q = hipEventQuery(c->ev[3]);
+    if (q == hipSuccess) break;
+    if (q != hipErrorNotReady) HIPCK(c, q);
+  }
   prof_collect(c);
   for (int b = 0; b < B; ++b) {
     int n = 0;
     for (int i = 0; i <= H; ++i) {
-      const int t = c->host_out[(size_t)b * (H + 1) + i];
+      const int t = c->pin_out[(size_t)b * (H + 1) + i];
       out_tokens[(size_t)b * (H + 1) + i] = t;
       if (t >= 0) ++n;
     }
@@ -703,10 +710,12 @@ clover_status begin_batch(clover_ctx* c, const int32_t* seqs, int B, int& max_ke
     if (st != CLOVER_OK) return st;
     max_keys = std::max(max_keys, c->seq_len[s] + L.T);
   }
-  c->host_len.assign(c->seq_len.begin(), c->seq_len.end());
-  for (auto& v : c->host_len) v = std::max(v, 0);
-  HIPCK(c, hipMemcpyAsync(c->at<int>(L.seq_ids), c->host_ids.data(), sizeof(int) * B, hipMemcpyHostToDevice, c->st));
-  HIPCK(c, hipMemcpyAsync(c->at<int>(L.seq_len), c->host_len.data(), sizeof(int) * c->cfg.max_batch,
+  // pinned staging: the previous step has completed (finish_step waited for it), so the
+  // buffers are free to overwrite
+  for (int b = 0; b < B; ++b) c->pin_ids[b] = seqs[b];
+  for (int i = 0; i < c->cfg.max_batch; ++i) c->pin_len[i] = std::max(c->seq_len[i], 0);
+  HIPCK(c, hipMemcpyAsync(c->at<int>(L.seq_ids), c->pin_ids, sizeof(int) * B, hipMemcpyHostToDevice, c->st));
+  HIPCK(c, hipMemcpyAsync(c->at<int>(L.seq_len), c->pin_len, sizeof(int) * c->cfg.max_batch,
                           hipMemcpyHostToDevice, c->st));
   return CLOVER_OK;
 }
@@ -860,6 +869,11 @@ clover_status clover_init(const clover_config* cfg, void* const* weights, void* 
   for (int i = 0; i < 4; ++i)
     if ((e = hipEventCreate(&c->ev[i])) != hipSuccess) return fail(e, "event");
   if ((e = hipStreamCreateWithFlags(&c->cap_st, hipStreamNonBlocking)) != hipSuccess) return fail(e, "capture stream");
+  const size_t H1 = (size_t)c->L.H + 1;
+  if ((e = hipHostMalloc((void**)&c->pin_ids, sizeof(int) * cfg->max_batch, hipHostMallocDefault)) != hipSuccess ||
+      (e = hipHostMalloc((void**)&c->pin_len, sizeof(int) * cfg->max_batch, hipHostMallocDefault)) != hipSuccess ||
+      (e = hipHostMalloc((void**)&c->pin_out, sizeof(int) * cfg->max_batch * H1, hipHostMallocDefault)) != hipSuccess)
+    return fail(e, "pinned staging");
   // zero the KV pools (attention reads whole 16-key blocks), counters and state
   if ((e = hipMemsetAsync(c->ws, 0, L.pool_ptrs, c->st)) != hipSuccess) return fail(e, "memset pools");
   if ((e = hipMemsetAsync(c->ws + L.block_table, 0, L.x - L.block_table, c->st)) != hipSuccess) return fail(e, "memset state");
@@ -885,6 +899,8 @@ void clover_destroy(clover_ctx* ctx) {
     for (hipGraphExec_t x : {g.draft, g.verify, g.accept})
       if (x) (void)hipGraphExecDestroy(x);
   if (ctx->cap_st) (void)hipStreamDestroy(ctx->cap_st);
+  for (int* p : {ctx->pin_ids, ctx->pin_len, ctx->pin_out})
+    if (p) (void)hipHostFree(p);
   delete ctx;
 }
 
