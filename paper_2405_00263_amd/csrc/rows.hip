@@ -387,42 +387,126 @@ hipError_t launch_rowfix(int dtype, RowFixParams& p, hipStream_t st) {
 
 // ---- Attention Decoder input preparation (Sec. 3.2 Eq. 1, Sec. 3.4) -------------------------
 // For frontier row f: h = parent state, a = RMSNorm_ad(h), e = W_lm[token] / ||W_lm[token]||.
+// 16-byte vectors of storage elements <-> floats
+__device__ __forceinline__ void vec_unpack(u32x4_t v, float* out, bf16_t) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    out[2 * i] = __uint_as_float(v[i] << 16);
+    out[2 * i + 1] = __uint_as_float(v[i] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ void vec_unpack(u32x4_t v, float* out, float) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) out[i] = __uint_as_float(v[i]);
+}
+__device__ __forceinline__ u32x4_t vec_pack(const float* in, bf16_t) {
+  u32x4_t v;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = (uint32_t)f2bf(in[2 * i]) | ((uint32_t)f2bf(in[2 * i + 1]) << 16);
+  return v;
+}
+__device__ __forceinline__ u32x4_t vec_pack(const float* in, float) {
+  u32x4_t v;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = __float_as_uint(in[i]);
+  return v;
+}
+
+// Attention Decoder inputs of one frontier row (Sec. 3.2, 3.4): a = RMSNorm(h) * g (storage),
+// e = W_lm[tok] / max(||W_lm[tok]||_2, 1e-12) (storage) and a float copy of h.  Each
+// thread owns whole 16-byte segments s (elements [s*EPL, s*EPL + EPL)): of h, of the gain,
+// and of the token's LM-head row, which the packed layout keeps as one vector per segment
+// (fragment s/4, lane group s%4).  Everything is loaded once, up front; one combined
+// reduction gives both norms.
+static constexpr int AD_MAXV = 8;  // segments per thread: d <= 256 * 8 * EPL
 template <typename S>
 __global__ __launch_bounds__(256) void ad_prep_kernel(const AdPrepParams p) {
   using T = St<S>;
-  __shared__ float red[4];
+  constexpr int EPL = T::EPL;
+  __shared__ float red[2][4];
   const int f = blockIdx.x, b = f / p.F, fl = f % p.F;
   const int slot = p.seq_ids[b];
-  const int d = p.d;
+  const int d = p.d, nseg = d / EPL;
   const float* h = p.use_slot_state ? p.prev + (size_t)slot * d
                                     : p.prev + (size_t)(b * p.Fprev + fl / p.kprev) * d;
-  const int tok = p.cand_token[(size_t)slot * p.cand_stride + p.base_node + fl];
-  const S* lm = reinterpret_cast<const S*>(p.lm_packed);
-  float ss = 0.f, se = 0.f;
-  for (int k = threadIdx.x; k < d; k += 256) {
-    const float v = h[k];
-    ss += v * v;
-    const float w = T::to_f(lm[packed_index(tok, k, p.lm_nchunks, T::EPL)]);
-    se += w * w;
+  float hv[AD_MAXV][EPL];
+#pragma unroll
+  for (int i = 0; i < AD_MAXV; ++i) {
+    const int sg = threadIdx.x + i * 256;
+    if (sg < nseg) {
+#pragma unroll
+      for (int q = 0; q < EPL / 4; ++q) {
+        const float4 v = *reinterpret_cast<const float4*>(h + (size_t)sg * EPL + 4 * q);
+        hv[i][4 * q] = v.x; hv[i][4 * q + 1] = v.y; hv[i][4 * q + 2] = v.z; hv[i][4 * q + 3] = v.w;
+      }
+    }
   }
-  ss = block_sum256(ss, red);
-  se = block_sum256(se, red);
+  const int tok = p.cand_token[(size_t)slot * p.cand_stride + p.base_node + fl];
+  const u32x4_t* lm = reinterpret_cast<const u32x4_t*>(p.lm_packed) + (size_t)(tok >> 4) * p.lm_nchunks * 64 + (tok & 15);
+  const u32x4_t* gain = reinterpret_cast<const u32x4_t*>(p.ad_norm);
+  u32x4_t lv[AD_MAXV], gv[AD_MAXV];
+#pragma unroll
+  for (int i = 0; i < AD_MAXV; ++i) {
+    const int sg = threadIdx.x + i * 256;
+    if (sg < nseg) {
+      lv[i] = lm[(size_t)(sg >> 2) * 64 + 16 * (sg & 3)];
+      gv[i] = gain[sg];
+    }
+  }
+  float ss = 0.f, se = 0.f;
+  float ev[AD_MAXV][EPL];
+#pragma unroll
+  for (int i = 0; i < AD_MAXV; ++i) {
+    const int sg = threadIdx.x + i * 256;
+    if (sg < nseg) {
+      vec_unpack(lv[i], ev[i], S{});
+#pragma unroll
+      for (int q = 0; q < EPL; ++q) {
+        ss += hv[i][q] * hv[i][q];
+        se += ev[i][q] * ev[i][q];
+      }
+    }
+  }
+  ss = warp_sum(ss);
+  se = warp_sum(se);
+  if ((threadIdx.x & 63) == 0) {
+    red[0][threadIdx.x >> 6] = ss;
+    red[1][threadIdx.x >> 6] = se;
+  }
+  __syncthreads();
+  ss = red[0][0] + red[0][1] + red[0][2] + red[0][3];
+  se = red[1][0] + red[1][1] + red[1][2] + red[1][3];
   const float rinv = 1.0f / sqrtf(ss / (float)d + p.eps);
   const float einv = 1.0f / fmaxf(sqrtf(se), 1e-12f);
-  const S* gain = reinterpret_cast<const S*>(p.ad_norm);
-  S* a = reinterpret_cast<S*>(p.a_out) + (size_t)f * d;
-  S* e = reinterpret_cast<S*>(p.e_out) + (size_t)f * d;
-  for (int k = threadIdx.x; k < d; k += 256) {
-    const float v = h[k];
-    p.hin[(size_t)f * d + k] = v;
-    a[k] = T::from_f(v * rinv * T::to_f(gain[k]));
-    e[k] = T::from_f(T::to_f(lm[packed_index(tok, k, p.lm_nchunks, T::EPL)]) * einv);
+  u32x4_t* a = reinterpret_cast<u32x4_t*>(p.a_out) + (size_t)f * nseg;
+  u32x4_t* e = reinterpret_cast<u32x4_t*>(p.e_out) + (size_t)f * nseg;
+  float* hin = p.hin + (size_t)f * d;
+#pragma unroll
+  for (int i = 0; i < AD_MAXV; ++i) {
+    const int sg = threadIdx.x + i * 256;
+    if (sg < nseg) {
+      float g[EPL], av[EPL], eo[EPL];
+      vec_unpack(gv[i], g, S{});
+#pragma unroll
+      for (int q = 0; q < EPL; ++q) {
+        av[q] = hv[i][q] * rinv * g[q];
+        eo[q] = ev[i][q] * einv;
+      }
+      a[sg] = vec_pack(av, S{});
+      e[sg] = vec_pack(eo, S{});
+#pragma unroll
+      for (int q = 0; q < EPL / 4; ++q)
+        *reinterpret_cast<float4*>(hin + (size_t)sg * EPL + 4 * q) =
+            make_float4(hv[i][4 * q], hv[i][4 * q + 1], hv[i][4 * q + 2], hv[i][4 * q + 3]);
+    }
   }
 }
 
 hipError_t launch_ad_prep(int dtype, AdPrepParams& p, hipStream_t st) {
   const int M = p.nbatch * p.F;
   if (M <= 0) return hipSuccess;
+  const int epl = dtype == 1 ? 8 : 4;
+  if (p.d % epl || p.d > 256 * AD_MAXV * epl) return hipErrorInvalidValue;
   if (dtype == 1)
     hipLaunchKernelGGL(ad_prep_kernel<bf16_t>, dim3(M), dim3(256), 0, st, p);
   else
