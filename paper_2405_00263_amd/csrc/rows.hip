@@ -10,12 +10,46 @@
 namespace clover {
 
 // ---- embedding: x[m] = emb[tok[m]] --------------------------------------------------------
+// 16-byte vectors of storage elements <-> floats
+__device__ __forceinline__ void vec_unpack(u32x4_t v, float* out, bf16_t) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    out[2 * i] = __uint_as_float(v[i] << 16);
+    out[2 * i + 1] = __uint_as_float(v[i] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ void vec_unpack(u32x4_t v, float* out, float) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) out[i] = __uint_as_float(v[i]);
+}
+__device__ __forceinline__ u32x4_t vec_pack(const float* in, bf16_t) {
+  u32x4_t v;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = (uint32_t)f2bf(in[2 * i]) | ((uint32_t)f2bf(in[2 * i + 1]) << 16);
+  return v;
+}
+__device__ __forceinline__ u32x4_t vec_pack(const float* in, float) {
+  u32x4_t v;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = __float_as_uint(in[i]);
+  return v;
+}
+
 template <typename S>
 __global__ void embed_kernel(const S* __restrict__ emb, const int* __restrict__ tok, int d,
                              float* __restrict__ x) {
+  // 16-byte segments of the embedding row (EPL elements each), widened to float
+  constexpr int EPL = St<S>::EPL;
   const int m = blockIdx.x;
-  const S* row = emb + (size_t)tok[m] * d;
-  for (int k = threadIdx.x; k < d; k += blockDim.x) x[(size_t)m * d + k] = St<S>::to_f(row[k]);
+  const u32x4_t* row = reinterpret_cast<const u32x4_t*>(emb + (size_t)tok[m] * d);
+  float* out = x + (size_t)m * d;
+  for (int sg = threadIdx.x; sg < d / EPL; sg += blockDim.x) {
+    float v[EPL];
+    vec_unpack(row[sg], v, S{});
+#pragma unroll
+    for (int q = 0; q < EPL / 4; ++q)
+      *reinterpret_cast<float4*>(out + sg * EPL + 4 * q) = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+  }
 }
 
 // Rotary factors of each row's position (rotate-half pairing): the angle is formed and
@@ -308,6 +342,15 @@ static constexpr int FIX_THREADS = 1024;
 static constexpr int FIX_MAXS = 8;
 static constexpr int FIX_VEC = 2;  // float4 per thread: d <= 8192
 
+// four consecutive storage elements in one store
+__device__ __forceinline__ void store4(bf16_t* p, float a, float b, float c, float d) {
+  *reinterpret_cast<u32x2_t*>(p) = u32x2_t{(uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16),
+                                           (uint32_t)f2bf(c) | ((uint32_t)f2bf(d) << 16)};
+}
+__device__ __forceinline__ void store4(float* p, float a, float b, float c, float d) {
+  *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);
+}
+
 template <typename S>
 __global__ __launch_bounds__(FIX_THREADS) void rowfix_kernel(const RowFixParams p) {
   using T = St<S>;
@@ -318,9 +361,15 @@ __global__ __launch_bounds__(FIX_THREADS) void rowfix_kernel(const RowFixParams 
   float4 acc[FIX_VEC];
   float4 part[FIX_MAXS][FIX_VEC];
   float4 res[FIX_VEC];
+  float4 gn[FIX_VEC];  // RMSNorm gain, loaded with everything else before the reduction
 #pragma unroll
   for (int i = 0; i < FIX_VEC; ++i) {
     const int e = threadIdx.x * 4 + i * FIX_THREADS * 4;
+    gn[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (e < d && p.out_norm) {
+      const S* g = reinterpret_cast<const S*>(p.gain) + e;
+      gn[i] = make_float4(T::to_f(g[0]), T::to_f(g[1]), T::to_f(g[2]), T::to_f(g[3]));
+    }
     res[i] = make_float4(0.f, 0.f, 0.f, 0.f);
     if (e < d && p.resid) res[i] = *reinterpret_cast<const float4*>(p.resid + (size_t)m * p.ldr + e);
 #pragma unroll
@@ -362,16 +411,13 @@ __global__ __launch_bounds__(FIX_THREADS) void rowfix_kernel(const RowFixParams 
   float tot = 0.f;
   for (int q = 0; q < FIX_THREADS / 64; ++q) tot += red[q];
   const float rinv = 1.0f / sqrtf(tot / (float)d + p.eps);
-  const S* gain = reinterpret_cast<const S*>(p.gain);
 #pragma unroll
   for (int i = 0; i < FIX_VEC; ++i) {
     const int e = threadIdx.x * 4 + i * FIX_THREADS * 4;
     if (e >= d) continue;
     S* on = reinterpret_cast<S*>(p.out_norm) + (size_t)m * p.ldn + e;
-    on[0] = T::from_f(acc[i].x * rinv * T::to_f(gain[e]));
-    on[1] = T::from_f(acc[i].y * rinv * T::to_f(gain[e + 1]));
-    on[2] = T::from_f(acc[i].z * rinv * T::to_f(gain[e + 2]));
-    on[3] = T::from_f(acc[i].w * rinv * T::to_f(gain[e + 3]));
+    store4(on, acc[i].x * rinv * gn[i].x, acc[i].y * rinv * gn[i].y, acc[i].z * rinv * gn[i].z,
+           acc[i].w * rinv * gn[i].w);
   }
 }
 
@@ -387,31 +433,6 @@ hipError_t launch_rowfix(int dtype, RowFixParams& p, hipStream_t st) {
 
 // ---- Attention Decoder input preparation (Sec. 3.2 Eq. 1, Sec. 3.4) -------------------------
 // For frontier row f: h = parent state, a = RMSNorm_ad(h), e = W_lm[token] / ||W_lm[token]||.
-// 16-byte vectors of storage elements <-> floats
-__device__ __forceinline__ void vec_unpack(u32x4_t v, float* out, bf16_t) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    out[2 * i] = __uint_as_float(v[i] << 16);
-    out[2 * i + 1] = __uint_as_float(v[i] & 0xffff0000u);
-  }
-}
-__device__ __forceinline__ void vec_unpack(u32x4_t v, float* out, float) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) out[i] = __uint_as_float(v[i]);
-}
-__device__ __forceinline__ u32x4_t vec_pack(const float* in, bf16_t) {
-  u32x4_t v;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) v[i] = (uint32_t)f2bf(in[2 * i]) | ((uint32_t)f2bf(in[2 * i + 1]) << 16);
-  return v;
-}
-__device__ __forceinline__ u32x4_t vec_pack(const float* in, float) {
-  u32x4_t v;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) v[i] = __float_as_uint(in[i]);
-  return v;
-}
-
 // Attention Decoder inputs of one frontier row (Sec. 3.2, 3.4): a = RMSNorm(h) * g (storage),
 // e = W_lm[tok] / max(||W_lm[tok]||_2, 1e-12) (storage) and a float copy of h.  Each
 // thread owns whole 16-byte segments s (elements [s*EPL, s*EPL + EPL)): of h, of the gain,
