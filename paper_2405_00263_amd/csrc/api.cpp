@@ -40,6 +40,7 @@ void set_global_err(const char* fmt, ...) {
 
 constexpr size_t ALIGN = 256;
 constexpr int GEMM_MAX_SPLITS = 8;
+constexpr int QKV_MAX_SPLITS = 2;  // Q|K|V may be split when the plan prefers it (fix-up pass)
 size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 int es_of(int dtype) { return dtype == CLOVER_BF16 ? 2 : 4; }
@@ -231,7 +232,8 @@ Layout make_layout(const clover_config& c) {
   // split-K partials [S][M][N] of the residual-type GEMMs (at most GEMM_MAX_SPLITS)
   const size_t maxM = std::max<size_t>({(size_t)L.Mv, (size_t)L.Mp, (size_t)L.Fmaxrows});
   const size_t maxN = std::max<size_t>({(size_t)d, (size_t)qd});
-  L.gpart_floats = (size_t)GEMM_MAX_SPLITS * maxM * maxN;
+  L.gpart_floats = std::max((size_t)GEMM_MAX_SPLITS * maxM * maxN,
+                            (size_t)QKV_MAX_SPLITS * maxM * (size_t)(qd + 2 * c.n_kv_heads * c.head_dim));
   L.gpart2_floats = (size_t)GEMM_MAX_SPLITS * L.Fmaxrows * 2 * qd;  // Attention Decoder keys/values
   L.gpart = take(4 * L.gpart_floats);
   L.gpart2 = take(4 * L.gpart2_floats);
@@ -425,7 +427,18 @@ hipError_t run_layer(clover_ctx* c, const LayerPtrs& lw, int layer_idx, float* x
   g.row_seq = c->at<int>(L.row_seq); g.row_slot = c->at<int>(L.row_slot);
   g.block_table = c->at<int>(L.block_table); g.max_blocks = L.mbps;
   g.n_heads = cf.n_heads; g.n_kv = cf.n_kv_heads; g.hd = hd; g.rope_cs = c->at<float>(L.rope_cs);
-  if ((e = run_gemm(c, g, M, d, {{lw.wq, qd}, {lw.wk, kvd}, {lw.wv, kvd}}))) return e;
+  const int qkv_tiles = (qd + 2 * kvd) / 16, kc = kc_of(cf.dtype);
+  if (plan_gemm(cf.dtype, M, qkv_tiles, d / kc, false, QKV_MAX_SPLITS).S > 1) {
+    // K-split Q|K|V: partials, then the fix-up pass (sums, rotary, stores)
+    g.mode = EP_PARTIAL; g.max_splits = QKV_MAX_SPLITS; g.part = part;
+    int sq = 1;
+    if ((e = run_gemm(c, g, M, d, {{lw.wq, qd}, {lw.wk, kvd}, {lw.wv, kvd}}, &sq))) return e;
+    g.M = M;
+    ProfScope ps(c, CLOVER_KSTAT_OTHER, 0, 0);
+    if ((e = launch_qkv_fix(cf.dtype, g, part, sq, c->st))) return e;
+  } else if ((e = run_gemm(c, g, M, d, {{lw.wq, qd}, {lw.wk, kvd}, {lw.wv, kvd}}))) {
+    return e;
+  }
   att.Q = c->at<void>(L.qbuf); att.ldq = qd;
   att.O = c->at<void>(L.obuf); att.ldo = qd;
   att.kcache = kp; att.vcache = vp;

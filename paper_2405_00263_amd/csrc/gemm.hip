@@ -68,6 +68,44 @@ __device__ __forceinline__ const u32x4_t* wave_weight_ptr(const GemmParams& p, i
   return reinterpret_cast<const u32x4_t*>(p.seg[seg].w) + (size_t)t * p.nchunks * 64;
 }
 
+// Finishes one value of the packed Q|K|V output: physical column pc (tile-local rotary
+// order), row m.  v and its rotary partner (physical column pc ^ 8) are the complete sums;
+// kb = physical KV block * 16 + key slot of row m.  Q/K get the rotary factors of row m's
+// position (rope_cs), Q goes to qbuf, K/V to the paged cache.
+template <typename S>
+__device__ __forceinline__ void qkv_store(const GemmParams& p, int m, int pc, float v, float partner, int kb) {
+  using T = St<S>;
+  const int hd = p.hd, half = hd >> 1, qd = p.n_heads * hd, kvd = p.n_kv * hd;
+  const int pt = pc >> 4, jj = pc & 15;
+  const int qt = qd / 16, kt = kvd / 16;
+  const bool rot = pt < qt + kt;
+  int n;  // logical output column
+  if (rot) {
+    const int seg0 = pt < qt ? 0 : qt;
+    n = seg0 * 16 + rope_row(pt - seg0, jj, hd);
+  } else {
+    n = pc;
+  }
+  const int d = n % hd;
+  if (rot) {
+    const int dlo = (d < half) ? d : d - half;  // rotary frequency index
+    const float2 cs = reinterpret_cast<const float2*>(p.rope_cs)[(size_t)m * half + dlo];
+    v = (jj < 8) ? (v * cs.x - partner * cs.y) : (v * cs.x + partner * cs.y);
+  }
+  if (n < qd) {
+    reinterpret_cast<S*>(p.qbuf)[(size_t)m * p.ldq + n] = T::from_f(v);
+  } else {
+    const bool isk = n < qd + kvd;
+    const int kvh = (isk ? n - qd : n - qd - kvd) / hd;
+    const size_t base = ((size_t)(kb >> 4) * p.n_kv + kvh) * (size_t)(16 * hd);
+    const int key = kb & 15;
+    if (isk)
+      reinterpret_cast<S*>(p.kcache)[base + kblk_off(key, d, T::EPL)] = T::from_f(v);
+    else
+      reinterpret_cast<S*>(p.vcache)[base + vblk_off(key, d)] = T::from_f(v);
+  }
+}
+
 template <typename S, int NW>
 __device__ void gemm_epilogue(const GemmParams& p, const float* tile, int g, int m0, int mrows,
                               const int* s_kvbase) {
@@ -86,45 +124,13 @@ __device__ void gemm_epilogue(const GemmParams& p, const float* tile, int g, int
     return;
   }
   // EP_QKV.  Each thread owns one column of the tile (THREADS / COLS == 4 rows at a time).
-  const int col = tid % COLS, w = col >> 4, jj = col & 15;
-  const int hd = p.hd, half = hd >> 1, qd = p.n_heads * hd, kvd = p.n_kv * hd;
-  const int pt = g * NW + w;  // physical tile over [q; k; v]
-  const int qt = qd / 16, kt = kvd / 16;
-  if (pt >= qt + 2 * kt) return;
-  const bool rot = pt < qt + kt;
-  int n, d;  // logical output column and its dimension within the head
-  if (rot) {
-    const int seg0 = pt < qt ? 0 : qt;
-    n = seg0 * 16 + rope_row(pt - seg0, jj, hd);
-    d = n % hd;
-  } else {
-    n = pt * 16 + jj;
-    d = n % hd;
-  }
-  const int dlo = (d < half) ? d : d - half;  // rotary frequency index
-  const float2* rcs = reinterpret_cast<const float2*>(p.rope_cs);
+  const int col = tid % COLS;
+  const int pc = g * COLS + col;  // physical column over the packed [q; k; v] tiles
+  if (pc >= (p.n_heads + 2 * p.n_kv) * p.hd) return;
   for (int r = tid / COLS; r < mrows; r += THREADS / COLS) {
     const int m = m0 + r;
     if (m >= p.M) break;
-    float v = tile[r * TSTRIDE + col];
-    if (rot) {
-      const float partner = tile[r * TSTRIDE + (col ^ 8)];
-      const float2 cs = rcs[(size_t)m * half + dlo];
-      v = (jj < 8) ? (v * cs.x - partner * cs.y) : (v * cs.x + partner * cs.y);
-    }
-    if (n < qd) {
-      reinterpret_cast<S*>(p.qbuf)[(size_t)m * p.ldq + n] = T::from_f(v);
-    } else {
-      const bool isk = n < qd + kvd;
-      const int kvh = (isk ? n - qd : n - qd - kvd) / hd;
-      const int kb = s_kvbase[r];  // physical block * 16 + key
-      const size_t base = ((size_t)(kb >> 4) * p.n_kv + kvh) * (size_t)(16 * hd);
-      const int key = kb & 15;
-      if (isk)
-        reinterpret_cast<S*>(p.kcache)[base + kblk_off(key, d, T::EPL)] = T::from_f(v);
-      else
-        reinterpret_cast<S*>(p.vcache)[base + vblk_off(key, d)] = T::from_f(v);
-    }
+    qkv_store<S>(p, m, pc, tile[r * TSTRIDE + col], tile[r * TSTRIDE + (col ^ 8)], s_kvbase[r]);
   }
 }
 
@@ -295,6 +301,24 @@ static double plan_cost(const GemmPlan& pl, int es, int M, int ntiles, int nchun
   return std::max(t_cu, t_hbm) + 0.1 * std::min(t_cu, t_hbm);
 }
 
+// Shapes of the shipped workloads whose best (waves, splits) a forced-plan sweep over every
+// combination measured on MI355X; the cost model above ranks these few percent off.
+struct TunedPlan {
+  int mt, ntiles, nchunks;
+  bool swiglu;
+  int nw, S;
+};
+static const TunedPlan kTuned[] = {
+    // 7B-shape bf16 (d 4096, 32 heads of 128, SwiGLU 11008, vocab 125696)
+    {4, 768, 128, false, 6, 2},   // Q|K|V, 64 rows (split: the fix-up pass applies rotary)
+    {4, 256, 128, false, 6, 4},   // O, 64 rows
+    {4, 256, 344, false, 8, 8},   // down, 64 rows
+    {4, 1376, 128, true, 6, 1},   // gate|up, 64 rows
+    {4, 7856, 128, false, 8, 1},  // LM head, 64 rows
+    {2, 7856, 128, false, 8, 1},  // LM head, 32 rows
+    {1, 7856, 128, false, 2, 1},  // LM head, 1-16 rows
+};
+
 GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int max_splits) {
   const int es = es_of(dtype), EPL = 16 / es, KC = 4 * EPL;
   GemmPlan best{};
@@ -318,6 +342,21 @@ GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int m
         best_cost = c;
         best = pl;
       }
+    }
+  }
+  if (dtype == 1) {
+    const int mt = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+    for (const TunedPlan& t : kTuned) {
+      if (t.mt != mt || t.ntiles != ntiles || t.nchunks != nchunks || t.swiglu != swiglu) continue;
+      if (t.S > std::max(1, std::min(max_splits, nchunks / (2 * STAGE_CHUNKS)))) continue;
+      const int cps = (nchunks + t.S - 1) / t.S;
+      if ((nchunks + cps - 1) / cps != t.S) continue;
+      best.nw = t.nw;
+      best.mt = mt;
+      best.mchunks = (std::max(M, 1) + 16 * mt - 1) / (16 * mt);
+      best.ngroups = swiglu ? ((ntiles / 2) + t.nw / 2 - 1) / (t.nw / 2) : (ntiles + t.nw - 1) / t.nw;
+      best.S = t.S;
+      best.cps = cps;
     }
   }
   const int mrows = 16 * best.mt;
@@ -369,6 +408,34 @@ hipError_t launch_gemm(int dtype, GemmParams& p, hipStream_t st, const LaunchTim
     return hipSuccess;
   }
   return dtype == 1 ? launch_gemm_t<bf16_t>(p, pl, st, lt) : launch_gemm_t<float>(p, pl, st, lt);
+}
+
+// Q|K|V finished from K-split partials part[s][m][pc] (packed column order), summed in split
+// order, then rotary and stores as in the fused epilogue.  One thread per (row, column).
+template <typename S>
+__global__ __launch_bounds__(256) void qkv_fix_kernel(const GemmParams p, const float* __restrict__ part, int S_, int N) {
+  const int pc = blockIdx.x * 256 + threadIdx.x, m = blockIdx.y;
+  if (pc >= N) return;
+  const int slot = p.row_slot[m];
+  const int kb = p.block_table[(size_t)p.row_seq[m] * p.max_blocks + (slot >> 4)] * 16 + (slot & 15);
+  float v = 0.f, w = 0.f;
+  for (int s = 0; s < S_; ++s) {
+    const float* r = part + ((size_t)s * p.M + m) * N;
+    v += r[pc];
+    w += r[pc ^ 8];
+  }
+  qkv_store<S>(p, m, pc, v, w, kb);
+}
+
+hipError_t launch_qkv_fix(int dtype, const GemmParams& p, const float* part, int S, hipStream_t st) {
+  const int N = (p.n_heads + 2 * p.n_kv) * p.hd;
+  if (p.M <= 0) return hipSuccess;
+  dim3 grid((N + 255) / 256, p.M);
+  if (dtype == 1)
+    hipLaunchKernelGGL(qkv_fix_kernel<bf16_t>, grid, dim3(256), 0, st, p, part, S, N);
+  else
+    hipLaunchKernelGGL(qkv_fix_kernel<float>, grid, dim3(256), 0, st, p, part, S, N);
+  return hipGetLastError();
 }
 
 // ---- packing ------------------------------------------------------------------------------

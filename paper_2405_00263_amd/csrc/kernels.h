@@ -54,6 +54,10 @@ struct GemmPlan {
 GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int max_splits);
 // Fills plan fields of p and launches; returns hipSuccess or an error.
 hipError_t launch_gemm(int dtype, GemmParams& p, hipStream_t st, const LaunchTiming* lt = nullptr);
+// Q|K|V from K-split partials part[S][M][N] (a GEMM in EP_PARTIAL mode over the packed Q|K|V
+// weights): sums in split order, rotary, Q to qbuf and K/V to the paged cache, exactly as the
+// EP_QKV epilogue.  p carries the EP_QKV fields.
+hipError_t launch_qkv_fix(int dtype, const GemmParams& p, const float* part, int S, hipStream_t st);
 // rope_hd > 0: a Q/K weight of heads rope_hd wide, packed so that each 16-row tile holds
 // 8 dims of a head's first rotary half and their 8 partners (tile-local rotary epilogue)
 hipError_t launch_pack(int dtype, const void* src, int rows, int cols, void* dst, int rope_hd,
