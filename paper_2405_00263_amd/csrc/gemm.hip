@@ -147,7 +147,13 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(const GemmParams p) {
   S* xs = reinterpret_cast<S*>(smem);
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int g = blockIdx.x, split = blockIdx.y, mc = blockIdx.z;
+  // Workgroup ids are dealt to the 8 XCDs round-robin.  The row chunks of one (group, split)
+  // take consecutive ids on one XCD, so they stream the same weight tiles at about the same
+  // time and all but the first find them in that XCD's L2 (one chunk: the identity map).
+  const int xcd = blockIdx.x & 7, q = blockIdx.x >> 3;
+  const int mc = q % p.mchunks, r = (q / p.mchunks) * 8 + xcd;
+  if (r >= p.ngroups * p.S) return;  // padding of the last round
+  const int g = r % p.ngroups, split = r / p.ngroups;
   const int m0 = mc * MROWS;
   const int c0 = split * p.cps;
   const int c1 = min(p.nchunks, c0 + p.cps);
@@ -369,7 +375,7 @@ GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int m
 
 template <typename S, int MT>
 static void launch_nw(const GemmPlan& pl, GemmParams& p, hipStream_t st, const LaunchTiming* lt) {
-  dim3 grid(pl.ngroups, pl.S, pl.mchunks), block(pl.nw * 64);
+  dim3 grid(8 * ((pl.ngroups * pl.S + 7) / 8) * pl.mchunks), block(pl.nw * 64);
   auto go = [&](auto kern) {
     if (lt) hipExtLaunchKernelGGL(kern, grid, block, (uint32_t)pl.lds_bytes, st, lt->start, lt->stop, 0, p);
     else hipLaunchKernelGGL(kern, grid, block, pl.lds_bytes, st, p);
