@@ -142,6 +142,10 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-kernel-timing", action="store_true",
                     help="skip the second, per-launch timed pass (no roofline figure)")
+    ap.add_argument("--prompt-len", type=int, default=0,
+                    help="override the prompt length (context sweep cells)")
+    ap.add_argument("--tree-tokens", type=int, default=0, help="override T (tree tokens, root included)")
+    ap.add_argument("--topk", default="", help="override the per-depth top-k, e.g. 16,4,2")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "
@@ -154,6 +158,15 @@ def main():
     import paper_2405_00263_amd as P
 
     cfg = synth.get_config(args.workload)
+    over = {}
+    if args.prompt_len:
+        over["prompt_len"] = (args.prompt_len, args.prompt_len)
+    if args.tree_tokens:
+        over["tree_tokens"] = args.tree_tokens
+    if args.topk:
+        over["topk"] = tuple(int(v) for v in args.topk.split(","))
+    if over:
+        cfg = cfg.with_(**over)
     torch.cuda.set_device(0)
     lens = _prompt_lengths(cfg)
     H1 = cfg.n_spec_heads + 1
