@@ -13,7 +13,7 @@ SRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libclover.so")
 BUILD = os.path.join(HERE, "_build")
 ARCH = "gfx950"
-SOURCES = ["gemm.hip", "attention.hip", "rows.hip", "tree.hip", "api.cpp"]
+SOURCES = ["gemm.hip", "gemm_tiled.hip", "attention.hip", "rows.hip", "tree.hip", "api.cpp"]
 CFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           # packed fp32 instructions stay off (see the project notes on gfx950 correctness)
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

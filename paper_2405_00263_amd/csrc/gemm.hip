@@ -26,6 +26,7 @@
 //    needed inside the GEMM;
 //  * fused epilogues (rotary + KV append, SwiGLU) run unsplit on an LDS tile.
 #include "common.h"
+#include "gemm_epi.h"
 #include "kernels.h"
 
 #include <hip/hip_ext.h>
@@ -39,13 +40,6 @@ static constexpr int STAGE_CHUNKS = 4;   // chunks of X per LDS stage
 static constexpr int PF = 16;            // weight fragments in flight per wave (16 KB)
 static constexpr int RING = PF / STAGE_CHUNKS;  // stages covered by the prefetch ring
 static_assert(RING % 2 == 0, "stages alternate between two LDS buffers inside a superstage");
-
-// source row of row r of physical tile t in a Q/K weight packed with tile-local rotary
-// pairs: rows 0..7 are dims q*8.. of the first half of a head, rows 8..15 their partners
-__host__ __device__ __forceinline__ int rope_row(int t, int r, int hd) {
-  const int tph = hd / 16, h = t / tph, q = t % tph;
-  return h * hd + (r < 8 ? q * 8 + r : hd / 2 + q * 8 + (r - 8));
-}
 
 template <int NW>
 __device__ __forceinline__ const u32x4_t* wave_weight_ptr(const GemmParams& p, int g, int wave,
@@ -66,44 +60,6 @@ __device__ __forceinline__ const u32x4_t* wave_weight_ptr(const GemmParams& p, i
   }
   if (!active) return nullptr;
   return reinterpret_cast<const u32x4_t*>(p.seg[seg].w) + (size_t)t * p.nchunks * 64;
-}
-
-// Finishes one value of the packed Q|K|V output: physical column pc (tile-local rotary
-// order), row m.  v and its rotary partner (physical column pc ^ 8) are the complete sums;
-// kb = physical KV block * 16 + key slot of row m.  Q/K get the rotary factors of row m's
-// position (rope_cs), Q goes to qbuf, K/V to the paged cache.
-template <typename S>
-__device__ __forceinline__ void qkv_store(const GemmParams& p, int m, int pc, float v, float partner, int kb) {
-  using T = St<S>;
-  const int hd = p.hd, half = hd >> 1, qd = p.n_heads * hd, kvd = p.n_kv * hd;
-  const int pt = pc >> 4, jj = pc & 15;
-  const int qt = qd / 16, kt = kvd / 16;
-  const bool rot = pt < qt + kt;
-  int n;  // logical output column
-  if (rot) {
-    const int seg0 = pt < qt ? 0 : qt;
-    n = seg0 * 16 + rope_row(pt - seg0, jj, hd);
-  } else {
-    n = pc;
-  }
-  const int d = n % hd;
-  if (rot) {
-    const int dlo = (d < half) ? d : d - half;  // rotary frequency index
-    const float2 cs = reinterpret_cast<const float2*>(p.rope_cs)[(size_t)m * half + dlo];
-    v = (jj < 8) ? (v * cs.x - partner * cs.y) : (v * cs.x + partner * cs.y);
-  }
-  if (n < qd) {
-    reinterpret_cast<S*>(p.qbuf)[(size_t)m * p.ldq + n] = T::from_f(v);
-  } else {
-    const bool isk = n < qd + kvd;
-    const int kvh = (isk ? n - qd : n - qd - kvd) / hd;
-    const size_t base = ((size_t)(kb >> 4) * p.n_kv + kvh) * (size_t)(16 * hd);
-    const int key = kb & 15;
-    if (isk)
-      reinterpret_cast<S*>(p.kcache)[base + kblk_off(key, d, T::EPL)] = T::from_f(v);
-    else
-      reinterpret_cast<S*>(p.vcache)[base + vblk_off(key, d)] = T::from_f(v);
-  }
 }
 
 template <typename S, int NW>
@@ -325,7 +281,12 @@ static const TunedPlan kTuned[] = {
     {1, 7856, 128, false, 2, 1},  // LM head, 1-16 rows
 };
 
+// From this many rows on, bf16 GEMMs use the register-blocked kernel (gemm_tiled.hip).
+static constexpr int TILED_MIN_M = 128;
+
 GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int max_splits) {
+  if (dtype == 1 && (M >= TILED_MIN_M || tiled_has_tuned(M, ntiles, nchunks, swiglu, max_splits)))
+    return plan_tiled(M, ntiles, nchunks, swiglu, max_splits);
   const int es = es_of(dtype), EPL = 16 / es, KC = 4 * EPL;
   GemmPlan best{};
   double best_cost = 1e30;
@@ -413,6 +374,7 @@ hipError_t launch_gemm(int dtype, GemmParams& p, hipStream_t st, const LaunchTim
     }
     return hipSuccess;
   }
+  if (pl.tiled) return launch_tiled(p, pl, st, lt);
   return dtype == 1 ? launch_gemm_t<bf16_t>(p, pl, st, lt) : launch_gemm_t<float>(p, pl, st, lt);
 }
 

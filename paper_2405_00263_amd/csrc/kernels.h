@@ -44,14 +44,24 @@ struct GemmParams {
 };
 
 struct GemmPlan {
-  int nw;        // waves per workgroup, one 16-row weight tile each (2, 3, 4, 6 or 8)
-  int mt;        // m-tiles of 16 rows per chunk (1, 2 or 4)
+  int tiled;     // 0: weight-streaming kernel; 1: register-blocked kernel (bf16, large M)
+  int nw;        // waves per workgroup (streaming: one 16-row weight tile each, 2..8; tiled: 4 or 8)
+  int mt;        // m-tiles of 16 rows per chunk (streaming 1, 2 or 4) or per wave (tiled, 4)
+  int tw;        // tiled: 16-row weight tiles per wave
+  int ring;      // tiled: register prefetch depth in LDS stages
   int mchunks, ngroups, S, cps;
   size_t lds_bytes;
   size_t part_floats;
 };
 
 GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int max_splits);
+// Plan and launch of the register-blocked kernel (plan_gemm picks it for large M and for
+// the swept shapes where it beats the streaming kernel).
+GemmPlan plan_tiled(int M, int ntiles, int nchunks, bool swiglu, int max_splits);
+bool tiled_has_tuned(int M, int ntiles, int nchunks, bool swiglu, int max_splits);
+// a plan of one instantiated shape (mt, tw, ring, nw waves) and split, for sweeps
+GemmPlan plan_tiled_forced(int M, int ntiles, int nchunks, bool swiglu, int mt, int tw, int ring, int nw, int S);
+hipError_t launch_tiled(GemmParams& p, const GemmPlan& pl, hipStream_t st, const LaunchTiming* lt);
 // Fills plan fields of p and launches; returns hipSuccess or an error.
 hipError_t launch_gemm(int dtype, GemmParams& p, hipStream_t st, const LaunchTiming* lt = nullptr);
 // Q|K|V from K-split partials part[S][M][N] (a GEMM in EP_PARTIAL mode over the packed Q|K|V
