@@ -57,6 +57,23 @@ __device__ __forceinline__ f32x4_t mma_pv(u32x4_t v, u32x2_t, const float p[4], 
   return c;
 }
 
+// Reductions over the four lanes that hold one query row's keys (lanes j, j+16, j+32,
+// j+48): VALU lane swaps (upper/lower 32 lanes, then odd/even 16-lane rows) instead of
+// LDS-routed shuffles.  Every lane of the row ends with the same value, summed in the
+// same order.
+__device__ __forceinline__ float row4_max(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float row4_sum(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 template <typename S> struct VFrag;
 template <> struct VFrag<bf16_t> { typedef u32x2_t type; };
 template <> struct VFrag<float> { typedef u32x4_t type; };
@@ -176,26 +193,26 @@ __global__ __launch_bounds__(AT_THREADS) void attn_kernel(const AttnParams p) {
   // running max m_i is kept in raw score units; the scale folds into one multiply-add
   // per exponent.  Groups wholly inside the committed prefix skip the mask logic.
   constexpr int NG = 4;
+  static_assert(CB - 1 + 2 * (NG - 1) < 2 * CB, "score reads of a group stay inside the chunk buffer");
   using VT = typename VFrag<S>::type;
   // tail rule as data, so the score loop has no branch on the mode: causal rows see tail
   // keys up to their own index, tree rows the keys whose mask bit is set
   const bool causal_mode = p.causal != 0;
   const int tail_lim = causal_mode ? row : 0x7fffffff;
   auto consume = [&](int cb0, int kb0g, int nblk) {
+    // All NG score products are computed (four independent matrix-core chains, no branch
+    // between them); blocks past nblk read LDS inside the chunk buffer and are masked below.
     f32x4_t s[NG];
 #pragma unroll
     for (int i = 0; i < NG; ++i) {
-      s[i] = f32x4_t{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-      if (i < nblk) {
-        const u32x4_t* kblk = lds + (cb0 + 2 * i) * BVEC;
-        f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      const u32x4_t* kblk = lds + (cb0 + 2 * i) * BVEC;
+      f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int c = 0; c < NQC; ++c) acc = mma_frag(kblk[c * 64 + lane], qf[c], acc, S{});
-        s[i] = acc;
-      }
+      for (int c = 0; c < NQC; ++c) acc = mma_frag(kblk[c * 64 + lane], qf[c], acc, S{});
+      s[i] = acc;
     }
     // s[i][r] = score of key (kb0g + 2i)*16 + 4g + r for query row j
-    const bool plain = (kb0g + 2 * (nblk - 1)) * 16 + 15 < P;  // all keys committed
+    const bool plain = nblk == NG && (kb0g + 2 * (NG - 1)) * 16 + 15 < P;  // all keys committed
     if (!plain) {
 #pragma unroll
       for (int i = 0; i < NG; ++i)
@@ -205,15 +222,14 @@ __global__ __launch_bounds__(AT_THREADS) void attn_kernel(const AttnParams p) {
           const int tk = key - P;
           const uint64_t word = tk < 64 ? mw0 : mw1;
           const bool tree_ok = causal_mode | (((word >> (tk & 63)) & 1ull) != 0);
-          const bool vis = valid & (key < nkeys) & ((tk < 0) | (tree_ok & (tk <= tail_lim)));
+          const bool vis = valid & (i < nblk) & (key < nkeys) & ((tk < 0) | (tree_ok & (tk <= tail_lim)));
           s[i][r] = vis ? s[i][r] : -INFINITY;
         }
     }
     float mloc = -INFINITY;
 #pragma unroll
     for (int i = 0; i < NG; ++i) mloc = fmaxf(mloc, fmaxf(fmaxf(s[i][0], s[i][1]), fmaxf(s[i][2], s[i][3])));
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+    mloc = row4_max(mloc);
     const float m_new = fmaxf(m_i, mloc);
     // every exponent below is <= 0; exp2(-inf) = 0 removes masked keys
     const float nm = (m_new == -INFINITY) ? 0.f : -m_new * scale2;
@@ -230,8 +246,7 @@ __global__ __launch_bounds__(AT_THREADS) void attn_kernel(const AttnParams p) {
       }
       pb[i] = pack_p(pr[i], S{});
     }
-    lsum += __shfl_xor(lsum, 16);
-    lsum += __shfl_xor(lsum, 32);
+    lsum = row4_sum(lsum);
     l_i = l_i * alpha + lsum;
     m_i = m_new;
     if (!__all(alpha == 1.f)) {
