@@ -257,7 +257,7 @@ def main():
             "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4) if mfma_bound else round(achieved / HBM_PEAK_GBS, 4),
             "traffic": measured_traffic(cfg.name),
             "kernel": ("verify-forward GEMMs (register-blocked tiled_kernel)" if mfma_bound
-                       else "verify-forward GEMMs (streaming gemm_kernel; tiled_kernel for the swept O and down shapes)"),
+                       else "verify-forward GEMMs (streaming gemm_kernel)"),
             "weight_stream_GBps": round(achieved, 1),
             "timed_steps": kt_steps,
             "launches": g["launches"],

@@ -285,8 +285,7 @@ static const TunedPlan kTuned[] = {
 static constexpr int TILED_MIN_M = 128;
 
 GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int max_splits) {
-  if (dtype == 1 && (M >= TILED_MIN_M || tiled_has_tuned(M, ntiles, nchunks, swiglu, max_splits)))
-    return plan_tiled(M, ntiles, nchunks, swiglu, max_splits);
+  if (dtype == 1 && M >= TILED_MIN_M) return plan_tiled(M, ntiles, nchunks, swiglu, max_splits);
   const int es = es_of(dtype), EPL = 16 / es, KC = 4 * EPL;
   GemmPlan best{};
   double best_cost = 1e30;

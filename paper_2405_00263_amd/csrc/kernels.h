@@ -55,10 +55,8 @@ struct GemmPlan {
 };
 
 GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int max_splits);
-// Plan and launch of the register-blocked kernel (plan_gemm picks it for large M and for
-// the swept shapes where it beats the streaming kernel).
+// Plan and launch of the register-blocked kernel (plan_gemm picks it for bf16 and large M).
 GemmPlan plan_tiled(int M, int ntiles, int nchunks, bool swiglu, int max_splits);
-bool tiled_has_tuned(int M, int ntiles, int nchunks, bool swiglu, int max_splits);
 // a plan of one instantiated shape (mt, tw, ring, nw waves) and split, for sweeps
 GemmPlan plan_tiled_forced(int M, int ntiles, int nchunks, bool swiglu, int mt, int tw, int ring, int nw, int S);
 hipError_t launch_tiled(GemmParams& p, const GemmPlan& pl, hipStream_t st, const LaunchTiming* lt);
