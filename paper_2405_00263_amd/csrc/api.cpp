@@ -148,7 +148,7 @@ struct Layout {
   size_t tree_token, tree_parent, tree_depth, tree_pos, tree_mask, target, acc, acc_len, out_tokens;
   size_t dstate[CLOVER_MAX_HEADS], dlogits[CLOVER_MAX_HEADS];
   size_t d_hin, d_a, d_e, d_q, d_kv, d_o, d_sst, d_r, d_rn;
-  size_t gpart, gpart2, amax_keys, topk_scratch;
+  size_t gpart, gpart2, amax_part, topk_scratch;
   size_t apart, apart_floats;  // attention split partials
   size_t gpart_floats, gpart2_floats;
   size_t total;
@@ -237,7 +237,9 @@ Layout make_layout(const clover_config& c) {
   L.gpart2_floats = (size_t)GEMM_MAX_SPLITS * L.Fmaxrows * 2 * qd;  // Attention Decoder keys/values
   L.gpart = take(4 * L.gpart_floats);
   L.gpart2 = take(4 * L.gpart2_floats);
-  L.amax_keys = take(8 * (size_t)L.Mv);
+  // per-(column group, row) argmax keys of the LM-head epilogue: a group holds at least
+  // two 16-column tiles in every plan
+  L.amax_part = take(8 * ((size_t)V / 32 + 1) * (size_t)L.Mv);
   L.topk_scratch = take(4 * topk_scratch_floats(L.Fmaxrows, (int)V, 16));
   // attention split partials: the largest of the verify launches (every batch size) and
   // the prefill chunks (every chunk length)
@@ -372,7 +374,8 @@ void prof_collect(clover_ctx* c) {  // after a stream sync
 // Y = X W^T through the streaming GEMM.  EP_PARTIAL writes [S][M][N] fp32 partials to
 // `part` (S <= max_splits; the consumer sums them) and returns S through *splits.
 hipError_t run_gemm(clover_ctx* c, GemmParams p, int M, int K,
-                    std::initializer_list<std::pair<const void*, int>> segs, int* splits = nullptr) {
+                    std::initializer_list<std::pair<const void*, int>> segs, int* splits = nullptr,
+                    int* groups = nullptr) {
   p.M = M;
   p.K = K;
   p.nchunks = K / kc_of(c->cfg.dtype);
@@ -392,6 +395,7 @@ hipError_t run_gemm(clover_ctx* c, GemmParams p, int M, int K,
     e = launch_gemm(c->cfg.dtype, p, c->st, ps.timing());
   }
   if (splits) *splits = p.S;
+  if (groups) *groups = p.ngroups;
   return e;
 }
 
@@ -518,16 +522,17 @@ hipError_t enq_verify(clover_ctx* c, int B, int max_keys) {
   rf.M = M; rf.d = d; rf.part = c->at<float>(L.gpart); rf.S = pend; rf.ldp = d;
   rf.resid = x; rf.ldr = d; rf.out_f = x; rf.ldo = d; rf.out_copy_f = xa;
   rf.gain = c->final_norm; rf.eps = cf.rms_eps; rf.out_norm = c->at<void>(L.xn); rf.ldn = d;
-  rf.zero_keys = c->at<unsigned long long>(L.amax_keys); rf.zero_n = M;
   HE(run_rowfix(c, rf));
+  // LM head; its epilogue leaves per-(column group, row) argmax keys, reduced per row
   GemmParams lm{};
   lm.X = c->at<void>(L.xn); lm.ldx = d; lm.mode = EP_PARTIAL; lm.max_splits = 1;
   lm.part = c->at<float>(L.vlogits);
-  HE(run_gemm(c, lm, M, d, {{c->lm_head, cf.vocab}}));
+  lm.amax_part = c->at<unsigned long long>(L.amax_part);
+  int lm_groups = 0;
+  HE(run_gemm(c, lm, M, d, {{c->lm_head, cf.vocab}}, nullptr, &lm_groups));
   {
     ProfScope ps(c, CLOVER_KSTAT_OTHER, 0, 0);
-    HE(launch_argmax(c->at<float>(L.vlogits), M, cf.vocab, c->at<int>(L.target),
-                     c->at<unsigned long long>(L.amax_keys), true, c->st));
+    HE(launch_argmax_groups(c->at<unsigned long long>(L.amax_part), lm_groups, M, c->at<int>(L.target), c->st));
   }
   // Augmenting Block over the tree (tree mask, its own KV cache)
   HE(run_layer(c, c->layers[cf.n_layers], cf.n_layers, xa, M, att, max_keys, 0, &pend));
@@ -979,15 +984,15 @@ clover_status clover_prefill(clover_ctx* c, int32_t seq, const int32_t* tokens, 
     rf.M = rows; rf.d = d; rf.part = c->at<float>(L.gpart); rf.S = pend; rf.ldp = d;
     rf.resid = x; rf.ldr = d; rf.out_f = x; rf.ldo = d; rf.out_copy_f = xa;
     rf.gain = c->final_norm; rf.eps = cf.rms_eps; rf.out_norm = c->at<void>(L.xn); rf.ldn = d;
-    rf.zero_keys = c->at<unsigned long long>(L.amax_keys); rf.zero_n = 1;
     HIPCK(c, run_rowfix(c, rf));
     if (c0 + rows == n) {
       GemmParams lm{};
       lm.X = (const char*)c->at<char>(L.xn) + (size_t)(rows - 1) * d * L.es; lm.ldx = d;
       lm.mode = EP_PARTIAL; lm.max_splits = 1; lm.part = c->at<float>(L.vlogits);
-      HIPCK(c, run_gemm(c, lm, 1, d, {{c->lm_head, cf.vocab}}));
-      HIPCK(c, launch_argmax(c->at<float>(L.vlogits), 1, cf.vocab, c->at<int>(L.amax),
-                             c->at<unsigned long long>(L.amax_keys), true, c->st));
+      lm.amax_part = c->at<unsigned long long>(L.amax_part);
+      int lm_groups = 0;
+      HIPCK(c, run_gemm(c, lm, 1, d, {{c->lm_head, cf.vocab}}, nullptr, &lm_groups));
+      HIPCK(c, launch_argmax_groups(c->at<unsigned long long>(L.amax_part), lm_groups, 1, c->at<int>(L.amax), c->st));
     }
     HIPCK(c, run_layer(c, c->layers[cf.n_layers], cf.n_layers, xa, rows, att, c0 + rows, 0, &pend));
     RowFixParams ra{};

@@ -52,6 +52,53 @@ __device__ __forceinline__ f32x4_t mma_frag(u32x4_t a, u32x4_t b, f32x4_t c, flo
   return c;
 }
 
+// ---- argmax keys ---------------------------------------------------------------------
+// Every element maps to a 64-bit key whose order is (value ascending, index descending):
+// the maximum key is the largest value with the lowest index (ties resolve to the lowest
+// index), so partial maxima combine exactly and in any order.
+__device__ __forceinline__ unsigned long long amax_key(float v, int i) {
+  uint32_t u = __float_as_uint(v + 0.0f);  // -0 -> +0: equal values tie on the index
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((unsigned long long)u << 32) | (uint32_t)(0x7fffffff - i);
+}
+__device__ __forceinline__ unsigned long long umax64(unsigned long long a, unsigned long long b) {
+  return a > b ? a : b;
+}
+// Reductions over the 16 lanes of a matrix-core row group by DPP row rotations (VALU
+// only); every lane of the group ends with the result.
+template <int ROR>
+__device__ __forceinline__ int dpp_row_ror(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, 0x120 + ROR, 0xf, 0xf, false);
+}
+__device__ __forceinline__ float row16_max(float x) {
+  x = fmaxf(x, __int_as_float(dpp_row_ror<8>(__float_as_int(x))));
+  x = fmaxf(x, __int_as_float(dpp_row_ror<4>(__float_as_int(x))));
+  x = fmaxf(x, __int_as_float(dpp_row_ror<2>(__float_as_int(x))));
+  return fmaxf(x, __int_as_float(dpp_row_ror<1>(__float_as_int(x))));
+}
+__device__ __forceinline__ int row16_min(int x) {
+  x = min(x, dpp_row_ror<8>(x));
+  x = min(x, dpp_row_ror<4>(x));
+  x = min(x, dpp_row_ror<2>(x));
+  return min(x, dpp_row_ror<1>(x));
+}
+// argmax key of a row group's best element: v and column n of this lane (n = INT_MAX and
+// v = -inf for lanes without a column); ties take the lowest column
+__device__ __forceinline__ unsigned long long row16_amax_key(float v, int n) {
+  const float mx = row16_max(v);
+  return amax_key(mx, row16_min(v == mx ? n : 0x7fffffff));
+}
+__device__ __forceinline__ unsigned long long shfl_xor_u64(unsigned long long v, int o) {
+  const unsigned lo = __shfl_xor((unsigned)(v & 0xffffffffu), o), hi = __shfl_xor((unsigned)(v >> 32), o);
+  return ((unsigned long long)hi << 32) | lo;
+}
+// max over the 16 lanes of a matrix-core row group (lanes sharing l / 16)
+__device__ __forceinline__ unsigned long long max16_u64(unsigned long long k) {
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) k = umax64(k, shfl_xor_u64(k, o));
+  return k;
+}
+
 // ---- packed weight layout ----------------------------------------------------------
 // W[N][K] row-major is stored as fragments (tile t = n/16, chunk c = k/KC) of 64 lanes
 // x EPL elements; lane = n%16 + 16 * ((k%KC)/EPL), element = k%EPL.

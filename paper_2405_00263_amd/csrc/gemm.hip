@@ -90,7 +90,9 @@ __device__ void gemm_epilogue(const GemmParams& p, const float* tile, int g, int
   }
 }
 
-template <typename S, int MT, int NW>
+// AMAX: the EP_PARTIAL epilogue also leaves per-(group, row) argmax keys in p.amax_part
+// (a separate instantiation, so the other GEMMs keep their code unchanged)
+template <typename S, int MT, int NW, bool AMAX>
 __global__ __launch_bounds__(NW * 64) void gemm_kernel(const GemmParams p) {
   using T = St<S>;
   constexpr int THREADS = NW * 64, COLS = NW * 16, TSTRIDE = COLS + 4;
@@ -219,16 +221,37 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(const GemmParams p) {
 
   if (p.mode == EP_PARTIAL) {
     // split `split` writes rows m0.. of its own [M][N] fp32 slice
-    if (!active) return;
+    if (!AMAX && !active) return;
     const int n = (g * NW + wave) * 16 + (lane & 15);  // segments are contiguous in N
-    float* out = p.part + (size_t)split * p.M * p.N;
+    if (active) {
+      float* out = p.part + (size_t)split * p.M * p.N;
 #pragma unroll
-    for (int t = 0; t < MT; ++t)
+      for (int t = 0; t < MT; ++t)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = m0 + t * 16 + 4 * (lane >> 4) + r;
-        if (m < p.M) out[(size_t)m * p.N + n] = acc[t][r];
+        for (int r = 0; r < 4; ++r) {
+          const int m = m0 + t * 16 + 4 * (lane >> 4) + r;
+          if (m < p.M) out[(size_t)m * p.N + n] = acc[t][r];
+        }
+    }
+    if constexpr (AMAX) {
+      // each row's best (value, column) over this group's columns: lanes, then waves
+      unsigned long long* s_key = reinterpret_cast<unsigned long long*>(smem);  // [NW][MROWS]
+#pragma unroll
+      for (int t = 0; t < MT; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const unsigned long long k =
+              row16_amax_key(active ? acc[t][r] : -INFINITY, active ? n : 0x7fffffff);
+          if ((lane & 15) == 0) s_key[wave * MROWS + t * 16 + 4 * (lane >> 4) + r] = k;
+        }
+      __syncthreads();
+      for (int i = threadIdx.x; i < MROWS; i += THREADS) {
+        if (m0 + i >= p.M) break;
+        unsigned long long best = 0ull;
+        for (int w = 0; w < NW; ++w) best = umax64(best, s_key[w * MROWS + i]);
+        p.amax_part[(size_t)g * p.M + m0 + i] = best;
       }
+    }
     return;
   }
   const int col = wave * 16 + (lane & 15);
@@ -333,7 +356,7 @@ GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int m
   return best;
 }
 
-template <typename S, int MT>
+template <typename S, int MT, bool AMAX>
 static void launch_nw(const GemmPlan& pl, GemmParams& p, hipStream_t st, const LaunchTiming* lt) {
   dim3 grid(8 * ((pl.ngroups * pl.S + 7) / 8) * pl.mchunks), block(pl.nw * 64);
   auto go = [&](auto kern) {
@@ -341,26 +364,34 @@ static void launch_nw(const GemmPlan& pl, GemmParams& p, hipStream_t st, const L
     else hipLaunchKernelGGL(kern, grid, block, pl.lds_bytes, st, p);
   };
   switch (pl.nw) {
-    case 2: go(gemm_kernel<S, MT, 2>); break;
-    case 3: go(gemm_kernel<S, MT, 3>); break;
-    case 6: go(gemm_kernel<S, MT, 6>); break;
-    case 8: go(gemm_kernel<S, MT, 8>); break;
-    default: go(gemm_kernel<S, MT, 4>); break;
+    case 2: go(gemm_kernel<S, MT, 2, AMAX>); break;
+    case 3: go(gemm_kernel<S, MT, 3, AMAX>); break;
+    case 6: go(gemm_kernel<S, MT, 6, AMAX>); break;
+    case 8: go(gemm_kernel<S, MT, 8, AMAX>); break;
+    default: go(gemm_kernel<S, MT, 4, AMAX>); break;
   }
 }
 
 template <typename S>
 static hipError_t launch_gemm_t(GemmParams& p, const GemmPlan& pl, hipStream_t st, const LaunchTiming* lt) {
-  switch (pl.mt) {
-    case 1: launch_nw<S, 1>(pl, p, st, lt); break;
-    case 2: launch_nw<S, 2>(pl, p, st, lt); break;
-    default: launch_nw<S, 4>(pl, p, st, lt); break;
+  if (p.amax_part) {
+    switch (pl.mt) {
+      case 1: launch_nw<S, 1, true>(pl, p, st, lt); break;
+      case 2: launch_nw<S, 2, true>(pl, p, st, lt); break;
+      default: launch_nw<S, 4, true>(pl, p, st, lt); break;
+    }
+  } else {
+    switch (pl.mt) {
+      case 1: launch_nw<S, 1, false>(pl, p, st, lt); break;
+      case 2: launch_nw<S, 2, false>(pl, p, st, lt); break;
+      default: launch_nw<S, 4, false>(pl, p, st, lt); break;
+    }
   }
   return hipGetLastError();
 }
 
 hipError_t launch_gemm(int dtype, GemmParams& p, hipStream_t st, const LaunchTiming* lt) {
-  const int maxs = p.mode == EP_PARTIAL ? std::max(1, p.max_splits) : 1;
+  const int maxs = p.mode == EP_PARTIAL && !p.amax_part ? std::max(1, p.max_splits) : 1;
   const GemmPlan pl = plan_gemm(dtype, p.M, p.ntiles, p.nchunks, p.mode == EP_SWIGLU, maxs);
   p.ngroups = pl.ngroups;
   p.mchunks = pl.mchunks;

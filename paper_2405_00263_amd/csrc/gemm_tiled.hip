@@ -32,7 +32,7 @@ namespace clover {
 static constexpr int TWAVES = 4;  // waves per row of waves (column groups per workgroup)
 static constexpr int TSC = 2;     // 32-wide k chunks per LDS stage
 
-template <int MT, int TW, int RING, int WR>
+template <int MT, int TW, int RING, int WR, bool AMAX>
 __global__ __launch_bounds__(WR * TWAVES * 64) void tiled_kernel(const GemmParams p) {
   using S = bf16_t;
   using T = St<S>;
@@ -195,6 +195,34 @@ __global__ __launch_bounds__(WR * TWAVES * 64) void tiled_kernel(const GemmParam
           if (m < p.M) out[(size_t)m * p.N + n] = acc[t][j][i];
         }
     }
+    if constexpr (AMAX) {
+      // each row's best (value, column) over this group's columns: tiles, lanes, waves
+      __syncthreads();  // the LDS stages are no longer read
+      unsigned long long* s_key = reinterpret_cast<unsigned long long*>(smem);  // [TWAVES][BM]
+#pragma unroll
+      for (int t = 0; t < MT; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          // this lane's best over its tiles (tiles ascend in column: strict > keeps the lowest)
+          float v = -INFINITY;
+          int n = 0x7fffffff;
+#pragma unroll
+          for (int j = 0; j < TW; ++j)
+            if (act[j] && acc[t][j][i] > v) {
+              v = acc[t][j][i];
+              n = otile[j] * 16 + ccol;
+            }
+          const unsigned long long k = row16_amax_key(v, n);
+          if (ccol == 0) s_key[wave * BM + wrow * WM + t * 16 + 4 * (lane >> 4) + i] = k;
+        }
+      __syncthreads();
+      for (int r = threadIdx.x; r < BM; r += THREADS) {
+        if (m0 + r >= p.M) break;
+        unsigned long long best = 0ull;
+        for (int w = 0; w < TWAVES; ++w) best = umax64(best, s_key[w * BM + r]);
+        p.amax_part[(size_t)g * p.M + m0 + r] = best;
+      }
+    }
   } else if (p.mode == EP_SWIGLU) {
     S* out = reinterpret_cast<S*>(p.out_s);
 #pragma unroll
@@ -279,7 +307,7 @@ GemmPlan make_plan(const TiledShape& sh, int M, int ntiles, int nchunks, bool sw
                       : (ntiles + TWAVES * sh.tw - 1) / (TWAVES * sh.tw);
   pl.cps = (nchunks + S - 1) / S;
   pl.S = (nchunks + pl.cps - 1) / pl.cps;
-  pl.lds_bytes = 2ull * bm * (TSC * 32 + 8) * 2;
+  pl.lds_bytes = std::max<size_t>(2ull * bm * (TSC * 32 + 8) * 2, 8ull * TWAVES * bm);  // X stages; argmax keys
   pl.part_floats = (size_t)pl.S * M * ntiles * 16;
   return pl;
 }
@@ -312,7 +340,7 @@ GemmPlan plan_tiled_forced(int M, int ntiles, int nchunks, bool swiglu, int mt, 
 
 template <int MT, int TW, int RING, int WR>
 static void launch_shape(const GemmPlan& pl, GemmParams& p, hipStream_t st, const LaunchTiming* lt) {
-  auto kern = tiled_kernel<MT, TW, RING, WR>;
+  auto kern = p.amax_part ? tiled_kernel<MT, TW, RING, WR, true> : tiled_kernel<MT, TW, RING, WR, false>;
   dim3 grid(8 * ((pl.ngroups * pl.S + 7) / 8) * pl.mchunks), block(WR * TWAVES * 64);
   if (lt) hipExtLaunchKernelGGL(kern, grid, block, (uint32_t)pl.lds_bytes, st, lt->start, lt->stop, 0, p);
   else hipLaunchKernelGGL(kern, grid, block, pl.lds_bytes, st, p);

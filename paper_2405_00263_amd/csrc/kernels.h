@@ -32,6 +32,9 @@ struct GemmParams {
   int ngroups, mchunks, S, cps;
   int max_splits;  // EP_PARTIAL: upper bound on K splits (1 = unsplit)
   float* part;     // EP_PARTIAL output [S][M][N]
+  // EP_PARTIAL with one split: optional per-(column group, row) argmax keys [ngroups][M]
+  // of the output (amax_key order), reduced by launch_argmax_groups; null: off
+  unsigned long long* amax_part;
   int mode;
   void* out_s; int ldos;
   // EP_QKV
@@ -110,6 +113,9 @@ hipError_t launch_embed(int dtype, const void* emb, const int* tok, int M, int d
                         hipStream_t st);
 // cs[m][i] = (cos, sin)(pos[m] * theta^(-2i/hd)), i < hd/2: the rotary factors of each row
 hipError_t launch_rope_table(const int* pos, int M, int hd, float theta, float* cs, hipStream_t st);
+// out[m] = argmax of row m from the keys[G][M] a GEMM left in GemmParams::amax_part (G =
+// its plan's ngroups)
+hipError_t launch_argmax_groups(const unsigned long long* keys, int G, int M, int* out, hipStream_t st);
 // keys: M u64 scratch; keys_zeroed: a previous kernel already cleared them
 hipError_t launch_argmax(const float* logits, int M, int V, int* out, unsigned long long* keys,
                          bool keys_zeroed, hipStream_t st);

@@ -97,20 +97,10 @@ __device__ __forceinline__ float block_sum256(float v, float* red) {
 }
 
 // ---- argmax (lowest index on ties) ---------------------------------------------------------
-// Every element maps to a 64-bit key whose order is (value ascending, index descending):
-// the maximum key is the largest value with the lowest index.  Chunks of a row reduce
-// to one key each and combine with a 64-bit atomic max, which is exact and
-// order-independent, so the result is deterministic.
+// Chunks of a row reduce to one key each (amax_key) and combine with a 64-bit atomic
+// max, which is exact and order-independent, so the result is deterministic.
 __device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
   return va > vb || (va == vb && ia < ib);
-}
-__device__ __forceinline__ unsigned long long amax_key(float v, int i) {
-  uint32_t u = __float_as_uint(v);
-  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-  return ((unsigned long long)u << 32) | (uint32_t)(0x7fffffff - i);
-}
-__device__ __forceinline__ unsigned long long umax64(unsigned long long a, unsigned long long b) {
-  return a > b ? a : b;
 }
 
 static constexpr int RED_THREADS = 256;
@@ -148,6 +138,31 @@ __global__ __launch_bounds__(RED_THREADS) void argmax_kernel(const float* __rest
 __global__ void argmax_finish_kernel(const unsigned long long* __restrict__ keys, int M, int* __restrict__ out) {
   const int m = blockIdx.x * blockDim.x + threadIdx.x;
   if (m < M) out[m] = 0x7fffffff - (int)(keys[m] & 0xffffffffu);
+}
+
+// Row m's argmax from the per-(group, row) keys a GEMM's epilogue left in keys[G][M].
+__global__ __launch_bounds__(RED_THREADS) void argmax_groups_kernel(const unsigned long long* __restrict__ keys, int G,
+                                                                    int M, int* __restrict__ out) {
+  const int m = blockIdx.x;
+  unsigned long long best = 0ull;
+  for (int g = threadIdx.x; g < G; g += RED_THREADS) best = umax64(best, keys[(size_t)g * M + m]);
+  best = umax64(best, max16_u64(best));
+  best = umax64(best, shfl_xor_u64(best, 16));
+  best = umax64(best, shfl_xor_u64(best, 32));
+  __shared__ unsigned long long s_best[RED_THREADS / 64];
+  if ((threadIdx.x & 63) == 0) s_best[threadIdx.x >> 6] = best;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < RED_THREADS / 64; ++w) best = umax64(best, s_best[w]);
+    out[m] = 0x7fffffff - (int)(best & 0xffffffffu);
+  }
+}
+
+hipError_t launch_argmax_groups(const unsigned long long* keys, int G, int M, int* out, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  if (G < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(argmax_groups_kernel, dim3(M), dim3(RED_THREADS), 0, st, keys, G, M, out);
+  return hipGetLastError();
 }
 
 __global__ void zero_u64_kernel(unsigned long long* p, int n) {

@@ -277,6 +277,8 @@ def test_bf16_128_row_verify_and_chunked_prefill():
     err = float(np.max(np.abs(vl - ver.logits)))
     note(f"128-row verify logits: max |err| {err:.3e}")
     assert err < 2e-2
+    # the LM head's fused argmax equals the argmax of its own logits (lowest index on ties)
+    assert np.array_equal(eng.debug("target", np.int32, (cfg.tree_tokens,)), np.argmax(vl, axis=1))
     top2 = np.sort(ver.logits, axis=1)[:, -2:]
     if np.min(top2[:, 1] - top2[:, 0]) >= 4e-2:  # no near tie decides a target
         assert got == ref
@@ -307,6 +309,7 @@ def test_bf16_batch_of_eight_verify_rows():
     trees = eng.debug("tree_token", np.int32, (B, T))
     parents = eng.debug("tree_parent", np.int32, (B, T))
     vl = eng.debug("verify_logits", np.float32, (B * T, V))
+    assert np.array_equal(eng.debug("target", np.int32, (B * T,)), np.argmax(vl, axis=1))
     d1 = eng.debug("draft_logits1", np.float32, (B, V))
     compared = 0
     for b in range(B):
