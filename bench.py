@@ -95,14 +95,15 @@ def cpu_baseline(cfg, seed=0):
         cores = os.cpu_count() or 1
     c1 = cfg.with_(n_layers=1, batch=1)
     w = synth.make_weights(c1, seed=seed, device="cpu")
-    o = oracle.CloverOracle(c1, w)
+    o = oracle.make_oracle(c1, w)
     del w
     rng = np.random.default_rng(1)
     L = _prompt_lengths(cfg)[0]
     prec = o.prec
     shape = (L, c1.n_kv_heads, c1.head_dim)
     kv = [(prec.store(rng.standard_normal(shape)), prec.store(rng.standard_normal(shape)))]
-    ab = (prec.store(rng.standard_normal(shape)), prec.store(rng.standard_normal(shape)))
+    ab = None if cfg.draft == "medusa" else (prec.store(rng.standard_normal(shape)),
+                                             prec.store(rng.standard_normal(shape)))
     st = oracle.SeqState(tokens=list(rng.integers(0, c1.vocab, L)), kv=kv, ab_kv=ab,
                          h0=rng.standard_normal(c1.d_model), t0=int(rng.integers(0, c1.vocab)))
     # oracle steps of the 1-layer slice, repeated for a stable figure (about 6 s)
@@ -224,7 +225,8 @@ def main():
     d, F, V = cfg.d_model, cfg.ffn_dim, cfg.vocab
     qd, kvd = cfg.n_heads * cfg.head_dim, cfg.n_kv_heads * cfg.head_dim
     layer_w = (qd * d + 2 * kvd * d + d * qd + 3 * F * d) * es
-    verify_wbytes = (cfg.n_layers + 1) * layer_w + V * d * es
+    ab_layers = 0 if cfg.draft == "medusa" else 1  # the Augmenting Block runs inside the verify
+    verify_wbytes = (cfg.n_layers + ab_layers) * layer_w + V * d * es
     result = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -238,7 +240,7 @@ def main():
         "vs_baseline": None,
         "dtype": cfg.dtype,
         "data": "synthetic: random-init N(0,0.02) weights, uniform-random prompt tokens",
-        "config": {"workload": cfg.name, "n_layers": cfg.n_layers, "d_model": d,
+        "config": {"workload": cfg.name, "speculator": cfg.draft, "n_layers": cfg.n_layers, "d_model": d,
                    "n_heads": cfg.n_heads, "n_kv_heads": cfg.n_kv_heads, "head_dim": cfg.head_dim,
                    "ffn_dim": F, "vocab": V, "spec_heads": cfg.n_spec_heads, "topk": list(cfg.topk),
                    "batch": cfg.batch, "tree_tokens": T, "prompt_len": lens,

@@ -42,6 +42,18 @@ typedef enum {
 
 typedef enum { CLOVER_F32 = 0, CLOVER_BF16 = 1 } clover_dtype;
 
+/* Speculator of the step.
+ *  CLOVER_DRAFT_CLOVER: the Clover heads (Sec. 3): Augmenting Block state, per depth the
+ *    Regressive Connection and Attention Decoder on every frontier node, the head's MLP
+ *    and the shared LM head; the tree grows one regressive depth per head.
+ *  CLOVER_DRAFT_MEDUSA: the Medusa baseline the paper compares against (Sec. 1, 2.3;
+ *    Sec. 4.4: Clover without Attention Decoder, Regressive Connection and Augmenting
+ *    Block): every head reads the target's last hidden state of the last committed
+ *    token, head j's top-k tokens become the depth-j children of every depth-(j-1) node
+ *    (Cartesian product), and all heads share one LM-head pass.  There is no Augmenting
+ *    Block and no Attention Decoder, so their weights are absent from the weight list. */
+typedef enum { CLOVER_DRAFT_CLOVER = 0, CLOVER_DRAFT_MEDUSA = 1 } clover_draft_mode;
+
 #define CLOVER_MAX_HEADS 8
 
 /* Model and decoding configuration.  The target model is a pre-norm decoder
@@ -66,6 +78,7 @@ typedef struct {
   int32_t kv_block;     /* KV page size in tokens; must be 16 */
   int32_t prefill_chunk;/* prompt rows per prefill chunk (multiple of 64); 0 = 256 */
   int32_t flags;        /* CLOVER_FLAG_* */
+  int32_t draft_mode;   /* clover_draft_mode */
 } clover_config;
 
 #define CLOVER_FLAG_KEEP_LOGITS 1 /* keep draft and verify logits of the last step readable */
@@ -86,7 +99,8 @@ clover_status clover_check_config(const clover_config* cfg);
  * final_norm, lm_head, ab.{same nine}, ad.{norm,wq,wk,wv,wo}, head{j}.{w1,b1}.
  * The ab.* tensors are the Augmenting Block (Sec. 3.3), ad.* the Attention Decoder
  * (Sec. 3.2, Eq. 1-2), head{j}.* the per-head MLP layers; lm_head is shared by all
- * heads and supplies the Regressive Connection embeddings (Sec. 3.4). */
+ * heads and supplies the Regressive Connection embeddings (Sec. 3.4).  With
+ * CLOVER_DRAFT_MEDUSA the ab.* and ad.* entries are left out. */
 size_t clover_weight_count(const clover_config* cfg);
 /* Writes the NUL-terminated name of weight i into buf; returns its length or -1. */
 int clover_weight_name(const clover_config* cfg, size_t i, char* buf, size_t buflen);

@@ -22,3 +22,9 @@ from .model import (Precision, rmsnorm, rope, attention, silu, logsumexp,  # noq
                     LayerWeights, layer_forward, BaseModel)
 from .clover import (CloverOracle, SeqState, Tree, Candidates, build_tree, tree_mask,  # noqa: F401
                      accept, rc_embed, attention_decoder, topk_ids)
+from .medusa import MedusaOracle  # noqa: F401
+
+
+def make_oracle(cfg, weights):
+    """The oracle of the workload's speculator (Clover heads or the Medusa baseline)."""
+    return MedusaOracle(cfg, weights) if getattr(cfg, "draft", "clover") == "medusa" else CloverOracle(cfg, weights)

@@ -19,6 +19,7 @@ FLAG_KEEP_LOGITS = 1
 FLAG_PROFILE = 2
 FLAG_EAGER = 4
 KSTAT = {"gemm_verify": 0, "gemm_draft": 1, "attention": 2, "other": 3}
+DRAFT_MODES = {"clover": 0, "medusa": 1}
 
 
 class CloverError(RuntimeError):
@@ -36,7 +37,8 @@ class ConfigC(ctypes.Structure):
                 ("n_spec_heads", ctypes.c_int32), ("topk", ctypes.c_int32 * MAX_HEADS),
                 ("tree_tokens", ctypes.c_int32), ("max_batch", ctypes.c_int32),
                 ("max_context", ctypes.c_int32), ("kv_block", ctypes.c_int32),
-                ("prefill_chunk", ctypes.c_int32), ("flags", ctypes.c_int32)]
+                ("prefill_chunk", ctypes.c_int32), ("flags", ctypes.c_int32),
+                ("draft_mode", ctypes.c_int32)]
 
 
 class TimingsC(ctypes.Structure):
@@ -130,6 +132,7 @@ def make_config(cfg, max_batch: Optional[int] = None, max_context: Optional[int]
     c.kv_block = 16
     c.prefill_chunk = int(prefill_chunk)
     c.flags = int(flags)
+    c.draft_mode = DRAFT_MODES[getattr(cfg, "draft", "clover")]
     return c
 
 

@@ -44,6 +44,9 @@ constexpr int QKV_MAX_SPLITS = 2;  // Q|K|V may be split when the plan prefers i
 size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 int es_of(int dtype) { return dtype == CLOVER_BF16 ? 2 : 4; }
+bool is_medusa(const clover_config& c) { return c.draft_mode == CLOVER_DRAFT_MEDUSA; }
+// layers with a KV cache: the target's, plus the Augmenting Block's (Clover draft only)
+int kv_layers(const clover_config& c) { return c.n_layers + (is_medusa(c) ? 0 : 1); }
 int kc_of(int dtype) { return dtype == CLOVER_BF16 ? 32 : 16; }
 
 // ---- canonical weights ----------------------------------------------------------------
@@ -70,12 +73,14 @@ std::vector<WSpec> weight_specs(const clover_config& c) {
   for (int l = 0; l < c.n_layers; ++l) layer_specs(c, "layer" + std::to_string(l), s);
   s.push_back({"final_norm", d, 0, false});
   s.push_back({"lm_head", V, d, true});
-  layer_specs(c, "ab", s);
-  s.push_back({"ad.norm", d, 0, false});
-  s.push_back({"ad.wq", qd, d, true});
-  s.push_back({"ad.wk", qd, d, true});
-  s.push_back({"ad.wv", qd, d, true});
-  s.push_back({"ad.wo", d, qd, true});
+  if (!is_medusa(c)) {
+    layer_specs(c, "ab", s);
+    s.push_back({"ad.norm", d, 0, false});
+    s.push_back({"ad.wq", qd, d, true});
+    s.push_back({"ad.wk", qd, d, true});
+    s.push_back({"ad.wv", qd, d, true});
+    s.push_back({"ad.wo", d, qd, true});
+  }
   for (int j = 0; j < c.n_spec_heads; ++j) {
     s.push_back({"head" + std::to_string(j) + ".w1", d, d, true});
     s.push_back({"head" + std::to_string(j) + ".b1", d, 0, false});
@@ -111,6 +116,8 @@ bool check_config(const clover_config* c, std::string& why) {
   auto fail = [&](const char* m) { why = m; return false; };
   if (!c) return fail("config is null");
   if (c->dtype != CLOVER_F32 && c->dtype != CLOVER_BF16) return fail("dtype must be F32 or BF16");
+  if (c->draft_mode != CLOVER_DRAFT_CLOVER && c->draft_mode != CLOVER_DRAFT_MEDUSA)
+    return fail("draft_mode must be CLOVER_DRAFT_CLOVER or CLOVER_DRAFT_MEDUSA");
   const int kc = kc_of(c->dtype);
   if (c->n_layers < 1 || c->n_layers > 1024) return fail("n_layers out of range");
   if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128) return fail("head_dim must be 32, 64 or 128");
@@ -148,6 +155,7 @@ struct Layout {
   size_t tree_token, tree_parent, tree_depth, tree_pos, tree_mask, target, acc, acc_len, out_tokens;
   size_t dstate[CLOVER_MAX_HEADS], dlogits[CLOVER_MAX_HEADS];
   size_t d_hin, d_a, d_e, d_q, d_kv, d_o, d_sst, d_r, d_rn;
+  size_t m_tok, m_logp;  // Medusa draft: per-(head, sequence) top-k tokens and log-probs
   size_t gpart, gpart2, amax_part, topk_scratch;
   size_t apart, apart_floats;  // attention split partials
   size_t gpart_floats, gpart2_floats;
@@ -170,11 +178,12 @@ Layout make_layout(const clover_config& c) {
     L.Fsum += c.max_batch * frontier(c, j);
     L.Fmaxrows = std::max(L.Fmaxrows, c.max_batch * frontier(c, j));
   }
+  if (is_medusa(c)) L.Fmaxrows = std::max(L.Fmaxrows, c.max_batch * L.H);  // all heads' rows at once
   L.mbps = (c.max_context + 15) / 16;
   L.nblocks = c.max_batch * L.mbps;
   const int64_t d = c.d_model, V = c.vocab, F = c.ffn_dim, hd = c.head_dim;
   const int64_t qd = c.n_heads * hd, kvd = c.n_kv_heads * hd;
-  const int NL = c.n_layers + 1;  // base layers + Augmenting Block
+  const int NL = kv_layers(c);  // base layers (+ Augmenting Block)
   L.pool_bytes = align_up((size_t)L.nblocks * kvd * 16 * L.es);
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + std::max<size_t>(bytes, 1)); return o; };
@@ -214,10 +223,18 @@ Layout make_layout(const clover_config& c) {
   L.acc = take(4 * (size_t)c.max_batch * (L.H + 1));
   L.acc_len = take(4 * (size_t)c.max_batch);
   L.out_tokens = take(4 * (size_t)c.max_batch * (L.H + 1));
-  for (int j = 1; j <= L.H; ++j) {
-    const size_t rows = (size_t)c.max_batch * frontier(c, j);
-    L.dstate[j - 1] = take(4 * rows * d);
-    L.dlogits[j - 1] = take(4 * rows * V);
+  if (is_medusa(c)) {
+    // one LM-head pass over every head's rows: logits [H][batch][V], head after head
+    const size_t all = take(4 * (size_t)L.H * c.max_batch * V);
+    for (int j = 1; j <= L.H; ++j) L.dlogits[j - 1] = all;
+    L.m_tok = take(4 * (size_t)L.H * c.max_batch * 16);
+    L.m_logp = take(4 * (size_t)L.H * c.max_batch * 16);
+  } else {
+    for (int j = 1; j <= L.H; ++j) {
+      const size_t rows = (size_t)c.max_batch * frontier(c, j);
+      L.dstate[j - 1] = take(4 * rows * d);
+      L.dlogits[j - 1] = take(4 * rows * V);
+    }
   }
   const size_t fr = L.Fmaxrows;
   L.d_hin = take(4 * fr * d);
@@ -277,7 +294,7 @@ struct clover_ctx {
   hipStream_t st;
   char* ws;
   std::vector<const void*> w;
-  std::vector<LayerPtrs> layers;  // n_layers + 1 (Augmenting Block last)
+  std::vector<LayerPtrs> layers;  // n_layers (+ Augmenting Block last, Clover draft)
   const void *emb, *final_norm, *lm_head, *ad_norm, *ad_wq, *ad_wk, *ad_wv, *ad_wo;
   std::vector<const void*> head_w1, head_b1;
   // host state
@@ -534,6 +551,7 @@ hipError_t enq_verify(clover_ctx* c, int B, int max_keys) {
     ProfScope ps(c, CLOVER_KSTAT_OTHER, 0, 0);
     HE(launch_argmax_groups(c->at<unsigned long long>(L.amax_part), lm_groups, M, c->at<int>(L.target), c->st));
   }
+  if (is_medusa(cf)) return hipSuccess;  // xa keeps x_N: the next Medusa draft reads it
   // Augmenting Block over the tree (tree mask, its own KV cache)
   HE(run_layer(c, c->layers[cf.n_layers], cf.n_layers, xa, M, att, max_keys, 0, &pend));
   RowFixParams ra{};
@@ -561,8 +579,8 @@ hipError_t enq_accept(clover_ctx* c, int B) {
   CompactParams cp{};
   cp.seq_ids = c->at<int>(L.seq_ids); cp.nbatch = B; cp.H = H;
   cp.acc = c->at<int>(L.acc); cp.acc_len = c->at<int>(L.acc_len); cp.seq_len = c->at<int>(L.seq_len);
-  cp.kpools = c->at<void*>(L.pool_ptrs); cp.vpools = c->at<void*>(L.pool_ptrs) + (cf.n_layers + 1);
-  cp.nlayers = cf.n_layers + 1;
+  cp.kpools = c->at<void*>(L.pool_ptrs); cp.vpools = c->at<void*>(L.pool_ptrs) + kv_layers(cf);
+  cp.nlayers = kv_layers(cf);
   cp.block_table = c->at<int>(L.block_table); cp.max_blocks = L.mbps;
   cp.n_kv = cf.n_kv_heads; cp.hd = cf.head_dim;
   ProfScope ps(c, CLOVER_KSTAT_OTHER, 0, 0);
@@ -631,9 +649,63 @@ hipError_t run_phase(clover_ctx* c, hipGraphExec_t* slot, bool graph, Fn&& fn) {
   return hipGraphLaunch(*slot, c->st);
 }
 
+hipError_t enq_tree(clover_ctx* c, int B);
+
+// Medusa draft (the paper's baseline, Sec. 2.3): every head reads x_N of the last committed
+// token; head j: r = x + SiLU(W1_j x + b1_j), logits = W_lm RMSNorm_f(r) -- the Clover head
+// block without Attention Decoder, Regressive Connection and Augmenting Block (Sec. 4.4).
+// The heads' rows share one LM-head pass; their top-k lists span the candidate tree as a
+// Cartesian product.
+hipError_t enq_draft_medusa(clover_ctx* c, int B) {
+  const clover_config& cf = c->cfg;
+  const Layout& L = c->L;
+  const int d = cf.d_model, H = L.H;
+  int* ids = c->at<int>(L.seq_ids);
+  int *ct = c->at<int>(L.cand_token), *cpar = c->at<int>(L.cand_parent), *cd = c->at<int>(L.cand_depth);
+  float* clp = c->at<float>(L.cand_lp);
+  HE(launch_set_root(ids, B, c->at<int>(L.t0), ct, cpar, cd, clp, L.NC, c->st));
+  HE(launch_gather_state(cf.dtype, ids, B, c->at<float>(L.h0), d, c->at<float>(L.d_hin), c->at<void>(L.d_a), c->st));
+  float* part = c->at<float>(L.gpart);
+  char* rn = c->at<char>(L.d_rn);
+  for (int j = 1; j <= H; ++j) {
+    int sh = 0;
+    GemmParams hm{};
+    hm.X = c->at<void>(L.d_a); hm.ldx = d; hm.mode = EP_PARTIAL; hm.max_splits = GEMM_MAX_SPLITS; hm.part = part;
+    HE(run_gemm(c, hm, B, d, {{c->head_w1[j - 1], d}}, &sh));
+    RowFixParams rh{};  // r = x + SiLU(W1 x + b1), then the shared final norm into head j's rows
+    rh.M = B; rh.d = d; rh.part = part; rh.S = sh; rh.ldp = d;
+    rh.resid = c->at<float>(L.d_hin); rh.ldr = d; rh.act = 1; rh.bias = c->head_b1[j - 1];
+    rh.gain = c->final_norm; rh.eps = cf.rms_eps;
+    rh.out_norm = rn + (size_t)(j - 1) * B * d * L.es; rh.ldn = d;
+    HE(run_rowfix(c, rh));
+  }
+  GemmParams lm{};
+  lm.X = rn; lm.ldx = d; lm.mode = EP_PARTIAL; lm.max_splits = 1;
+  lm.part = c->at<float>(L.dlogits[0]);
+  HE(run_gemm(c, lm, H * B, d, {{c->lm_head, cf.vocab}}));
+  int kmax = 1;
+  for (int j = 0; j < H; ++j) kmax = std::max(kmax, cf.topk[j]);
+  TopkParams tp{};  // the top-k_j of head j are the first k_j of its top-kmax
+  tp.logits = c->at<float>(L.dlogits[0]); tp.M = H * B; tp.V = cf.vocab; tp.k = kmax;
+  tp.tok = c->at<int>(L.m_tok); tp.logp = c->at<float>(L.m_logp);
+  tp.scratch = c->at<float>(L.topk_scratch);
+  HE(launch_topk(tp, c->st));
+  MedusaExpandParams mx{};
+  mx.seq_ids = ids; mx.nbatch = B; mx.H = H; mx.kmax = kmax;
+  for (int j = 0; j < H; ++j) mx.topk[j] = cf.topk[j];
+  mx.tok = c->at<int>(L.m_tok); mx.logp = c->at<float>(L.m_logp);
+  mx.cand_token = ct; mx.cand_parent = cpar; mx.cand_depth = cd; mx.cand_lp = clp; mx.cand_stride = L.NC;
+  {
+    ProfScope ps(c, CLOVER_KSTAT_OTHER, 0, 0);
+    HE(launch_medusa_expand(mx, c->st));
+  }
+  return enq_tree(c, B);
+}
+
 // Draft (Sec. 3): per depth, Attention Decoder on the frontier (Eq. 1-2), head MLP,
 // shared final norm + LM head, top-k children; then truncation into the verify tree.
 hipError_t enq_draft(clover_ctx* c, int B) {
+  if (is_medusa(c->cfg)) return enq_draft_medusa(c, B);
   const clover_config& cf = c->cfg;
   const Layout& L = c->L;
   const int d = cf.d_model, qd = cf.n_heads * cf.head_dim, H = L.H;
@@ -694,9 +766,16 @@ hipError_t enq_draft(clover_ctx* c, int B) {
     tp.scratch = c->at<float>(L.topk_scratch);
     HE(launch_topk(tp, c->st));
   }
+  return enq_tree(c, B);
+}
+
+// Truncation of every listed sequence's candidates into its verify tree and verify rows.
+hipError_t enq_tree(clover_ctx* c, int B) {
+  const Layout& L = c->L;
   TreeParams tr{};
-  tr.seq_ids = ids; tr.nbatch = B;
-  tr.cand_token = ct; tr.cand_parent = cpar; tr.cand_depth = cd; tr.cand_lp = clp;
+  tr.seq_ids = c->at<int>(L.seq_ids); tr.nbatch = B;
+  tr.cand_token = c->at<int>(L.cand_token); tr.cand_parent = c->at<int>(L.cand_parent);
+  tr.cand_depth = c->at<int>(L.cand_depth); tr.cand_lp = c->at<float>(L.cand_lp);
   tr.cand_stride = L.NC; tr.n_cand = L.NC; tr.T = L.T; tr.mask_words = L.W;
   tr.seq_len = c->at<int>(L.seq_len);
   tr.tree_token = c->at<int>(L.tree_token); tr.tree_parent = c->at<int>(L.tree_parent);
@@ -865,8 +944,10 @@ clover_status clover_init(const clover_config* cfg, void* const* weights, void* 
   for (int l = 0; l < cfg->n_layers; ++l) c->layers.push_back(take_layer());
   c->final_norm = c->w[k++];
   c->lm_head = c->w[k++];
-  c->layers.push_back(take_layer());
-  c->ad_norm = c->w[k++]; c->ad_wq = c->w[k++]; c->ad_wk = c->w[k++]; c->ad_wv = c->w[k++]; c->ad_wo = c->w[k++];
+  if (!is_medusa(*cfg)) {
+    c->layers.push_back(take_layer());
+    c->ad_norm = c->w[k++]; c->ad_wq = c->w[k++]; c->ad_wk = c->w[k++]; c->ad_wv = c->w[k++]; c->ad_wo = c->w[k++];
+  }
   for (int j = 0; j < cfg->n_spec_heads; ++j) {
     c->head_w1.push_back(c->w[k++]);
     c->head_b1.push_back(c->w[k++]);
@@ -895,10 +976,11 @@ clover_status clover_init(const clover_config* cfg, void* const* weights, void* 
   // zero the KV pools (attention reads whole 16-key blocks), counters and state
   if ((e = hipMemsetAsync(c->ws, 0, L.pool_ptrs, c->st)) != hipSuccess) return fail(e, "memset pools");
   if ((e = hipMemsetAsync(c->ws + L.block_table, 0, L.x - L.block_table, c->st)) != hipSuccess) return fail(e, "memset state");
-  std::vector<void*> pools(2 * (cfg->n_layers + 1));
-  for (int l = 0; l <= cfg->n_layers; ++l) {
+  const int NL = kv_layers(*cfg);
+  std::vector<void*> pools(2 * NL);
+  for (int l = 0; l < NL; ++l) {
     pools[l] = c->ws + L.kpool + L.pool_bytes * l;
-    pools[cfg->n_layers + 1 + l] = c->ws + L.vpool + L.pool_bytes * l;
+    pools[NL + l] = c->ws + L.vpool + L.pool_bytes * l;
   }
   if ((e = hipMemcpyAsync(c->ws + L.pool_ptrs, pools.data(), sizeof(void*) * pools.size(),
                           hipMemcpyHostToDevice, c->st)) != hipSuccess)
@@ -994,11 +1076,13 @@ clover_status clover_prefill(clover_ctx* c, int32_t seq, const int32_t* tokens, 
       HIPCK(c, run_gemm(c, lm, 1, d, {{c->lm_head, cf.vocab}}, nullptr, &lm_groups));
       HIPCK(c, launch_argmax_groups(c->at<unsigned long long>(L.amax_part), lm_groups, 1, c->at<int>(L.amax), c->st));
     }
-    HIPCK(c, run_layer(c, c->layers[cf.n_layers], cf.n_layers, xa, rows, att, c0 + rows, 0, &pend));
-    RowFixParams ra{};
-    ra.M = rows; ra.d = d; ra.part = c->at<float>(L.gpart); ra.S = pend; ra.ldp = d;
-    ra.resid = xa; ra.ldr = d; ra.out_f = xa; ra.ldo = d;
-    HIPCK(c, run_rowfix(c, ra));
+    if (!is_medusa(cf)) {  // Augmenting Block over the chunk; Medusa keeps x_N in xa
+      HIPCK(c, run_layer(c, c->layers[cf.n_layers], cf.n_layers, xa, rows, att, c0 + rows, 0, &pend));
+      RowFixParams ra{};
+      ra.M = rows; ra.d = d; ra.part = c->at<float>(L.gpart); ra.S = pend; ra.ldp = d;
+      ra.resid = xa; ra.ldr = d; ra.out_f = xa; ra.ldo = d;
+      HIPCK(c, run_rowfix(c, ra));
+    }
     if (c0 + rows == n)
       HIPCK(c, launch_finish_prefill(seq, c->at<int>(L.amax), xa + (size_t)(rows - 1) * d, d,
                                      c->at<int>(L.t0), c->at<float>(L.h0), c->st));
@@ -1129,8 +1213,13 @@ clover_status clover_debug_read(clover_ctx* c, const char* name, void* host_dst,
       {"x_last", L.x, 4 * B * T * (size_t)cf.d_model}, {"ab_out", L.xa, 4 * B * T * (size_t)cf.d_model}};
   std::vector<std::string> dn;
   for (int j = 1; j <= L.H; ++j) dn.push_back("draft_logits" + std::to_string(j));
-  for (int j = 1; j <= L.H; ++j)
-    items.push_back({dn[j - 1].c_str(), L.dlogits[j - 1], 4 * B * frontier(cf, j) * (size_t)cf.vocab});
+  for (int j = 1; j <= L.H; ++j) {
+    if (is_medusa(cf))  // head j's rows of the last step's batch
+      items.push_back({dn[j - 1].c_str(), L.dlogits[0] + 4 * (size_t)(j - 1) * c->last_nbatch * cf.vocab,
+                       4 * (size_t)c->last_nbatch * cf.vocab});
+    else
+      items.push_back({dn[j - 1].c_str(), L.dlogits[j - 1], 4 * B * frontier(cf, j) * (size_t)cf.vocab});
+  }
   for (auto& it : items) {
     if (strcmp(it.n, name)) continue;
     const size_t n = std::min(bytes, it.bytes);
@@ -1148,7 +1237,7 @@ clover_status clover_debug_kv(clover_ctx* c, int32_t seq, int32_t layer, int32_t
   if (s) return s;
   const clover_config& cf = c->cfg;
   const Layout& L = c->L;
-  if (seq < 0 || seq >= cf.max_batch || layer < 0 || layer > cf.n_layers || !host_out)
+  if (seq < 0 || seq >= cf.max_batch || layer < 0 || layer >= kv_layers(cf) || !host_out)
     return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "bad argument");
   if (pos < 0 || pos >= (int)c->seq_blocks[seq].size() * 16) return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "position not allocated");
   const int hd = cf.head_dim, nkv = cf.n_kv_heads, EPL = 16 / L.es, KC = 4 * EPL;

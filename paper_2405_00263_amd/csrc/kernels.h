@@ -193,6 +193,19 @@ struct CompactParams {
 };
 hipError_t launch_compact(int dtype, CompactParams& p, hipStream_t st);
 
+// Medusa draft: candidate tree of every listed sequence from the heads' top-k lists
+// tok/logp [H][nbatch][kmax] (Cartesian product; the root, candidate 0, is already set)
+struct MedusaExpandParams {
+  const int* seq_ids; int nbatch, H, kmax;
+  int topk[8];
+  const int* tok; const float* logp;
+  int* cand_token; int* cand_parent; int* cand_depth; float* cand_lp; int cand_stride;
+};
+hipError_t launch_medusa_expand(const MedusaExpandParams& p, hipStream_t st);
+// Medusa draft input: row b = h0[seq_ids[b]] as fp32 (out_f) and in the storage type (out_s)
+hipError_t launch_gather_state(int dtype, const int* seq_ids, int nbatch, const float* h0, int d,
+                               float* out_f, void* out_s, hipStream_t st);
+
 hipError_t launch_fill_i32(int* p, int v, size_t n, hipStream_t st);
 // draft root (candidate 0 of each listed slot) from the pending token t0[slot]
 hipError_t launch_set_root(const int* seq_ids, int nbatch, const int* t0, int* cand_token,

@@ -590,6 +590,34 @@ hipError_t launch_ad_attn(int dtype, const float* q, int Sq, const float* kv, in
   return hipGetLastError();
 }
 
+// Medusa heads read the target's hidden state of the last committed token (per slot):
+// gathered into batch rows, as fp32 (the residual of the head block) and in the storage
+// type (the head GEMM's input).
+template <typename S>
+__global__ __launch_bounds__(256) void gather_state_kernel(const int* __restrict__ seq_ids,
+                                                           const float* __restrict__ h0, int d,
+                                                           float* __restrict__ out_f, S* __restrict__ out_s) {
+  const int b = blockIdx.x;
+  const float* src = h0 + (size_t)seq_ids[b] * d;
+  for (int k = threadIdx.x; k < d; k += 256) {
+    const float v = src[k];
+    out_f[(size_t)b * d + k] = v;
+    out_s[(size_t)b * d + k] = St<S>::from_f(v);
+  }
+}
+
+hipError_t launch_gather_state(int dtype, const int* seq_ids, int nbatch, const float* h0, int d,
+                               float* out_f, void* out_s, hipStream_t st) {
+  if (nbatch <= 0) return hipSuccess;
+  if (dtype == 1)
+    hipLaunchKernelGGL(gather_state_kernel<bf16_t>, dim3(nbatch), dim3(256), 0, st, seq_ids, h0, d, out_f,
+                       (bf16_t*)out_s);
+  else
+    hipLaunchKernelGGL(gather_state_kernel<float>, dim3(nbatch), dim3(256), 0, st, seq_ids, h0, d, out_f,
+                       (float*)out_s);
+  return hipGetLastError();
+}
+
 __global__ void fill_i32_kernel(int* p, int v, size_t n) {
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
     p[i] = v;

@@ -229,6 +229,39 @@ hipError_t launch_set_root(const int* seq_ids, int nbatch, const int* t0, int* c
   return hipGetLastError();
 }
 
+// Medusa candidates (Cartesian product, Sec. 2.3): the children of every depth-(j-1) node
+// are head j's top-k_j tokens, in rank order, with lp(child) = lp(parent) + logp_j(token)
+// in fp32.  Creation order matches the Clover draft's: depth by depth, parents in creation
+// order, children in rank order.  One workgroup per sequence; the cumulative log-probs of
+// a depth are written before the next depth reads them.
+__global__ __launch_bounds__(TREE_THREADS) void medusa_expand_kernel(const MedusaExpandParams p) {
+  const int b = blockIdx.x, slot = p.seq_ids[b];
+  const size_t cb = (size_t)slot * p.cand_stride;
+  int base_prev = 0, base = 1, fprev = 1;
+  for (int j = 1; j <= p.H; ++j) {
+    const int k = p.topk[j - 1];
+    const size_t row = ((size_t)(j - 1) * p.nbatch + b) * p.kmax;  // head j, sequence b
+    for (int e = threadIdx.x; e < fprev * k; e += TREE_THREADS) {
+      const int n = e / k, r = e % k, parent = base_prev + n, child = base + e;
+      p.cand_token[cb + child] = p.tok[row + r];
+      p.cand_parent[cb + child] = parent;
+      p.cand_depth[cb + child] = j;
+      p.cand_lp[cb + child] = p.cand_lp[cb + parent] + p.logp[row + r];
+    }
+    __syncthreads();
+    base_prev = base;
+    base += fprev * k;
+    fprev *= k;
+  }
+}
+
+hipError_t launch_medusa_expand(const MedusaExpandParams& p, hipStream_t st) {
+  if (p.nbatch <= 0) return hipSuccess;
+  if (p.H < 1 || p.H > 8 || p.kmax < 1 || p.kmax > 16) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(medusa_expand_kernel, dim3(p.nbatch), dim3(TREE_THREADS), 0, st, p);
+  return hipGetLastError();
+}
+
 __global__ void finish_prefill_kernel(int slot, const int* amax, const float* ab_row, int d, int* t0,
                                       float* h0) {
   if (threadIdx.x == 0) t0[slot] = amax[0];

@@ -30,6 +30,7 @@ class CloverConfig:
     rms_eps: float = 1e-6
     rope_theta: float = 10000.0
     kv_block: int = 16
+    draft: str = "clover"      # speculator: "clover" heads or the "medusa" baseline
 
     @property
     def n_spec_heads(self) -> int:
@@ -77,6 +78,10 @@ CONFIGS = {
         ffn_dim=28672, vocab=125696, dtype="bf16", topk=(8, 4, 2, 2), tree_tokens=64,
         batch=1, prompt_len=(2048, 2048), steps=64, max_context=2048 + 64 * 5 + 128),
 }
+# the same shapes with the Medusa baseline as speculator (no Augmenting Block or Attention
+# Decoder; heads on the last hidden state, Cartesian-product tree)
+for _n in ("tiny_fp32", "llama7b_b1", "llama7b_b8", "large_gqa_b1"):
+    CONFIGS[_n + "_medusa"] = CONFIGS[_n].with_(name=_n + "_medusa", draft="medusa")
 
 # tree-size sweep on the 7B shape: (tree tokens incl. root, per-depth top-k)
 SWEEP_TREES = ((16, (4, 2, 2)), (32, (4, 3, 2)), (64, (8, 4, 2)), (128, (16, 4, 2)))

@@ -30,10 +30,11 @@ def weight_specs(c: CloverConfig) -> List[Tuple[str, Tuple[int, ...]]]:
     for l in range(c.n_layers):
         specs += _layer_specs(f"layer{l}", c)
     specs += [("final_norm", (d,)), ("lm_head", (V, d))]
-    specs += _layer_specs("ab", c)
-    qd = c.n_heads * c.head_dim
-    specs += [("ad.norm", (d,)), ("ad.wq", (qd, d)), ("ad.wk", (qd, d)), ("ad.wv", (qd, d)),
-              ("ad.wo", (d, qd))]
+    if c.draft != "medusa":  # Augmenting Block and Attention Decoder: Clover heads only
+        specs += _layer_specs("ab", c)
+        qd = c.n_heads * c.head_dim
+        specs += [("ad.norm", (d,)), ("ad.wq", (qd, d)), ("ad.wk", (qd, d)), ("ad.wv", (qd, d)),
+                  ("ad.wo", (d, qd))]
     for j in range(c.n_spec_heads):
         specs += [(f"head{j}.w1", (d, d)), (f"head{j}.b1", (d,))]
     return specs

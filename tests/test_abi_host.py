@@ -59,7 +59,8 @@ def test_workspace_sizes_fit_one_device():
 
 @pytest.mark.parametrize("field,value", [("head_dim", 48), ("n_kv_heads", 3), ("d_model", 100),
                                          ("tree_tokens", 200), ("vocab", 1000), ("kv_block", 32),
-                                         ("ffn_dim", 40), ("max_batch", 0), ("prefill_chunk", 100)])
+                                         ("ffn_dim", 40), ("max_batch", 0), ("prefill_chunk", 100),
+                                         ("draft_mode", 2), ("draft_mode", -1)])
 def test_invalid_config_rejected(field, value):
     import paper_2405_00263_amd as P
     c = P.make_config(synth.get_config("tiny_fp32"))

@@ -354,3 +354,87 @@ def test_graph_replay_matches_eager_launches():
         assert np.array_equal(g.debug("h0", np.float32, (2, cfg.d_model)), e.debug("h0", np.float32, (2, cfg.d_model)))
         torch.cuda.synchronize()
     assert g.seq_len(0) == e.seq_len(0) and g.seq_len(1) == e.seq_len(1)
+
+
+def test_medusa_tiny_fp32_sixteen_steps_match_oracle_and_greedy():
+    """The Medusa baseline on the same kernels: heads on x_N of the last committed token,
+    one LM-head pass for all heads, Cartesian candidate tree.  Head logits within 1e-4 of
+    the oracle, candidate and verify trees exact, tokens equal to the oracle's and to
+    plain greedy decoding; committed KV equals the oracle's."""
+    P = need_gpu()
+    note("engine medusa tiny_fp32 16 steps")
+    cfg = synth.get_config("tiny_fp32_medusa")
+    w = synth.make_weights(cfg, seed=0, perturb=True)
+    eng = _engine(P, cfg, w)
+    o = oracle.MedusaOracle(cfg, w)
+    prompt = synth.make_prompt(cfg)
+    t0 = eng.prefill(0, prompt)
+    st = o.prefill(prompt)
+    assert t0 == st.t0
+    assert np.max(np.abs(eng.debug("h0", np.float32, (1, cfg.d_model))[0] - st.h0)) < 1e-4
+    out = [t0]
+    T = cfg.tree_tokens
+    for step in range(16):
+        ours = eng.step([0])[0]
+        ref, det = o.step(st)
+        cands = det["cands"]
+        for j in range(1, cfg.n_spec_heads + 1):
+            dl = eng.debug(f"draft_logits{j}", np.float32, (1, cfg.vocab))[0]
+            assert np.max(np.abs(dl - cands.head_logits[j - 1])) < 1e-4, (step, j)
+        n = len(cands.token)
+        for f, dt in (("token", np.int32), ("parent", np.int32), ("depth", np.int32)):
+            assert np.array_equal(eng.debug(f"cand_{f}", dt, (1, n))[0], getattr(cands, f)), (step, f)
+        assert np.array_equal(eng.debug("tree_token", np.int32, (1, T))[0], det["tree"].tokens)
+        assert np.array_equal(eng.debug("tree_parent", np.int32, (1, T))[0], det["tree"].parent)
+        vl = eng.debug("verify_logits", np.float32, (T, cfg.vocab))
+        assert np.max(np.abs(vl - det["ver"].logits)) < 1e-4
+        assert ours == ref, (step, ours, ref)
+        out += ours
+    assert eng.seq_len(0) == st.L
+    assert out == o.base.greedy_generate(prompt, len(out))
+    for layer in (0, cfg.n_layers - 1):
+        for pos in (0, 127, 128, st.L - 1):
+            for which in (0, 1):
+                got = eng.debug_kv(0, layer, pos, bool(which))
+                assert np.max(np.abs(got - st.kv[layer][which][pos].reshape(-1))) < 1e-4, (layer, pos, which)
+    with pytest.raises(P.CloverError):
+        eng.debug_kv(0, cfg.n_layers, 0, False)  # no Augmenting Block cache in Medusa mode
+
+
+def test_medusa_bf16_batch_of_three_within_tolerance():
+    """bf16 Medusa over three sequences of different lengths: each sequence's head logits
+    within 2e-2 of its oracle; trees and tokens compared while no decision is a near tie."""
+    P = need_gpu()
+    note("engine medusa bf16 batch 3")
+    cfg = _bf16_small().with_(draft="medusa", batch=3)
+    w = synth.make_weights(cfg, seed=8, perturb=True)
+    eng = _engine(P, cfg, w)
+    o = oracle.MedusaOracle(cfg, w)
+    lens = [100, 37, 64]
+    states = []
+    for s in range(3):
+        prompt = synth.make_prompt(cfg, seq=s, n=lens[s])
+        assert eng.prefill(s, prompt) == (st := o.prefill(prompt)).t0
+        states.append(st)
+    B, T, V = 3, cfg.tree_tokens, cfg.vocab
+    for step in range(3):
+        got = eng.step([0, 1, 2])
+        trees = eng.debug("tree_token", np.int32, (B, T))
+        vl = eng.debug("verify_logits", np.float32, (B * T, V))
+        heads = [eng.debug(f"draft_logits{j}", np.float32, (B, V)) for j in range(1, cfg.n_spec_heads + 1)]
+        same = True
+        for b in range(B):
+            ref, det = o.step(states[b])
+            for j in range(cfg.n_spec_heads):
+                assert float(np.max(np.abs(heads[j][b] - det["cands"].head_logits[j]))) < 2e-2, (step, b, j)
+            if not np.array_equal(trees[b], det["tree"].tokens):
+                same = False
+                continue
+            assert float(np.max(np.abs(vl[b * T:(b + 1) * T] - det["ver"].logits))) < 2e-2
+            top2 = np.sort(det["ver"].logits, axis=1)[:, -2:]
+            if np.min(top2[:, 1] - top2[:, 0]) >= 4e-2:
+                assert got[b] == ref, (step, b)
+            else:
+                same = False
+        if not same:
+            break

@@ -1,0 +1,100 @@
+"""Pins for the oracle's Medusa draft (the paper's baseline speculator).
+
+Each pin holds by the method's definition, not by retyping the oracle:
+- greedy speculative output equals greedy autoregressive output (Sec. 1, 2.1);
+- the candidate tree is the Cartesian product of the heads' top-k sets (Sec. 1, 2.3):
+  brute force over every root path;
+- Sec. 4.4: Clover with the Attention Decoder, the Regressive Connection and the
+  Augmenting Block removed is Medusa.  With their output projections zeroed the
+  Augmenting Block and the Attention Decoder are exactly the identity, so the Clover
+  oracle then drafts the very tree the Medusa oracle drafts, step after step.
+"""
+import itertools
+
+import numpy as np
+import pytest
+import scipy.special
+
+import oracle
+import synth
+from oracle import CloverOracle, MedusaOracle, topk_ids
+
+
+def _medusa(seed=0, **kw):
+    cfg = synth.tiny_test_config(draft="medusa", **kw)
+    w = synth.make_weights(cfg, seed=seed, perturb=True)
+    return cfg, w, MedusaOracle(cfg, w)
+
+
+def test_medusa_weight_list_has_no_clover_parts():
+    cfg = synth.tiny_test_config(draft="medusa")
+    names = [n for n, _ in synth.weight_specs(cfg)]
+    assert not any(n.startswith(("ab.", "ad.")) for n in names)
+    assert [n for n in names if n.startswith("head")] == [f"head{j}.{p}" for j in range(3) for p in ("w1", "b1")]
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_medusa_speculative_equals_greedy_autoregressive(seed):
+    cfg, _, o = _medusa(seed, topk=(3, 2, 2), tree_tokens=12)
+    prompt = synth.make_prompt(cfg, seq=seed, n=12)
+    spec, _ = o.generate(prompt, 14)
+    assert spec == o.base.greedy_generate(prompt, 14)
+
+
+@pytest.mark.parametrize("topk", [(4, 3, 2), (2, 2, 2), (3, 1, 2)])
+def test_medusa_tree_is_cartesian_product(topk):
+    cfg, _, o = _medusa(3, topk=topk)
+    st = o.prefill(synth.make_prompt(cfg, n=10))
+    c = o.draft(st)
+    H = len(topk)
+    assert len(c.token) == 1 + sum(int(np.prod(topk[:j + 1])) for j in range(H))
+    kids = [list(topk_ids(c.head_logits[j], topk[j])) for j in range(H)]
+    # every root path of depth j spells one element of K_1 x ... x K_j, each exactly once
+    for j in range(1, H + 1):
+        paths = []
+        for n in np.nonzero(c.depth == j)[0]:
+            p, toks = int(n), []
+            while p > 0:
+                toks.append(int(c.token[p])); p = int(c.parent[p])
+            paths.append(tuple(toks[::-1]))
+        assert sorted(paths) == sorted(itertools.product(*[[int(t) for t in kids[i]] for i in range(j)]))
+    # children of one parent are head j's top-k in rank order; lp adds logp_j in fp32
+    for n in range(1, len(c.token)):
+        j, par = int(c.depth[n]), int(c.parent[n])
+        sib = [i for i in range(len(c.token)) if c.parent[i] == par]
+        assert [int(c.token[i]) for i in sib] == [int(t) for t in kids[j - 1]]
+        logp = c.head_logits[j - 1] - scipy.special.logsumexp(c.head_logits[j - 1])
+        want = np.float64(c.lp[par]) + logp[c.token[n]]
+        assert abs(float(c.lp[n]) - want) <= 2e-7 * max(1.0, abs(want))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_clover_without_its_three_components_is_medusa(dtype):
+    """Sec. 4.4: zero the Augmenting Block's attention and MLP output projections and the
+    Attention Decoder's output projection; the Clover oracle's candidate trees, verify
+    trees and emitted tokens then equal the Medusa oracle's on the same base and heads."""
+    cfg_m = synth.tiny_test_config(draft="medusa", dtype=dtype, topk=(3, 2, 2), tree_tokens=12)
+    cfg_c = cfg_m.with_(draft="clover")
+    wc = synth.make_weights(cfg_c, seed=5, perturb=True)
+    for n in ("ab.wo", "ab.w_down", "ad.wo"):
+        wc[n] = wc[n] * 0
+    wm = {n: wc[n] for n, _ in synth.weight_specs(cfg_m)}
+    oc, om = CloverOracle(cfg_c, wc), MedusaOracle(cfg_m, wm)
+    prompt = synth.make_prompt(cfg_m, n=14)
+    sc, sm = oc.prefill(prompt), om.prefill(prompt)
+    assert sc.t0 == sm.t0 and np.array_equal(sc.h0, sm.h0)
+    for _ in range(5):
+        ec, dc = oc.step(sc)
+        em, dm = om.step(sm)
+        for f in ("token", "parent", "depth", "lp"):
+            assert np.array_equal(getattr(dc["cands"], f), getattr(dm["cands"], f)), f
+        assert np.array_equal(dc["tree"].tokens, dm["tree"].tokens)
+        assert ec == em
+        assert np.array_equal(sc.h0, sm.h0)
+
+
+def test_make_oracle_picks_the_speculator():
+    cfg, w, _ = _medusa()
+    assert isinstance(oracle.make_oracle(cfg, w), MedusaOracle)
+    cfg_c = cfg.with_(draft="clover")
+    assert isinstance(oracle.make_oracle(cfg_c, synth.make_weights(cfg_c)), CloverOracle)
