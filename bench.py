@@ -102,8 +102,8 @@ def cpu_baseline(cfg, seed=0):
     prec = o.prec
     shape = (L, c1.n_kv_heads, c1.head_dim)
     kv = [(prec.store(rng.standard_normal(shape)), prec.store(rng.standard_normal(shape)))]
-    ab = None if cfg.draft == "medusa" else (prec.store(rng.standard_normal(shape)),
-                                             prec.store(rng.standard_normal(shape)))
+    ab = None if cfg.ab_kind in ("none", "mlp") else (prec.store(rng.standard_normal(shape)),
+                                                       prec.store(rng.standard_normal(shape)))
     st = oracle.SeqState(tokens=list(rng.integers(0, c1.vocab, L)), kv=kv, ab_kv=ab,
                          h0=rng.standard_normal(c1.d_model), t0=int(rng.integers(0, c1.vocab)))
     # oracle steps of the 1-layer slice, repeated for a stable figure (about 6 s)
@@ -149,6 +149,10 @@ def main():
                     help="override the prompt length (context sweep cells)")
     ap.add_argument("--tree-tokens", type=int, default=0, help="override T (tree tokens, root included)")
     ap.add_argument("--topk", default="", help="override the per-depth top-k, e.g. 16,4,2")
+    ap.add_argument("--draft", default="", choices=["", "clover", "medusa"],
+                    help="override the speculator: Clover heads or the Medusa baseline")
+    ap.add_argument("--ab", default="", choices=["", "default", "full", "attn", "mlp", "none"],
+                    help="override the Augmenting Block variant (Sec. 4.4)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "
@@ -168,6 +172,10 @@ def main():
         over["tree_tokens"] = args.tree_tokens
     if args.topk:
         over["topk"] = tuple(int(v) for v in args.topk.split(","))
+    if args.draft:
+        over["draft"] = args.draft
+    if args.ab:
+        over["ab"] = args.ab
     if over:
         cfg = cfg.with_(**over)
     torch.cuda.set_device(0)
@@ -225,8 +233,10 @@ def main():
     d, F, V = cfg.d_model, cfg.ffn_dim, cfg.vocab
     qd, kvd = cfg.n_heads * cfg.head_dim, cfg.n_kv_heads * cfg.head_dim
     layer_w = (qd * d + 2 * kvd * d + d * qd + 3 * F * d) * es
-    ab_layers = 0 if cfg.draft == "medusa" else 1  # the Augmenting Block runs inside the verify
-    verify_wbytes = (cfg.n_layers + ab_layers) * layer_w + V * d * es
+    # the Augmenting Block (or its configured half) runs inside the verify
+    ab_w = {"full": layer_w, "none": 0, "attn": (qd * d + 2 * kvd * d + d * qd) * es,
+            "mlp": 3 * F * d * es}[cfg.ab_kind]
+    verify_wbytes = cfg.n_layers * layer_w + ab_w + V * d * es
     result = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -240,7 +250,8 @@ def main():
         "vs_baseline": None,
         "dtype": cfg.dtype,
         "data": "synthetic: random-init N(0,0.02) weights, uniform-random prompt tokens",
-        "config": {"workload": cfg.name, "speculator": cfg.draft, "n_layers": cfg.n_layers, "d_model": d,
+        "config": {"workload": cfg.name, "speculator": cfg.draft, "augmenting_block": cfg.ab_kind,
+                   "n_layers": cfg.n_layers, "d_model": d,
                    "n_heads": cfg.n_heads, "n_kv_heads": cfg.n_kv_heads, "head_dim": cfg.head_dim,
                    "ffn_dim": F, "vocab": V, "spec_heads": cfg.n_spec_heads, "topk": list(cfg.topk),
                    "batch": cfg.batch, "tree_tokens": T, "prompt_len": lens,

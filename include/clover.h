@@ -54,6 +54,20 @@ typedef enum { CLOVER_F32 = 0, CLOVER_BF16 = 1 } clover_dtype;
  *    Block and no Attention Decoder, so their weights are absent from the weight list. */
 typedef enum { CLOVER_DRAFT_CLOVER = 0, CLOVER_DRAFT_MEDUSA = 1 } clover_draft_mode;
 
+/* Augmenting Block variants explored in Sec. 4.4: a whole pre-norm transformer layer
+ * (attention and MLP halves), the attention half only, the MLP half only, or none (the
+ * heads then read x_N, the residual after the target's last layer).  Its output at the
+ * last committed token is the drafting state h_0.  CLOVER_AB_DEFAULT is CLOVER_AB_FULL
+ * for the Clover draft and CLOVER_AB_NONE for the Medusa draft; a Medusa draft with an
+ * Augmenting Block is Clover without Attention Decoder and Regressive Connection. */
+typedef enum {
+  CLOVER_AB_DEFAULT = 0,
+  CLOVER_AB_FULL = 1,
+  CLOVER_AB_ATTN = 2,
+  CLOVER_AB_MLP = 3,
+  CLOVER_AB_NONE = 4
+} clover_ab_mode;
+
 #define CLOVER_MAX_HEADS 8
 
 /* Model and decoding configuration.  The target model is a pre-norm decoder
@@ -79,6 +93,7 @@ typedef struct {
   int32_t prefill_chunk;/* prompt rows per prefill chunk (multiple of 64); 0 = 256 */
   int32_t flags;        /* CLOVER_FLAG_* */
   int32_t draft_mode;   /* clover_draft_mode */
+  int32_t ab_mode;      /* clover_ab_mode */
 } clover_config;
 
 #define CLOVER_FLAG_KEEP_LOGITS 1 /* keep draft and verify logits of the last step readable */
@@ -100,7 +115,9 @@ clover_status clover_check_config(const clover_config* cfg);
  * The ab.* tensors are the Augmenting Block (Sec. 3.3), ad.* the Attention Decoder
  * (Sec. 3.2, Eq. 1-2), head{j}.* the per-head MLP layers; lm_head is shared by all
  * heads and supplies the Regressive Connection embeddings (Sec. 3.4).  With
- * CLOVER_DRAFT_MEDUSA the ab.* and ad.* entries are left out. */
+ * CLOVER_DRAFT_MEDUSA the ad.* entries are left out; the ab.* entries are those of the
+ * Augmenting Block's halves that clover_ab_mode keeps (attn_norm, wq, wk, wv, wo for the
+ * attention half, mlp_norm, w_gate, w_up, w_down for the MLP half). */
 size_t clover_weight_count(const clover_config* cfg);
 /* Writes the NUL-terminated name of weight i into buf; returns its length or -1. */
 int clover_weight_name(const clover_config* cfg, size_t i, char* buf, size_t buflen);

@@ -164,7 +164,7 @@ def accept(tokens: Sequence[int], parent: Sequence[int], target: Sequence[int]):
 class SeqState:
     tokens: List[int]                                  # committed tokens, positions 0..L-1
     kv: List[Tuple[np.ndarray, np.ndarray]]           # per base layer, [L, n_kv, hd]
-    ab_kv: Tuple[np.ndarray, np.ndarray]               # Augmenting Block cache
+    ab_kv: Optional[Tuple[np.ndarray, np.ndarray]]     # Augmenting Block cache (None: no attention)
     h0: np.ndarray                                     # AB output at position L-1
     t0: int                                            # next token (root of the next tree)
 
@@ -188,14 +188,21 @@ class CloverOracle:
                   for k, v in weights.items()}
         self.base = BaseModel(cfg, self.w)
         self.prec = self.base.prec
-        self.ab = LayerWeights.from_dict(self.w, "ab")
+        self.ab_kind = getattr(cfg, "ab_kind", "full")
+        self.ab = None if self.ab_kind == "none" else LayerWeights.from_dict(self.w, "ab", partial=True)
 
     # -- Augmenting Block -------------------------------------------------------------------
     def ab_forward(self, x_rows, pos, ab_kv, tail_visible):
+        """Sec. 3.3 (and the variants of Sec. 4.4): the whole layer, its attention or MLP half,
+        or none (the rows pass through).  Returns (h, k_new, v_new); k/v None without attention."""
         c = self.cfg
-        return layer_forward(x_rows, np.asarray(pos), self.ab, ab_kv[0], ab_kv[1], tail_visible,
+        if self.ab_kind == "none":
+            return x_rows, None, None
+        attn = self.ab_kind in ("full", "attn")
+        kp, vp = ab_kv if attn else (None, None)
+        return layer_forward(x_rows, np.asarray(pos), self.ab, kp, vp, tail_visible,
                              c.n_heads, c.n_kv_heads, c.head_dim, c.rms_eps, c.rope_theta,
-                             self.prec)
+                             self.prec, attn=attn, mlp=self.ab_kind in ("full", "mlp"))
 
     # -- prefill (Sec. 1: the prompt is processed in one pass and yields the first token) ---
     def prefill(self, prompt: Sequence[int]) -> SeqState:
@@ -204,7 +211,8 @@ class CloverOracle:
         x, kv = self.base.forward_rows(prompt, np.arange(n), None, causal)
         t0 = int(np.argmax(self.base.logits(x[-1:])[0]))
         h, k, v = self.ab_forward(x, np.arange(n), self.base.empty_kv(), causal)
-        return SeqState(tokens=list(prompt), kv=kv, ab_kv=(k, v), h0=h[-1].copy(), t0=t0)
+        return SeqState(tokens=list(prompt), kv=kv, ab_kv=None if k is None else (k, v),
+                        h0=h[-1].copy(), t0=t0)
 
     # -- drafting (Sec. 3) ---------------------------------------------------------------
     def head_logits(self, j: int, s: np.ndarray) -> np.ndarray:
@@ -253,7 +261,8 @@ class CloverOracle:
                  for (kp, vp), (k, v) in zip(st.kv, ver.kv)]
         causal = np.tril(np.ones((A, A), dtype=bool))
         h, k, v = self.ab_forward(ver.x_last[acc], L + np.arange(A), st.ab_kv, causal)
-        st.ab_kv = (np.concatenate([st.ab_kv[0], k]), np.concatenate([st.ab_kv[1], v]))
+        if k is not None:
+            st.ab_kv = (np.concatenate([st.ab_kv[0], k]), np.concatenate([st.ab_kv[1], v]))
         st.h0 = h[-1].copy()
         st.tokens.extend(int(t) for t in tree.tokens[acc])
         st.t0 = bonus

@@ -103,19 +103,37 @@ class LayerWeights:
     w_down: np.ndarray
 
     @staticmethod
-    def from_dict(w: Dict[str, np.ndarray], prefix: str) -> "LayerWeights":
-        return LayerWeights(**{f: w[f"{prefix}.{f}"] for f in LayerWeights.__dataclass_fields__})
+    def from_dict(w: Dict[str, np.ndarray], prefix: str, partial: bool = False) -> "LayerWeights":
+        """partial: tensors of a half the layer does not have (Augmenting Block variants) are None."""
+        return LayerWeights(**{f: (w.get(f"{prefix}.{f}") if partial else w[f"{prefix}.{f}"])
+                               for f in LayerWeights.__dataclass_fields__})
 
 
 def layer_forward(x: np.ndarray, pos: np.ndarray, lw: LayerWeights, k_prefix: np.ndarray,
                   v_prefix: np.ndarray, tail_visible: np.ndarray, n_heads: int, n_kv: int,
-                  head_dim: int, eps: float, theta: float, prec: Precision):
+                  head_dim: int, eps: float, theta: float, prec: Precision, attn: bool = True,
+                  mlp: bool = True):
     """One pre-norm decoder layer over new rows ``x`` at positions ``pos``.
 
     The new rows see all ``k_prefix``/``v_prefix`` keys and the new rows' own keys
     where ``tail_visible`` is set.  Returns (x_out, k_new, v_new) with k_new after
-    rotary, both in storage precision (what a KV cache holds).
+    rotary, both in storage precision (what a KV cache holds).  ``attn`` / ``mlp``
+    keep the attention / MLP half (the Augmenting Block variants of Sec. 4.4); without
+    the attention half k_new and v_new are None.
     """
+    k = v = None
+    if attn:
+        x, k, v = _attention_half(x, pos, lw, k_prefix, v_prefix, tail_visible, n_heads, n_kv,
+                                  head_dim, eps, theta, prec)
+    if mlp:
+        m = prec.store(rmsnorm(x, lw.mlp_norm, eps))
+        act = prec.store(silu(m @ lw.w_gate.T) * (m @ lw.w_up.T))
+        x = x + act @ lw.w_down.T
+    return x, k, v
+
+
+def _attention_half(x, pos, lw, k_prefix, v_prefix, tail_visible, n_heads, n_kv, head_dim, eps,
+                    theta, prec):
     n = x.shape[0]
     a = prec.store(rmsnorm(x, lw.attn_norm, eps))
     q = rope((a @ lw.wq.T).reshape(n, n_heads, head_dim), pos, theta)
@@ -126,11 +144,7 @@ def layer_forward(x: np.ndarray, pos: np.ndarray, lw: LayerWeights, k_prefix: np
     vals = np.concatenate([v_prefix, v], axis=0)
     visible = np.concatenate([np.ones((n, k_prefix.shape[0]), dtype=bool), tail_visible], axis=1)
     o = attention(q, keys, vals, visible).reshape(n, n_heads * head_dim)
-    x = x + prec.store(o) @ lw.wo.T
-    m = prec.store(rmsnorm(x, lw.mlp_norm, eps))
-    act = prec.store(silu(m @ lw.w_gate.T) * (m @ lw.w_up.T))
-    x = x + act @ lw.w_down.T
-    return x, k, v
+    return x + prec.store(o) @ lw.wo.T, k, v
 
 
 class BaseModel:

@@ -20,6 +20,7 @@ FLAG_PROFILE = 2
 FLAG_EAGER = 4
 KSTAT = {"gemm_verify": 0, "gemm_draft": 1, "attention": 2, "other": 3}
 DRAFT_MODES = {"clover": 0, "medusa": 1}
+AB_MODES = {"default": 0, "full": 1, "attn": 2, "mlp": 3, "none": 4}
 
 
 class CloverError(RuntimeError):
@@ -38,7 +39,7 @@ class ConfigC(ctypes.Structure):
                 ("tree_tokens", ctypes.c_int32), ("max_batch", ctypes.c_int32),
                 ("max_context", ctypes.c_int32), ("kv_block", ctypes.c_int32),
                 ("prefill_chunk", ctypes.c_int32), ("flags", ctypes.c_int32),
-                ("draft_mode", ctypes.c_int32)]
+                ("draft_mode", ctypes.c_int32), ("ab_mode", ctypes.c_int32)]
 
 
 class TimingsC(ctypes.Structure):
@@ -133,6 +134,7 @@ def make_config(cfg, max_batch: Optional[int] = None, max_context: Optional[int]
     c.prefill_chunk = int(prefill_chunk)
     c.flags = int(flags)
     c.draft_mode = DRAFT_MODES[getattr(cfg, "draft", "clover")]
+    c.ab_mode = AB_MODES[getattr(cfg, "ab", "default")]
     return c
 
 

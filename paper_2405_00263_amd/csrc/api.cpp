@@ -45,8 +45,15 @@ size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 int es_of(int dtype) { return dtype == CLOVER_BF16 ? 2 : 4; }
 bool is_medusa(const clover_config& c) { return c.draft_mode == CLOVER_DRAFT_MEDUSA; }
-// layers with a KV cache: the target's, plus the Augmenting Block's (Clover draft only)
-int kv_layers(const clover_config& c) { return c.n_layers + (is_medusa(c) ? 0 : 1); }
+int ab_mode(const clover_config& c) {
+  if (c.ab_mode != CLOVER_AB_DEFAULT) return c.ab_mode;
+  return is_medusa(c) ? CLOVER_AB_NONE : CLOVER_AB_FULL;
+}
+bool ab_attn(const clover_config& c) { return ab_mode(c) == CLOVER_AB_FULL || ab_mode(c) == CLOVER_AB_ATTN; }
+bool ab_mlp(const clover_config& c) { return ab_mode(c) == CLOVER_AB_FULL || ab_mode(c) == CLOVER_AB_MLP; }
+bool has_ab(const clover_config& c) { return ab_attn(c) || ab_mlp(c); }
+// layers with a KV cache: the target's, plus the Augmenting Block's when it has attention
+int kv_layers(const clover_config& c) { return c.n_layers + (ab_attn(c) ? 1 : 0); }
 int kc_of(int dtype) { return dtype == CLOVER_BF16 ? 32 : 16; }
 
 // ---- canonical weights ----------------------------------------------------------------
@@ -58,12 +65,14 @@ struct WSpec {
   bool matrix;
 };
 
-void layer_specs(const clover_config& c, const std::string& pre, std::vector<WSpec>& out) {
+// attn / mlp: include the attention half (attn_norm .. wo) / the MLP half (mlp_norm .. w_down)
+void layer_specs(const clover_config& c, const std::string& pre, std::vector<WSpec>& out,
+                 bool attn = true, bool mlp = true) {
   const int64_t d = c.d_model, F = c.ffn_dim, qd = (int64_t)c.n_heads * c.head_dim,
                 kvd = (int64_t)c.n_kv_heads * c.head_dim;
   const int64_t shp[9][2] = {{d, 0}, {qd, d}, {kvd, d}, {kvd, d}, {d, qd}, {d, 0}, {F, d}, {F, d}, {d, F}};
   for (int i = 0; i < 9; ++i)
-    out.push_back({pre + "." + kLayer[i], shp[i][0], shp[i][1], shp[i][1] != 0});
+    if (i < 5 ? attn : mlp) out.push_back({pre + "." + kLayer[i], shp[i][0], shp[i][1], shp[i][1] != 0});
 }
 
 std::vector<WSpec> weight_specs(const clover_config& c) {
@@ -73,8 +82,8 @@ std::vector<WSpec> weight_specs(const clover_config& c) {
   for (int l = 0; l < c.n_layers; ++l) layer_specs(c, "layer" + std::to_string(l), s);
   s.push_back({"final_norm", d, 0, false});
   s.push_back({"lm_head", V, d, true});
+  if (has_ab(c)) layer_specs(c, "ab", s, ab_attn(c), ab_mlp(c));
   if (!is_medusa(c)) {
-    layer_specs(c, "ab", s);
     s.push_back({"ad.norm", d, 0, false});
     s.push_back({"ad.wq", qd, d, true});
     s.push_back({"ad.wk", qd, d, true});
@@ -118,6 +127,7 @@ bool check_config(const clover_config* c, std::string& why) {
   if (c->dtype != CLOVER_F32 && c->dtype != CLOVER_BF16) return fail("dtype must be F32 or BF16");
   if (c->draft_mode != CLOVER_DRAFT_CLOVER && c->draft_mode != CLOVER_DRAFT_MEDUSA)
     return fail("draft_mode must be CLOVER_DRAFT_CLOVER or CLOVER_DRAFT_MEDUSA");
+  if (c->ab_mode < CLOVER_AB_DEFAULT || c->ab_mode > CLOVER_AB_NONE) return fail("ab_mode out of range");
   const int kc = kc_of(c->dtype);
   if (c->n_layers < 1 || c->n_layers > 1024) return fail("n_layers out of range");
   if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128) return fail("head_dim must be 32, 64 or 128");
@@ -422,12 +432,11 @@ hipError_t run_rowfix(clover_ctx* c, RowFixParams rp) {
   return launch_rowfix(c->cfg.dtype, rp, c->st);
 }
 
-// One pre-norm decoder layer over M rows of the residual `x` (in place).  `pend` is the
-// split count of the previous down-projection partials in gpart still to be added to
-// x (0: none); returns through *pend_out the split count of this layer's
-// down-projection partials, which the caller's next row kernel adds.
-hipError_t run_layer(clover_ctx* c, const LayerPtrs& lw, int layer_idx, float* x, int M,
-                     AttnParams att, int max_keys, int pend, int* pend_out) {
+// The attention half of a layer on the normalised rows in xn: Q|K|V with rotary and paged
+// KV append, tree-masked (or causal) attention, output projection into split-K partials in
+// gpart, whose split count it returns through *splits.
+hipError_t run_attention_half(clover_ctx* c, const LayerPtrs& lw, int layer_idx, int M, AttnParams att,
+                              int max_keys, int* splits) {
   const clover_config& cf = c->cfg;
   const Layout& L = c->L;
   const int d = cf.d_model, hd = cf.head_dim, qd = cf.n_heads * hd, kvd = cf.n_kv_heads * hd;
@@ -436,11 +445,6 @@ hipError_t run_layer(clover_ctx* c, const LayerPtrs& lw, int layer_idx, float* x
   void* kp = c->ws + L.kpool + L.pool_bytes * layer_idx;
   void* vp = c->ws + L.vpool + L.pool_bytes * layer_idx;
   hipError_t e;
-  RowFixParams rf{};
-  rf.M = M; rf.d = d; rf.part = part; rf.S = pend; rf.ldp = d;
-  rf.resid = x; rf.ldr = d; rf.out_f = x; rf.ldo = d;
-  rf.gain = lw.attn_norm; rf.eps = cf.rms_eps; rf.out_norm = xn; rf.ldn = d;
-  if ((e = run_rowfix(c, rf))) return e;
   GemmParams g{};
   g.X = xn; g.ldx = d; g.mode = EP_QKV;
   g.qbuf = c->at<void>(L.qbuf); g.ldq = qd;
@@ -475,19 +479,45 @@ hipError_t run_layer(clover_ctx* c, const LayerPtrs& lw, int layer_idx, float* x
   }
   GemmParams o{};
   o.X = c->at<void>(L.obuf); o.ldx = qd; o.mode = EP_PARTIAL; o.max_splits = GEMM_MAX_SPLITS; o.part = part;
-  int so = 0;
-  if ((e = run_gemm(c, o, M, qd, {{lw.wo, d}}, &so))) return e;
-  rf.S = so; rf.gain = lw.mlp_norm;
+  return run_gemm(c, o, M, qd, {{lw.wo, d}}, splits);
+}
+
+// One pre-norm decoder layer over M rows of the residual `x` (in place).  `pend` is the
+// split count of the previous down-projection partials in gpart still to be added to
+// x (0: none); returns through *pend_out the split count of this layer's last
+// partials (down projection, or the output projection without the MLP half), which the
+// caller's next row kernel adds.  attn / mlp: run the attention / MLP half (Augmenting
+// Block variants; target layers run both).
+hipError_t run_layer(clover_ctx* c, const LayerPtrs& lw, int layer_idx, float* x, int M,
+                     AttnParams att, int max_keys, int pend, int* pend_out, bool attn = true,
+                     bool mlp = true) {
+  const clover_config& cf = c->cfg;
+  const Layout& L = c->L;
+  const int d = cf.d_model;
+  void* xn = c->at<void>(L.xn);
+  float* part = c->at<float>(L.gpart);
+  hipError_t e;
+  RowFixParams rf{};
+  rf.M = M; rf.d = d; rf.part = part; rf.S = pend; rf.ldp = d;
+  rf.resid = x; rf.ldr = d; rf.out_f = x; rf.ldo = d;
+  rf.gain = attn ? lw.attn_norm : lw.mlp_norm; rf.eps = cf.rms_eps; rf.out_norm = xn; rf.ldn = d;
   if ((e = run_rowfix(c, rf))) return e;
+  if (attn) {
+    if ((e = run_attention_half(c, lw, layer_idx, M, att, max_keys, pend_out))) return e;
+    if (!mlp) return hipSuccess;
+    rf.S = *pend_out; rf.gain = lw.mlp_norm;
+    if ((e = run_rowfix(c, rf))) return e;
+  }
   GemmParams gu{};
   gu.X = xn; gu.ldx = d; gu.mode = EP_SWIGLU;
   gu.out_s = c->at<void>(L.act); gu.ldos = cf.ffn_dim; gu.N = cf.ffn_dim;
   if ((e = run_gemm(c, gu, M, d, {{lw.wg, cf.ffn_dim}, {lw.wu, cf.ffn_dim}}))) return e;
   GemmParams dn{};
   dn.X = c->at<void>(L.act); dn.ldx = cf.ffn_dim; dn.mode = EP_PARTIAL; dn.max_splits = GEMM_MAX_SPLITS;
-  dn.part = part;
+  dn.part = c->at<float>(L.gpart);
   return run_gemm(c, dn, M, cf.ffn_dim, {{lw.wd, d}}, pend_out);
 }
+
 
 clover_status ensure_blocks(clover_ctx* c, int slot, int upto) {
   const int need = (upto + 15) / 16;
@@ -551,9 +581,9 @@ hipError_t enq_verify(clover_ctx* c, int B, int max_keys) {
     ProfScope ps(c, CLOVER_KSTAT_OTHER, 0, 0);
     HE(launch_argmax_groups(c->at<unsigned long long>(L.amax_part), lm_groups, M, c->at<int>(L.target), c->st));
   }
-  if (is_medusa(cf)) return hipSuccess;  // xa keeps x_N: the next Medusa draft reads it
+  if (!has_ab(cf)) return hipSuccess;  // xa keeps x_N: the next draft reads it
   // Augmenting Block over the tree (tree mask, its own KV cache)
-  HE(run_layer(c, c->layers[cf.n_layers], cf.n_layers, xa, M, att, max_keys, 0, &pend));
+  HE(run_layer(c, c->layers[cf.n_layers], cf.n_layers, xa, M, att, max_keys, 0, &pend, ab_attn(cf), ab_mlp(cf)));
   RowFixParams ra{};
   ra.M = M; ra.d = d; ra.part = c->at<float>(L.gpart); ra.S = pend; ra.ldp = d;
   ra.resid = xa; ra.ldr = d; ra.out_f = xa; ra.ldo = d;
@@ -651,11 +681,11 @@ hipError_t run_phase(clover_ctx* c, hipGraphExec_t* slot, bool graph, Fn&& fn) {
 
 hipError_t enq_tree(clover_ctx* c, int B);
 
-// Medusa draft (the paper's baseline, Sec. 2.3): every head reads x_N of the last committed
-// token; head j: r = x + SiLU(W1_j x + b1_j), logits = W_lm RMSNorm_f(r) -- the Clover head
-// block without Attention Decoder, Regressive Connection and Augmenting Block (Sec. 4.4).
-// The heads' rows share one LM-head pass; their top-k lists span the candidate tree as a
-// Cartesian product.
+// Medusa draft (the paper's baseline, Sec. 2.3): every head reads the state h_0 of the last
+// committed token -- x_N, or the Augmenting Block's output when one is configured; head j:
+// r = h + SiLU(W1_j h + b1_j), logits = W_lm RMSNorm_f(r) -- the Clover head block without
+// Attention Decoder and Regressive Connection (Sec. 4.4).  The heads' rows share one
+// LM-head pass; their top-k lists span the candidate tree as a Cartesian product.
 hipError_t enq_draft_medusa(clover_ctx* c, int B) {
   const clover_config& cf = c->cfg;
   const Layout& L = c->L;
@@ -944,8 +974,13 @@ clover_status clover_init(const clover_config* cfg, void* const* weights, void* 
   for (int l = 0; l < cfg->n_layers; ++l) c->layers.push_back(take_layer());
   c->final_norm = c->w[k++];
   c->lm_head = c->w[k++];
+  if (has_ab(*cfg)) {  // the Augmenting Block's halves in weight-list order
+    LayerPtrs p{};
+    if (ab_attn(*cfg)) { p.attn_norm = c->w[k++]; p.wq = c->w[k++]; p.wk = c->w[k++]; p.wv = c->w[k++]; p.wo = c->w[k++]; }
+    if (ab_mlp(*cfg)) { p.mlp_norm = c->w[k++]; p.wg = c->w[k++]; p.wu = c->w[k++]; p.wd = c->w[k++]; }
+    c->layers.push_back(p);
+  }
   if (!is_medusa(*cfg)) {
-    c->layers.push_back(take_layer());
     c->ad_norm = c->w[k++]; c->ad_wq = c->w[k++]; c->ad_wk = c->w[k++]; c->ad_wv = c->w[k++]; c->ad_wo = c->w[k++];
   }
   for (int j = 0; j < cfg->n_spec_heads; ++j) {
@@ -1076,8 +1111,9 @@ clover_status clover_prefill(clover_ctx* c, int32_t seq, const int32_t* tokens, 
       HIPCK(c, run_gemm(c, lm, 1, d, {{c->lm_head, cf.vocab}}, nullptr, &lm_groups));
       HIPCK(c, launch_argmax_groups(c->at<unsigned long long>(L.amax_part), lm_groups, 1, c->at<int>(L.amax), c->st));
     }
-    if (!is_medusa(cf)) {  // Augmenting Block over the chunk; Medusa keeps x_N in xa
-      HIPCK(c, run_layer(c, c->layers[cf.n_layers], cf.n_layers, xa, rows, att, c0 + rows, 0, &pend));
+    if (has_ab(cf)) {  // Augmenting Block over the chunk; without it xa keeps x_N
+      HIPCK(c, run_layer(c, c->layers[cf.n_layers], cf.n_layers, xa, rows, att, c0 + rows, 0, &pend,
+                         ab_attn(cf), ab_mlp(cf)));
       RowFixParams ra{};
       ra.M = rows; ra.d = d; ra.part = c->at<float>(L.gpart); ra.S = pend; ra.ldp = d;
       ra.resid = xa; ra.ldr = d; ra.out_f = xa; ra.ldo = d;

@@ -31,6 +31,15 @@ class CloverConfig:
     rope_theta: float = 10000.0
     kv_block: int = 16
     draft: str = "clover"      # speculator: "clover" heads or the "medusa" baseline
+    # Augmenting Block: "full" layer, "attn" or "mlp" half only, "none"; "default" is
+    # "full" for the Clover draft and "none" for the Medusa draft
+    ab: str = "default"
+
+    @property
+    def ab_kind(self) -> str:
+        if self.ab != "default":
+            return self.ab
+        return "none" if self.draft == "medusa" else "full"
 
     @property
     def n_spec_heads(self) -> int:

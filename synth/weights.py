@@ -14,13 +14,14 @@ from .configs import CloverConfig
 _LAYER = ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "w_gate", "w_up", "w_down")
 
 
-def _layer_specs(prefix: str, c: CloverConfig) -> List[Tuple[str, Tuple[int, ...]]]:
+def _layer_specs(prefix: str, c: CloverConfig, attn: bool = True,
+                 mlp: bool = True) -> List[Tuple[str, Tuple[int, ...]]]:
     d, F = c.d_model, c.ffn_dim
     shapes = {
         "attn_norm": (d,), "wq": (c.q_dim, d), "wk": (c.kv_dim, d), "wv": (c.kv_dim, d),
         "wo": (d, c.q_dim), "mlp_norm": (d,), "w_gate": (F, d), "w_up": (F, d), "w_down": (d, F),
     }
-    return [(f"{prefix}.{n}", shapes[n]) for n in _LAYER]
+    return [(f"{prefix}.{n}", shapes[n]) for i, n in enumerate(_LAYER) if (attn if i < 5 else mlp)]
 
 
 def weight_specs(c: CloverConfig) -> List[Tuple[str, Tuple[int, ...]]]:
@@ -30,8 +31,9 @@ def weight_specs(c: CloverConfig) -> List[Tuple[str, Tuple[int, ...]]]:
     for l in range(c.n_layers):
         specs += _layer_specs(f"layer{l}", c)
     specs += [("final_norm", (d,)), ("lm_head", (V, d))]
-    if c.draft != "medusa":  # Augmenting Block and Attention Decoder: Clover heads only
-        specs += _layer_specs("ab", c)
+    if c.ab_kind != "none":  # the Augmenting Block's halves
+        specs += _layer_specs("ab", c, attn=c.ab_kind in ("full", "attn"), mlp=c.ab_kind in ("full", "mlp"))
+    if c.draft != "medusa":  # Attention Decoder: Clover heads only
         qd = c.n_heads * c.head_dim
         specs += [("ad.norm", (d,)), ("ad.wq", (qd, d)), ("ad.wk", (qd, d)), ("ad.wv", (qd, d)),
                   ("ad.wo", (d, qd))]

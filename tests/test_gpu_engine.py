@@ -438,3 +438,34 @@ def test_medusa_bf16_batch_of_three_within_tolerance():
                 same = False
         if not same:
             break
+
+
+@pytest.mark.parametrize("draft,ab", [("clover", "attn"), ("clover", "mlp"), ("clover", "none"),
+                                      ("medusa", "full")])
+def test_speculator_variants_match_oracle(draft, ab):
+    """The Augmenting Block variants of Sec. 4.4 (attention half, MLP half, none) under the
+    Clover draft, and the Augmenting Block feeding parallel heads (Clover without Attention
+    Decoder and Regressive Connection): tiny fp32, six steps, candidate and verify trees
+    exact, verify logits within 1e-4, tokens equal to the oracle's and to greedy decoding."""
+    P = need_gpu()
+    note(f"engine variant draft={draft} ab={ab}")
+    cfg = synth.get_config("tiny_fp32").with_(draft=draft, ab=ab)
+    w = synth.make_weights(cfg, seed=1, perturb=True)
+    eng = _engine(P, cfg, w)
+    o = oracle.make_oracle(cfg, w)
+    prompt = synth.make_prompt(cfg, seq=2)
+    assert eng.prefill(0, prompt) == (st := o.prefill(prompt)).t0
+    assert np.max(np.abs(eng.debug("h0", np.float32, (1, cfg.d_model))[0] - st.h0)) < 1e-4
+    T, out = cfg.tree_tokens, [st.t0]
+    for step in range(6):
+        ours = eng.step([0])[0]
+        ref, det = o.step(st)
+        n = len(det["cands"].token)
+        assert np.array_equal(eng.debug("cand_token", np.int32, (1, n))[0], det["cands"].token), step
+        assert np.array_equal(eng.debug("tree_token", np.int32, (1, T))[0], det["tree"].tokens), step
+        vl = eng.debug("verify_logits", np.float32, (T, cfg.vocab))
+        assert np.max(np.abs(vl - det["ver"].logits)) < 1e-4, step
+        assert np.max(np.abs(eng.debug("h0", np.float32, (1, cfg.d_model))[0] - st.h0)) < 1e-4, step
+        assert ours == ref, (step, ours, ref)
+        out += ours
+    assert out == o.base.greedy_generate(prompt, len(out))

@@ -98,3 +98,50 @@ def test_make_oracle_picks_the_speculator():
     assert isinstance(oracle.make_oracle(cfg, w), MedusaOracle)
     cfg_c = cfg.with_(draft="clover")
     assert isinstance(oracle.make_oracle(cfg_c, synth.make_weights(cfg_c)), CloverOracle)
+
+
+def _decode(o, prompt, steps=4):
+    st = o.prefill(prompt)
+    trace = [(st.t0, st.h0.copy())]
+    for _ in range(steps):
+        em, det = o.step(st)
+        trace.append((em, det["cands"].token.copy(), det["cands"].lp.copy(), det["tree"].tokens.copy(),
+                      st.h0.copy()))
+    return trace
+
+
+def _same(a, b):
+    assert len(a) == len(b)
+    for x, y in zip(a, b):
+        for u, v in zip(x, y):
+            assert np.array_equal(np.asarray(u), np.asarray(v))
+
+
+@pytest.mark.parametrize("variant,zeroed", [("attn", ("ab.w_down",)), ("mlp", ("ab.wo",)),
+                                            ("none", ("ab.wo", "ab.w_down"))])
+def test_augmenting_block_variants_are_the_full_block_with_a_half_removed(variant, zeroed):
+    """Sec. 4.4 explores the Augmenting Block as a whole layer, its attention half, its MLP
+    half, or none.  A half contributes exactly nothing when its output projection is zero,
+    so each variant must draft, verify and emit exactly what the full block does with the
+    other half's output projection zeroed."""
+    cfg_v = synth.tiny_test_config(ab=variant, topk=(3, 2, 2), tree_tokens=12)
+    cfg_f = cfg_v.with_(ab="full")
+    wf = synth.make_weights(cfg_f, seed=6, perturb=True)
+    for n in zeroed:
+        wf[n] = wf[n] * 0
+    wv = {n: wf[n] for n, _ in synth.weight_specs(cfg_v)}
+    prompt = synth.make_prompt(cfg_v, n=13)
+    _same(_decode(CloverOracle(cfg_v, wv), prompt), _decode(CloverOracle(cfg_f, wf), prompt))
+
+
+def test_medusa_heads_on_the_augmenting_block_are_clover_without_ad_and_rc():
+    """Sec. 4.4: Clover without the Attention Decoder (and with it the Regressive
+    Connection) keeps the Augmenting Block and drafts with parallel heads.  The Clover
+    oracle with a zero decoder output projection drafts exactly that Cartesian tree."""
+    cfg_m = synth.tiny_test_config(draft="medusa", ab="full", topk=(3, 2, 2), tree_tokens=12)
+    cfg_c = cfg_m.with_(draft="clover", ab="default")
+    wc = synth.make_weights(cfg_c, seed=7, perturb=True)
+    wc["ad.wo"] = wc["ad.wo"] * 0
+    wm = {n: wc[n] for n, _ in synth.weight_specs(cfg_m)}
+    prompt = synth.make_prompt(cfg_m, n=11)
+    _same(_decode(MedusaOracle(cfg_m, wm), prompt), _decode(CloverOracle(cfg_c, wc), prompt))
