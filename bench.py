@@ -31,7 +31,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 matrix-core peak of MI355X
-TILED_MIN_ROWS = 128  # verify GEMMs with this many rows run the register-blocked kernel
+TILED_MIN_ROWS = 129  # verify GEMMs with this many rows run the register-blocked kernel
 METRIC = "verify-step latency (ms) & tree-tokens/s at 7B shape; weight-stream HBM GB/s vs peak"
 
 
@@ -135,6 +135,77 @@ def cpu_baseline(cfg, seed=0):
     }
 
 
+def verify_weight_bytes(cfg):
+    """Bytes of weight one verify forward streams: target layers, the Augmenting Block (or
+    its configured half) and the LM head."""
+    es = 2 if cfg.dtype == "bf16" else 4
+    d, F, V = cfg.d_model, cfg.ffn_dim, cfg.vocab
+    qd, kvd = cfg.n_heads * cfg.head_dim, cfg.n_kv_heads * cfg.head_dim
+    attn_w = (qd * d + 2 * kvd * d + d * qd) * es
+    layer_w = attn_w + 3 * F * d * es
+    ab_w = {"full": layer_w, "none": 0, "attn": attn_w, "mlp": 3 * F * d * es}[cfg.ab_kind]
+    return cfg.n_layers * layer_w + ab_w + V * d * es
+
+
+def surface(args):
+    """Batch x tree-size cost surface of one step (Sec. 1 and 4.2 of the
+    paper argue that speculation pays while the verify stays memory-bound and loses its
+    edge as batch and tree grow towards the compute bound).
+
+    One JSON line per cell: batch B, tree tokens T, the per-phase latencies, and the verify
+    forward's weight-stream rate and matrix arithmetic rate (2 flops per weight per verify
+    row).  Every cell uses the same weights, a committed context of --prompt-len tokens per
+    sequence (default 1024), top-k (8, 4, 2) truncated to T (T = 128: (16, 4, 2)).
+    """
+    import torch
+    import synth
+    import paper_2405_00263_amd as P
+
+    base = synth.get_config(args.workload)
+    L0 = args.prompt_len or 1024
+    batches = [int(v) for v in args.surface_batches.split(",")]
+    trees = [int(v) for v in args.surface_trees.split(",")]
+    cells = [("clover", B, T) for B in batches for T in trees]
+    cells += [("medusa", B, 64) for B in batches]
+    print(f"[surface] {len(cells)} cells on {base.name}: generating weights on device", file=sys.stderr, flush=True)
+    w = synth.make_weights(base.with_(draft="clover", ab="default"), seed=args.seed, device="cuda")
+    for draft, B, T in cells:
+        cfg = base.with_(batch=B, tree_tokens=T, topk=(16, 4, 2) if T > 64 else (8, 4, 2), draft=draft,
+                         prompt_len=(L0, L0))
+        ww = {n: w[n] for n, _ in synth.weight_specs(cfg)}
+        H1 = cfg.n_spec_heads + 1
+        eng = P.CloverEngine(cfg, ww, max_batch=B, max_context=L0 + (args.warmup + args.steps) * H1 + T + 16)
+        seqs = list(range(B))
+        for b in seqs:
+            eng.prefill(b, synth.make_prompt(cfg, seq=b, n=L0))
+        for _ in range(args.warmup):
+            eng.step(seqs)
+        ph = {"draft_ms": [], "verify_ms": [], "total_ms": []}
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            eng.step(seqs)
+            tm = eng.timings()
+            for k in ph:
+                ph[k].append(tm[k])
+        torch.cuda.synchronize()
+        step_ms = 1e3 * (time.perf_counter() - t0) / args.steps
+        med = {k: statistics.median(v) for k, v in ph.items()}
+        wb = verify_weight_bytes(cfg)
+        params = wb / (2 if cfg.dtype == "bf16" else 4)
+        print(json.dumps({"surface_cell": {
+            "speculator": draft, "batch": B, "tree_tokens": T, "verify_rows": B * T, "context": L0,
+            "step_ms": round(step_ms, 4), "verify_ms": round(med["verify_ms"], 4),
+            "draft_ms": round(med["draft_ms"], 4),
+            "tree_tokens_per_s": round(B * T / (step_ms * 1e-3), 1),
+            "verify_weight_GBps": round(wb / (med["verify_ms"] * 1e-3) / 1e9, 1),
+            "verify_gemm_TFLOPs": round(2.0 * B * T * params / (med["verify_ms"] * 1e-3) / 1e12, 1),
+        }}), flush=True)
+        eng.close()
+        del eng
+        torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -153,12 +224,19 @@ def main():
                     help="override the speculator: Clover heads or the Medusa baseline")
     ap.add_argument("--ab", default="", choices=["", "default", "full", "attn", "mlp", "none"],
                     help="override the Augmenting Block variant (Sec. 4.4)")
+    ap.add_argument("--surface", action="store_true",
+                    help="batch x tree-size cost surface instead of the headline line (one JSON line per cell)")
+    ap.add_argument("--surface-batches", default="1,2,4,8,16")
+    ap.add_argument("--surface-trees", default="4,16,32,64,128")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "
               "(each sequence is independent, so more GPUs would each run their own batch)",
               file=sys.stderr)
         sys.exit(2)
+    if args.surface:
+        surface(args)
+        return
 
     import torch
     import synth
@@ -228,15 +306,8 @@ def main():
     mfma_bound = cfg.dtype == "bf16" and cfg.batch * cfg.tree_tokens >= TILED_MIN_ROWS
     tflops = g["flops"] / (g["total_ms"] * 1e-3) / 1e12 if g["total_ms"] > 0 else 0.0
     med = {k: statistics.median(v) for k, v in phase.items()}
-    # weight bytes streamed by one verify forward (layers + Augmenting Block + LM head)
-    es = 2 if cfg.dtype == "bf16" else 4
     d, F, V = cfg.d_model, cfg.ffn_dim, cfg.vocab
-    qd, kvd = cfg.n_heads * cfg.head_dim, cfg.n_kv_heads * cfg.head_dim
-    layer_w = (qd * d + 2 * kvd * d + d * qd + 3 * F * d) * es
-    # the Augmenting Block (or its configured half) runs inside the verify
-    ab_w = {"full": layer_w, "none": 0, "attn": (qd * d + 2 * kvd * d + d * qd) * es,
-            "mlp": 3 * F * d * es}[cfg.ab_kind]
-    verify_wbytes = cfg.n_layers * layer_w + ab_w + V * d * es
+    verify_wbytes = verify_weight_bytes(cfg)
     result = {
         "metric": METRIC,
         "value": round(value, 2),

@@ -33,6 +33,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <type_traits>
 
 namespace clover {
 
@@ -305,7 +306,17 @@ static const TunedPlan kTuned[] = {
 };
 
 // From this many rows on, bf16 GEMMs use the register-blocked kernel (gemm_tiled.hip).
-static constexpr int TILED_MIN_M = 128;
+static constexpr int TILED_MIN_M = 129;
+
+// Rows per chunk (16 * mt) of the streaming kernel.  Up to 128 rows a bf16 GEMM takes all
+// its rows in one chunk: each weight fragment is loaded into a CU once and feeds mt
+// matrix-core products (two 64-row chunks would load every fragment twice per CU, and a
+// CU's load rate, not HBM, would bound the kernel).
+static int chunk_mt(int dtype, int M) {
+  if (M <= 16) return 1;
+  if (M <= 32) return 2;
+  return (M <= 64 || dtype != 1) ? 4 : 8;
+}
 
 GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int max_splits) {
   if (dtype == 1 && M >= TILED_MIN_M) return plan_tiled(M, ntiles, nchunks, swiglu, max_splits);
@@ -316,7 +327,8 @@ GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int m
     if (swiglu && (nw & 1)) continue;
     GemmPlan pl{};
     pl.nw = nw;
-    pl.mt = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+    pl.mt = chunk_mt(dtype, M);
+    if (pl.mt == 8 && nw != 8) continue;  // the 128-row X ring fits registers with 8 waves only
     const int mrows = 16 * pl.mt;
     pl.mchunks = (std::max(M, 1) + mrows - 1) / mrows;
     pl.ngroups = swiglu ? ((ntiles / 2) + nw / 2 - 1) / (nw / 2) : (ntiles + nw - 1) / nw;
@@ -334,7 +346,7 @@ GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int m
     }
   }
   if (dtype == 1) {
-    const int mt = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+    const int mt = chunk_mt(dtype, M);
     for (const TunedPlan& t : kTuned) {
       if (t.mt != mt || t.ntiles != ntiles || t.nchunks != nchunks || t.swiglu != swiglu) continue;
       if (t.S > std::max(1, std::min(max_splits, nchunks / (2 * STAGE_CHUNKS)))) continue;
@@ -372,8 +384,29 @@ static void launch_nw(const GemmPlan& pl, GemmParams& p, hipStream_t st, const L
   }
 }
 
+// 128-row chunks (bf16 only) run with 8 waves
+template <bool AMAX>
+static hipError_t launch_mt8(const GemmPlan& pl, GemmParams& p, hipStream_t st, const LaunchTiming* lt) {
+  dim3 grid(8 * ((pl.ngroups * pl.S + 7) / 8) * pl.mchunks), block(pl.nw * 64);
+  auto go = [&](auto kern) {
+    if (lt) hipExtLaunchKernelGGL(kern, grid, block, (uint32_t)pl.lds_bytes, st, lt->start, lt->stop, 0, p);
+    else hipLaunchKernelGGL(kern, grid, block, pl.lds_bytes, st, p);
+  };
+  if (pl.nw != 8) return hipErrorInvalidValue;
+  go(gemm_kernel<bf16_t, 8, 8, AMAX>);
+  return hipSuccess;
+}
+
 template <typename S>
 static hipError_t launch_gemm_t(GemmParams& p, const GemmPlan& pl, hipStream_t st, const LaunchTiming* lt) {
+  if (pl.mt == 8) {
+    if constexpr (std::is_same<S, bf16_t>::value) {
+      const hipError_t e = p.amax_part ? launch_mt8<true>(pl, p, st, lt) : launch_mt8<false>(pl, p, st, lt);
+      if (e != hipSuccess) return e;
+      return hipGetLastError();
+    }
+    return hipErrorInvalidValue;
+  }
   if (p.amax_part) {
     switch (pl.mt) {
       case 1: launch_nw<S, 1, true>(pl, p, st, lt); break;

@@ -19,8 +19,11 @@ GEMM_CASES = [
     ("bf16", 64, 22016, 4096, False), ("bf16", 64, 125696, 4096, True), ("bf16", 64, 10240, 8192, False),
     ("bf16", 64, 8192, 28672, True), ("bf16", 512, 4096, 4096, True), ("bf16", 100, 1024, 512, False),
     ("bf16", 3, 48, 64, False),
+    # streaming kernel with one 128-row chunk (65..128 rows): 7B shapes and ragged row counts
+    ("bf16", 128, 12288, 4096, True), ("bf16", 128, 4096, 11008, True), ("bf16", 128, 22016, 4096, True),
+    ("bf16", 65, 4096, 4096, False), ("bf16", 127, 125696, 4096, True),
     # register-blocked kernel: swept 7B shapes, the default rule, ragged row counts
-    ("bf16", 128, 12288, 4096, True), ("bf16", 256, 4096, 11008, True), ("bf16", 300, 4096, 4096, True),
+    ("bf16", 129, 12288, 4096, True), ("bf16", 256, 4096, 11008, True), ("bf16", 300, 4096, 4096, True),
     ("bf16", 512, 22016, 4096, True), ("bf16", 200, 125696, 4096, True), ("bf16", 130, 1024, 512, False),
 ]
 
