@@ -68,6 +68,18 @@ typedef enum {
   CLOVER_AB_NONE = 4
 } clover_ab_mode;
 
+/* Key set of the Attention Decoder (Eq. 1-2).  Read literally, Eq. 1 gives one key, the
+ * embedding e_{i-1} of the previous token, so the softmax weight is exactly 1 and h_i =
+ * h_{i-1} + W_O W_V e_{i-1} (W_Q and W_K do not change the result).  Sec. 3.2's remark that
+ * the decoder takes only two vectors per request or beam reads as the key set
+ * {RMSNorm_ad(h_{i-1}), e_{i-1}}; the third reading attends over the embeddings of every
+ * token on the node's root path. */
+typedef enum {
+  CLOVER_AD_KEYS_SINGLE = 0, /* { e_{i-1} } (default) */
+  CLOVER_AD_KEYS_TWO = 1,    /* { RMSNorm_ad(h_{i-1}), e_{i-1} } */
+  CLOVER_AD_KEYS_PATH = 2    /* { e_0, ..., e_{i-1} } along the root path */
+} clover_ad_keys;
+
 #define CLOVER_MAX_HEADS 8
 
 /* Model and decoding configuration.  The target model is a pre-norm decoder
@@ -94,6 +106,7 @@ typedef struct {
   int32_t flags;        /* CLOVER_FLAG_* */
   int32_t draft_mode;   /* clover_draft_mode */
   int32_t ab_mode;      /* clover_ab_mode */
+  int32_t ad_keys;      /* clover_ad_keys (Clover draft) */
 } clover_config;
 
 #define CLOVER_FLAG_KEEP_LOGITS 1 /* keep draft and verify logits of the last step readable */

@@ -9,7 +9,9 @@ Test infrastructure only.  Follows Sec. 3 of the paper:
   h_{i-1}, K and V from e_{i-1}; h_i = h_{i-1} + Attention(Q, K, V).  Read
   literally, the key set is the single vector e_{i-1}, so the softmax weight is
   exactly 1.  The attention has the base model's head layout and an output
-  projection; its weights are shared by all heads.
+  projection; its weights are shared by all heads.  Two other readings of the key
+  set are selectable (``ad_keys``): the two vectors {RMSNorm(h), e} and the
+  embeddings of every token on the node's root path.
 * Per-head MLP (Sec. 3.2, Sec. 4.1 "Medusa initialisation"): read as the Medusa
   residual block r = h + SiLU(W1 h + b1), one per head.
 * Shared LM head (Sec. 3.4): every head reuses the target's final norm and LM
@@ -219,6 +221,24 @@ class CloverOracle:
         r = head_mlp(s, self.w[f"head{j}.w1"], self.w[f"head{j}.b1"], self.prec)
         return self.base.logits(r[None, :])[0]
 
+    def ad_keys(self, h: np.ndarray, n: int, token, parent) -> np.ndarray:
+        """Key/value inputs of the Attention Decoder for node n with state h (Eq. 1; the key
+        set is a reading): "single" {e(token_n)}; "two" {RMSNorm_ad(h), e(token_n)} (Sec. 3.2:
+        two vectors per request or beam); "path" {e(t) for every token on n's root path,
+        root first}."""
+        kind = getattr(self.cfg, "ad_keys", "single")
+        e = rc_embed(self.w["lm_head"], token[n])
+        if kind == "single":
+            return e[None, :]
+        if kind == "two":
+            a = self.prec.store(rmsnorm(h, self.w["ad.norm"], self.cfg.rms_eps))
+            return np.stack([a, e])
+        path = []
+        while n >= 0:
+            path.append(rc_embed(self.w["lm_head"], token[n]))
+            n = parent[n]
+        return np.stack(path[::-1])
+
     def draft(self, st: SeqState) -> Candidates:
         c = self.cfg
         depth, token, parent = [0], [st.t0], [-1]
@@ -228,9 +248,8 @@ class CloverOracle:
         for j in range(1, c.n_spec_heads + 1):
             frontier = [i for i in range(len(depth)) if depth[i] == j - 1]
             for n in frontier:
-                e = rc_embed(self.w["lm_head"], token[n])
-                s = attention_decoder(state[n], e, self.w, c.n_heads, c.head_dim, c.rms_eps,
-                                      self.prec)
+                s = attention_decoder(state[n], self.ad_keys(state[n], n, token, parent), self.w,
+                                      c.n_heads, c.head_dim, c.rms_eps, self.prec)
                 logits = self.head_logits(j - 1, s)
                 logp = logits - logsumexp(logits)
                 out.row_logits[n] = logits

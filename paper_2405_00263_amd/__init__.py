@@ -21,6 +21,7 @@ FLAG_EAGER = 4
 KSTAT = {"gemm_verify": 0, "gemm_draft": 1, "attention": 2, "other": 3}
 DRAFT_MODES = {"clover": 0, "medusa": 1}
 AB_MODES = {"default": 0, "full": 1, "attn": 2, "mlp": 3, "none": 4}
+AD_KEYS = {"single": 0, "two": 1, "path": 2}
 
 
 class CloverError(RuntimeError):
@@ -39,7 +40,8 @@ class ConfigC(ctypes.Structure):
                 ("tree_tokens", ctypes.c_int32), ("max_batch", ctypes.c_int32),
                 ("max_context", ctypes.c_int32), ("kv_block", ctypes.c_int32),
                 ("prefill_chunk", ctypes.c_int32), ("flags", ctypes.c_int32),
-                ("draft_mode", ctypes.c_int32), ("ab_mode", ctypes.c_int32)]
+                ("draft_mode", ctypes.c_int32), ("ab_mode", ctypes.c_int32),
+                ("ad_keys", ctypes.c_int32)]
 
 
 class TimingsC(ctypes.Structure):
@@ -135,6 +137,7 @@ def make_config(cfg, max_batch: Optional[int] = None, max_context: Optional[int]
     c.flags = int(flags)
     c.draft_mode = DRAFT_MODES[getattr(cfg, "draft", "clover")]
     c.ab_mode = AB_MODES[getattr(cfg, "ab", "default")]
+    c.ad_keys = AD_KEYS[getattr(cfg, "ad_keys", "single")]
     return c
 
 

@@ -128,6 +128,7 @@ bool check_config(const clover_config* c, std::string& why) {
   if (c->draft_mode != CLOVER_DRAFT_CLOVER && c->draft_mode != CLOVER_DRAFT_MEDUSA)
     return fail("draft_mode must be CLOVER_DRAFT_CLOVER or CLOVER_DRAFT_MEDUSA");
   if (c->ab_mode < CLOVER_AB_DEFAULT || c->ab_mode > CLOVER_AB_NONE) return fail("ab_mode out of range");
+  if (c->ad_keys < CLOVER_AD_KEYS_SINGLE || c->ad_keys > CLOVER_AD_KEYS_PATH) return fail("ad_keys out of range");
   const int kc = kc_of(c->dtype);
   if (c->n_layers < 1 || c->n_layers > 1024) return fail("n_layers out of range");
   if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128) return fail("head_dim must be 32, 64 or 128");
@@ -165,6 +166,7 @@ struct Layout {
   size_t tree_token, tree_parent, tree_depth, tree_pos, tree_mask, target, acc, acc_len, out_tokens;
   size_t dstate[CLOVER_MAX_HEADS], dlogits[CLOVER_MAX_HEADS];
   size_t d_hin, d_a, d_e, d_q, d_kv, d_o, d_sst, d_r, d_rn;
+  size_t d_kvpath;  // path key set: fp32 keys/values of every drafted depth's nodes
   size_t m_tok, m_logp;  // Medusa draft: per-(head, sequence) top-k tokens and log-probs
   size_t gpart, gpart2, amax_part, topk_scratch;
   size_t apart, apart_floats;  // attention split partials
@@ -248,7 +250,7 @@ Layout make_layout(const clover_config& c) {
   }
   const size_t fr = L.Fmaxrows;
   L.d_hin = take(4 * fr * d);
-  L.d_a = take((size_t)L.es * fr * d);
+  L.d_a = take((size_t)L.es * 2 * fr * d);  // normalised states, then embeddings (two-token keys)
   L.d_e = take((size_t)L.es * fr * d);
   L.d_q = take(4 * fr * qd);
   L.d_kv = take(4 * fr * 2 * qd);
@@ -256,12 +258,13 @@ Layout make_layout(const clover_config& c) {
   L.d_sst = take((size_t)L.es * fr * d);
   L.d_r = take(4 * fr * d);
   L.d_rn = take((size_t)L.es * fr * d);
+  L.d_kvpath = take(c.ad_keys == CLOVER_AD_KEYS_PATH ? 4 * (size_t)L.Fsum * 2 * qd : 0);
   // split-K partials [S][M][N] of the residual-type GEMMs (at most GEMM_MAX_SPLITS)
   const size_t maxM = std::max<size_t>({(size_t)L.Mv, (size_t)L.Mp, (size_t)L.Fmaxrows});
   const size_t maxN = std::max<size_t>({(size_t)d, (size_t)qd});
   L.gpart_floats = std::max((size_t)GEMM_MAX_SPLITS * maxM * maxN,
                             (size_t)QKV_MAX_SPLITS * maxM * (size_t)(qd + 2 * c.n_kv_heads * c.head_dim));
-  L.gpart2_floats = (size_t)GEMM_MAX_SPLITS * L.Fmaxrows * 2 * qd;  // Attention Decoder keys/values
+  L.gpart2_floats = (size_t)GEMM_MAX_SPLITS * 2 * L.Fmaxrows * 2 * qd;  // Attention Decoder keys/values
   L.gpart = take(4 * L.gpart_floats);
   L.gpart2 = take(4 * L.gpart2_floats);
   // per-(column group, row) argmax keys of the LM-head epilogue: a group holds at least
@@ -754,7 +757,11 @@ hipError_t enq_draft(clover_ctx* c, int B) {
     ap.cand_token = ct; ap.cand_stride = L.NC; ap.base_node = depth_base(cf, j - 1);
     ap.lm_packed = c->lm_head; ap.lm_nchunks = d / kc_of(cf.dtype);
     ap.ad_norm = c->ad_norm; ap.eps = cf.rms_eps; ap.d = d;
-    ap.hin = c->at<float>(L.d_hin); ap.a_out = c->at<void>(L.d_a); ap.e_out = c->at<void>(L.d_e);
+    // with the two-token key set the embeddings follow the normalised states in one [2M][d]
+    // block, so one K|V GEMM projects both
+    const bool two = cf.ad_keys == CLOVER_AD_KEYS_TWO;
+    ap.hin = c->at<float>(L.d_hin); ap.a_out = c->at<void>(L.d_a);
+    ap.e_out = two ? (void*)(c->at<char>(L.d_a) + (size_t)M * d * L.es) : c->at<void>(L.d_e);
     HE(launch_ad_prep(cf.dtype, ap, c->st));
     float* part = c->at<float>(L.gpart);
     float* part2 = c->at<float>(L.gpart2);
@@ -763,10 +770,28 @@ hipError_t enq_draft(clover_ctx* c, int B) {
     q.X = c->at<void>(L.d_a); q.ldx = d; q.mode = EP_PARTIAL; q.max_splits = GEMM_MAX_SPLITS; q.part = part;
     HE(run_gemm(c, q, M, d, {{c->ad_wq, qd}}, &sq));
     GemmParams kv{};
-    kv.X = c->at<void>(L.d_e); kv.ldx = d; kv.mode = EP_PARTIAL; kv.max_splits = GEMM_MAX_SPLITS; kv.part = part2;
-    HE(run_gemm(c, kv, M, d, {{c->ad_wk, qd}, {c->ad_wv, qd}}, &skv));
-    HE(launch_ad_attn(cf.dtype, part, sq, part2, skv, M, cf.n_heads, cf.head_dim,
-                            c->at<void>(L.d_o), c->st));
+    kv.X = two ? c->at<void>(L.d_a) : c->at<void>(L.d_e); kv.ldx = d; kv.mode = EP_PARTIAL;
+    kv.max_splits = GEMM_MAX_SPLITS; kv.part = part2;
+    HE(run_gemm(c, kv, two ? 2 * M : M, d, {{c->ad_wk, qd}, {c->ad_wv, qd}}, &skv));
+    AdAttnParams aa{};
+    aa.q = part; aa.Sq = sq; aa.kv = part2; aa.Skv = skv;
+    aa.M = M; aa.F = F; aa.n_heads = cf.n_heads; aa.hd = cf.head_dim;
+    aa.keys = cf.ad_keys; aa.depth = j - 1; aa.out = c->at<void>(L.d_o);
+    if (cf.ad_keys == CLOVER_AD_KEYS_PATH) {
+      // key/value rows of every depth's nodes, depth after depth; an ancestor at depth dd of
+      // a depth-(j-1) node fl has index fl / (k_dd * ... * k_{j-2}) among its depth's nodes
+      aa.kv_path = c->at<float>(L.d_kvpath);
+      int off = 0;
+      for (int dd = 0; dd < j; ++dd) {
+        aa.kv_path_off[dd] = off;
+        aa.path_nodes[dd] = frontier(cf, dd + 1);
+        off += B * frontier(cf, dd + 1);
+        int div = 1;
+        for (int t = dd; t < j - 1; ++t) div *= cf.topk[t];
+        aa.anc_div[dd] = div;
+      }
+    }
+    HE(launch_ad_attn(cf.dtype, aa, c->st));
     GemmParams o{};
     o.X = c->at<void>(L.d_o); o.ldx = qd; o.mode = EP_PARTIAL; o.max_splits = GEMM_MAX_SPLITS; o.part = part;
     HE(run_gemm(c, o, M, qd, {{c->ad_wo, d}}, &so));

@@ -159,8 +159,25 @@ struct AdPrepParams {
   float* hin; void* a_out; void* e_out;
 };
 hipError_t launch_ad_prep(int dtype, AdPrepParams& p, hipStream_t st);
-hipError_t launch_ad_attn(int dtype, const float* q, int Sq, const float* kv, int Skv, int M,
-                          int n_heads, int hd, void* out, hipStream_t st);
+// Attention Decoder attention (Eq. 1-2) of the M frontier rows of one depth.  Queries from
+// the Q GEMM's split-K partials q[Sq][M][H*hd]; keys/values from the K|V GEMM's partials
+// kv[Skv][rows][2*H*hd] (keys then values), where the key set of row f is
+//   AD_KEYS_SINGLE: { e(token) }                      (kv row f)
+//   AD_KEYS_TWO:    { RMSNorm_ad(h), e(token) }       (kv rows f and M + f)
+//   AD_KEYS_PATH:   { e(t) : t on the row's root path } (earlier depths from kv_path, own: kv row f)
+// With AD_KEYS_PATH the row's own key/value is also stored in kv_path at depth `depth`
+// (rows [B * nodes(d)] per depth d from kv_path_off[d]); an ancestor at depth d < depth of
+// frontier row f = b * F + fl is row b * nodes(d) + fl / anc_div[d] there.
+enum AdKeys : int { AD_KEYS_SINGLE = 0, AD_KEYS_TWO = 1, AD_KEYS_PATH = 2 };
+struct AdAttnParams {
+  const float* q; int Sq;
+  const float* kv; int Skv;
+  int M, F, n_heads, hd, keys, depth;
+  float* kv_path;                 // AD_KEYS_PATH: [sum_d B*nodes(d)][2*H*hd] fp32
+  int kv_path_off[8], path_nodes[8], anc_div[8];
+  void* out;                      // [M][H*hd] storage
+};
+hipError_t launch_ad_attn(int dtype, const AdAttnParams& p, hipStream_t st);
 
 // ---- tree, acceptance, compaction -----------------------------------------------------------
 struct TreeParams {

@@ -550,43 +550,117 @@ hipError_t launch_ad_prep(int dtype, AdPrepParams& p, hipStream_t st) {
   return hipGetLastError();
 }
 
-// ---- Attention Decoder attention (Eq. 1-2): one key per frontier row ----------------------
-// q: split-K partials [Sq][M][H*hd], kv: partials [Skv][M][2*H*hd] (keys then values), f32.
-// The softmax is taken over the key set of the row, which holds the single embedding
-// e_{i-1}.
+// ---- Attention Decoder attention (Eq. 1-2) ----------------------------------------------
+// One workgroup (one wave) per (frontier row, head).  The query and every key/value are the
+// split-K sums of their GEMM partials; the softmax runs over the row's key set (see
+// AdAttnParams) in fp32: scores q.k / sqrt(hd), max-subtracted exponentials, normalised
+// weighted sum of the values.  With a single key the weight is exactly 1.
+static constexpr int AD_MAX_KEYS = 9;   // path keys: one per depth 0..H-1, plus headroom
+static constexpr int AD_DPL = 2;        // dims per lane: hd <= 128
 template <typename S>
-__global__ __launch_bounds__(64) void ad_attn_kernel(const float* __restrict__ q, int Sq,
-                                                     const float* __restrict__ kv, int Skv, int M, int H,
-                                                     int hd, S* __restrict__ out) {
+__global__ __launch_bounds__(64) void ad_attn_kernel(const AdAttnParams p) {
   const int f = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
-  const int qd = H * hd;
-  float dot = 0.f;
-  for (int i = lane; i < hd; i += 64) {
-    float qv = 0.f, kk = 0.f;
-    for (int s = 0; s < Sq; ++s) qv += q[((size_t)s * M + f) * qd + h * hd + i];
-    for (int s = 0; s < Skv; ++s) kk += kv[((size_t)s * M + f) * 2 * qd + h * hd + i];
-    dot += qv * kk;
+  const int qd = p.n_heads * p.hd, M = p.M, hd = p.hd;
+  const int kvrows = p.keys == AD_KEYS_TWO ? 2 * M : M;
+  // split-K sum of one key/value row of the K|V GEMM for this lane's dims
+  auto sum_kv = [&](int row, float* k, float* v) {
+#pragma unroll
+    for (int u = 0; u < AD_DPL; ++u) {
+      const int i = lane + 64 * u;
+      k[u] = v[u] = 0.f;
+      if (i < hd)
+        for (int s = 0; s < p.Skv; ++s) {
+          const float* r = p.kv + ((size_t)s * kvrows + row) * 2 * qd + h * hd + i;
+          k[u] += r[0];
+          v[u] += r[qd];
+        }
+    }
+  };
+  // key slots (static indices): path keys take slots 0..depth-1 for the ancestors and
+  // `depth` for the row's own token; two keys take slot 0 for the state, 1 for the token
+  const int own = p.keys == AD_KEYS_PATH ? p.depth : (p.keys == AD_KEYS_TWO ? 1 : 0);
+  const int nk = own + 1;
+  float ko[AD_DPL], vo[AD_DPL], ks[AD_DPL], vs[AD_DPL];
+  sum_kv(p.keys == AD_KEYS_TWO ? M + f : f, ko, vo);
+  if (p.keys == AD_KEYS_TWO) sum_kv(f, ks, vs);
+  float kk[AD_MAX_KEYS][AD_DPL], vv[AD_MAX_KEYS][AD_DPL];
+  const int b = f / p.F, fl = f % p.F;
+#pragma unroll
+  for (int t = 0; t < AD_MAX_KEYS; ++t) {
+#pragma unroll
+    for (int u = 0; u < AD_DPL; ++u) {
+      const int i = lane + 64 * u;
+      float k = ko[u], v = vo[u];
+      if (t < own) {
+        if (p.keys == AD_KEYS_TWO) {
+          k = ks[u];
+          v = vs[u];
+        } else {  // path: the ancestor at depth t
+          const size_t row = p.kv_path_off[t] + (size_t)b * p.path_nodes[t] + fl / p.anc_div[t];
+          k = i < hd ? p.kv_path[row * 2 * qd + h * hd + i] : 0.f;
+          v = i < hd ? p.kv_path[row * 2 * qd + qd + h * hd + i] : 0.f;
+        }
+      }
+      kk[t][u] = k;
+      vv[t][u] = v;
+    }
   }
-  dot = warp_sum(dot);
-  const float sc = dot * rsqrtf((float)hd);
-  const float mx = sc;               // max over the single key
-  const float pw = expf(sc - mx);    // = 1
-  const float l = pw;
-  for (int i = lane; i < hd; i += 64) {
-    float vv = 0.f;
-    for (int s = 0; s < Skv; ++s) vv += kv[((size_t)s * M + f) * 2 * qd + qd + h * hd + i];
-    out[(size_t)f * qd + h * hd + i] = St<S>::from_f(pw * vv / l);
+  if (p.keys == AD_KEYS_PATH) {  // this depth's rows for the deeper depths' path keys
+    const size_t row = p.kv_path_off[p.depth] + f;
+#pragma unroll
+    for (int u = 0; u < AD_DPL; ++u) {
+      const int i = lane + 64 * u;
+      if (i < hd) {
+        p.kv_path[row * 2 * qd + h * hd + i] = ko[u];
+        p.kv_path[row * 2 * qd + qd + h * hd + i] = vo[u];
+      }
+    }
+  }
+  float q[AD_DPL];
+#pragma unroll
+  for (int u = 0; u < AD_DPL; ++u) {
+    const int i = lane + 64 * u;
+    float x = 0.f;
+    if (i < hd)
+      for (int s = 0; s < p.Sq; ++s) x += p.q[((size_t)s * M + f) * qd + h * hd + i];
+    q[u] = x;
+  }
+  const float scale = rsqrtf((float)hd);
+  float sc[AD_MAX_KEYS], mx = -INFINITY;
+#pragma unroll
+  for (int t = 0; t < AD_MAX_KEYS; ++t) {
+    float dot = 0.f;
+#pragma unroll
+    for (int u = 0; u < AD_DPL; ++u) dot += q[u] * kk[t][u];
+    sc[t] = warp_sum(dot) * scale;
+    if (t < nk) mx = fmaxf(mx, sc[t]);
+  }
+  float l = 0.f;
+#pragma unroll
+  for (int t = 0; t < AD_MAX_KEYS; ++t) {
+    sc[t] = t < nk ? expf(sc[t] - mx) : 0.f;  // a single key: exp(0) = 1
+    l += sc[t];
+  }
+#pragma unroll
+  for (int u = 0; u < AD_DPL; ++u) {
+    const int i = lane + 64 * u;
+    float o = 0.f;
+#pragma unroll
+    for (int t = 0; t < AD_MAX_KEYS; ++t) o += sc[t] * vv[t][u];
+    if (i < hd) reinterpret_cast<S*>(p.out)[(size_t)f * qd + h * hd + i] = St<S>::from_f(o / l);
   }
 }
 
-hipError_t launch_ad_attn(int dtype, const float* q, int Sq, const float* kv, int Skv, int M, int n_heads,
-                          int hd, void* out, hipStream_t st) {
-  if (M <= 0) return hipSuccess;
-  dim3 grid(M, n_heads);
+hipError_t launch_ad_attn(int dtype, const AdAttnParams& p, hipStream_t st) {
+  if (p.M <= 0) return hipSuccess;
+  if (p.hd > 64 * AD_DPL || p.keys < 0 || p.keys > AD_KEYS_PATH) return hipErrorInvalidValue;
+  if (p.keys == AD_KEYS_PATH && (p.depth < 0 || p.depth >= AD_MAX_KEYS - 1 || p.depth >= 8 || !p.kv_path))
+    return hipErrorInvalidValue;
+  dim3 grid(p.M, p.n_heads);
   if (dtype == 1)
-    hipLaunchKernelGGL(ad_attn_kernel<bf16_t>, grid, dim3(64), 0, st, q, Sq, kv, Skv, M, n_heads, hd, (bf16_t*)out);
+    hipLaunchKernelGGL(ad_attn_kernel<bf16_t>, grid, dim3(64), 0, st, p);
   else
-    hipLaunchKernelGGL(ad_attn_kernel<float>, grid, dim3(64), 0, st, q, Sq, kv, Skv, M, n_heads, hd, (float*)out);
+    hipLaunchKernelGGL(ad_attn_kernel<float>, grid, dim3(64), 0, st, p);
   return hipGetLastError();
 }
 

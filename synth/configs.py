@@ -34,6 +34,8 @@ class CloverConfig:
     # Augmenting Block: "full" layer, "attn" or "mlp" half only, "none"; "default" is
     # "full" for the Clover draft and "none" for the Medusa draft
     ab: str = "default"
+    # key set of the Attention Decoder: "single" {e}, "two" {RMSNorm(h), e}, "path" {e_0..}
+    ad_keys: str = "single"
 
     @property
     def ab_kind(self) -> str:

@@ -440,16 +440,19 @@ def test_medusa_bf16_batch_of_three_within_tolerance():
             break
 
 
-@pytest.mark.parametrize("draft,ab", [("clover", "attn"), ("clover", "mlp"), ("clover", "none"),
-                                      ("medusa", "full")])
-def test_speculator_variants_match_oracle(draft, ab):
+@pytest.mark.parametrize("draft,ab,ad_keys", [("clover", "attn", "single"), ("clover", "mlp", "single"),
+                                              ("clover", "none", "single"), ("medusa", "full", "single"),
+                                              ("clover", "default", "two"), ("clover", "default", "path")])
+def test_speculator_variants_match_oracle(draft, ab, ad_keys):
     """The Augmenting Block variants of Sec. 4.4 (attention half, MLP half, none) under the
-    Clover draft, and the Augmenting Block feeding parallel heads (Clover without Attention
-    Decoder and Regressive Connection): tiny fp32, six steps, candidate and verify trees
-    exact, verify logits within 1e-4, tokens equal to the oracle's and to greedy decoding."""
+    Clover draft, the Augmenting Block feeding parallel heads (Clover without Attention
+    Decoder and Regressive Connection), and the two-token and root-path key sets of the
+    Attention Decoder: tiny fp32, six steps, draft logits of every frontier row and verify
+    logits within 1e-4, candidate and verify trees exact, tokens equal to the oracle's and
+    to greedy decoding."""
     P = need_gpu()
-    note(f"engine variant draft={draft} ab={ab}")
-    cfg = synth.get_config("tiny_fp32").with_(draft=draft, ab=ab)
+    note(f"engine variant draft={draft} ab={ab} ad_keys={ad_keys}")
+    cfg = synth.get_config("tiny_fp32").with_(draft=draft, ab=ab, ad_keys=ad_keys)
     w = synth.make_weights(cfg, seed=1, perturb=True)
     eng = _engine(P, cfg, w)
     o = oracle.make_oracle(cfg, w)
@@ -461,6 +464,14 @@ def test_speculator_variants_match_oracle(draft, ab):
         ours = eng.step([0])[0]
         ref, det = o.step(st)
         n = len(det["cands"].token)
+        if draft == "clover":
+            F, base = 1, 0
+            for j in range(1, cfg.n_spec_heads + 1):
+                dl = eng.debug(f"draft_logits{j}", np.float32, (F, cfg.vocab))
+                for f in range(F):
+                    assert np.max(np.abs(dl[f] - det["cands"].row_logits[base + f])) < 1e-4, (step, j, f)
+                base += F
+                F *= cfg.topk[j - 1]
         assert np.array_equal(eng.debug("cand_token", np.int32, (1, n))[0], det["cands"].token), step
         assert np.array_equal(eng.debug("tree_token", np.int32, (1, T))[0], det["tree"].tokens), step
         vl = eng.debug("verify_logits", np.float32, (T, cfg.vocab))
