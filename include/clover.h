@@ -107,6 +107,8 @@ typedef struct {
   int32_t draft_mode;   /* clover_draft_mode */
   int32_t ab_mode;      /* clover_ab_mode */
   int32_t ad_keys;      /* clover_ad_keys (Clover draft) */
+  int32_t ad_per_head;  /* 0: one Attention Decoder shared by all heads (Eq. 1 has no head
+                           index); 1: one per head (weights ad{j}.* for depth j + 1) */
 } clover_config;
 
 #define CLOVER_FLAG_KEEP_LOGITS 1 /* keep draft and verify logits of the last step readable */
@@ -128,7 +130,8 @@ clover_status clover_check_config(const clover_config* cfg);
  * The ab.* tensors are the Augmenting Block (Sec. 3.3), ad.* the Attention Decoder
  * (Sec. 3.2, Eq. 1-2), head{j}.* the per-head MLP layers; lm_head is shared by all
  * heads and supplies the Regressive Connection embeddings (Sec. 3.4).  With
- * CLOVER_DRAFT_MEDUSA the ad.* entries are left out; the ab.* entries are those of the
+ * CLOVER_DRAFT_MEDUSA the ad.* entries are left out; with ad_per_head they are
+ * ad{j}.{norm,wq,wk,wv,wo} for each head j instead of one ad.* set; the ab.* entries are those of the
  * Augmenting Block's halves that clover_ab_mode keeps (attn_norm, wq, wk, wv, wo for the
  * attention half, mlp_norm, w_gate, w_up, w_down for the MLP half). */
 size_t clover_weight_count(const clover_config* cfg);

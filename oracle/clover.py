@@ -221,7 +221,14 @@ class CloverOracle:
         r = head_mlp(s, self.w[f"head{j}.w1"], self.w[f"head{j}.b1"], self.prec)
         return self.base.logits(r[None, :])[0]
 
-    def ad_keys(self, h: np.ndarray, n: int, token, parent) -> np.ndarray:
+    def decoder_weights(self, j: int) -> Dict[str, np.ndarray]:
+        """The Attention Decoder that drafts depth j: the shared ad.* set (Eq. 1 has no head
+        index), or head j's own ad{j-1}.* set when the configuration gives each head one."""
+        if not getattr(self.cfg, "ad_per_head", False):
+            return self.w
+        return {f"ad.{f}": self.w[f"ad{j - 1}.{f}"] for f in ("norm", "wq", "wk", "wv", "wo")}
+
+    def ad_keys(self, h: np.ndarray, n: int, token, parent, wad) -> np.ndarray:
         """Key/value inputs of the Attention Decoder for node n with state h (Eq. 1; the key
         set is a reading): "single" {e(token_n)}; "two" {RMSNorm_ad(h), e(token_n)} (Sec. 3.2:
         two vectors per request or beam); "path" {e(t) for every token on n's root path,
@@ -231,7 +238,7 @@ class CloverOracle:
         if kind == "single":
             return e[None, :]
         if kind == "two":
-            a = self.prec.store(rmsnorm(h, self.w["ad.norm"], self.cfg.rms_eps))
+            a = self.prec.store(rmsnorm(h, wad["ad.norm"], self.cfg.rms_eps))
             return np.stack([a, e])
         path = []
         while n >= 0:
@@ -247,8 +254,9 @@ class CloverOracle:
         out = Candidates(depth=None, token=None, parent=None, lp=None)
         for j in range(1, c.n_spec_heads + 1):
             frontier = [i for i in range(len(depth)) if depth[i] == j - 1]
+            wad = self.decoder_weights(j)
             for n in frontier:
-                s = attention_decoder(state[n], self.ad_keys(state[n], n, token, parent), self.w,
+                s = attention_decoder(state[n], self.ad_keys(state[n], n, token, parent, wad), wad,
                                       c.n_heads, c.head_dim, c.rms_eps, self.prec)
                 logits = self.head_logits(j - 1, s)
                 logp = logits - logsumexp(logits)

@@ -83,12 +83,15 @@ std::vector<WSpec> weight_specs(const clover_config& c) {
   s.push_back({"final_norm", d, 0, false});
   s.push_back({"lm_head", V, d, true});
   if (has_ab(c)) layer_specs(c, "ab", s, ab_attn(c), ab_mlp(c));
-  if (!is_medusa(c)) {
-    s.push_back({"ad.norm", d, 0, false});
-    s.push_back({"ad.wq", qd, d, true});
-    s.push_back({"ad.wk", qd, d, true});
-    s.push_back({"ad.wv", qd, d, true});
-    s.push_back({"ad.wo", d, qd, true});
+  if (!is_medusa(c)) {  // ad.* shared, or ad{j}.* per head
+    for (int j = 0; j < (c.ad_per_head ? c.n_spec_heads : 1); ++j) {
+      const std::string pre = c.ad_per_head ? "ad" + std::to_string(j) : std::string("ad");
+      s.push_back({pre + ".norm", d, 0, false});
+      s.push_back({pre + ".wq", qd, d, true});
+      s.push_back({pre + ".wk", qd, d, true});
+      s.push_back({pre + ".wv", qd, d, true});
+      s.push_back({pre + ".wo", d, qd, true});
+    }
   }
   for (int j = 0; j < c.n_spec_heads; ++j) {
     s.push_back({"head" + std::to_string(j) + ".w1", d, d, true});
@@ -129,6 +132,7 @@ bool check_config(const clover_config* c, std::string& why) {
     return fail("draft_mode must be CLOVER_DRAFT_CLOVER or CLOVER_DRAFT_MEDUSA");
   if (c->ab_mode < CLOVER_AB_DEFAULT || c->ab_mode > CLOVER_AB_NONE) return fail("ab_mode out of range");
   if (c->ad_keys < CLOVER_AD_KEYS_SINGLE || c->ad_keys > CLOVER_AD_KEYS_PATH) return fail("ad_keys out of range");
+  if (c->ad_per_head != 0 && c->ad_per_head != 1) return fail("ad_per_head must be 0 or 1");
   const int kc = kc_of(c->dtype);
   if (c->n_layers < 1 || c->n_layers > 1024) return fail("n_layers out of range");
   if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128) return fail("head_dim must be 32, 64 or 128");
@@ -308,7 +312,9 @@ struct clover_ctx {
   char* ws;
   std::vector<const void*> w;
   std::vector<LayerPtrs> layers;  // n_layers (+ Augmenting Block last, Clover draft)
-  const void *emb, *final_norm, *lm_head, *ad_norm, *ad_wq, *ad_wk, *ad_wv, *ad_wo;
+  const void *emb, *final_norm, *lm_head;
+  struct AdPtrs { const void *norm, *wq, *wk, *wv, *wo; };
+  std::vector<AdPtrs> ad;  // one Attention Decoder shared by the heads, or one per head
   std::vector<const void*> head_w1, head_b1;
   // host state
   std::vector<int> seq_len;                  // -1 inactive
@@ -756,7 +762,8 @@ hipError_t enq_draft(clover_ctx* c, int B) {
     ap.seq_ids = ids; ap.nbatch = B; ap.F = F;
     ap.cand_token = ct; ap.cand_stride = L.NC; ap.base_node = depth_base(cf, j - 1);
     ap.lm_packed = c->lm_head; ap.lm_nchunks = d / kc_of(cf.dtype);
-    ap.ad_norm = c->ad_norm; ap.eps = cf.rms_eps; ap.d = d;
+    const clover_ctx::AdPtrs& adw = c->ad[cf.ad_per_head ? j - 1 : 0];
+    ap.ad_norm = adw.norm; ap.eps = cf.rms_eps; ap.d = d;
     // with the two-token key set the embeddings follow the normalised states in one [2M][d]
     // block, so one K|V GEMM projects both
     const bool two = cf.ad_keys == CLOVER_AD_KEYS_TWO;
@@ -768,11 +775,11 @@ hipError_t enq_draft(clover_ctx* c, int B) {
     int sq = 0, skv = 0, so = 0, sh = 0;
     GemmParams q{};
     q.X = c->at<void>(L.d_a); q.ldx = d; q.mode = EP_PARTIAL; q.max_splits = GEMM_MAX_SPLITS; q.part = part;
-    HE(run_gemm(c, q, M, d, {{c->ad_wq, qd}}, &sq));
+    HE(run_gemm(c, q, M, d, {{adw.wq, qd}}, &sq));
     GemmParams kv{};
     kv.X = two ? c->at<void>(L.d_a) : c->at<void>(L.d_e); kv.ldx = d; kv.mode = EP_PARTIAL;
     kv.max_splits = GEMM_MAX_SPLITS; kv.part = part2;
-    HE(run_gemm(c, kv, two ? 2 * M : M, d, {{c->ad_wk, qd}, {c->ad_wv, qd}}, &skv));
+    HE(run_gemm(c, kv, two ? 2 * M : M, d, {{adw.wk, qd}, {adw.wv, qd}}, &skv));
     AdAttnParams aa{};
     aa.q = part; aa.Sq = sq; aa.kv = part2; aa.Skv = skv;
     aa.M = M; aa.F = F; aa.n_heads = cf.n_heads; aa.hd = cf.head_dim;
@@ -794,7 +801,7 @@ hipError_t enq_draft(clover_ctx* c, int B) {
     HE(launch_ad_attn(cf.dtype, aa, c->st));
     GemmParams o{};
     o.X = c->at<void>(L.d_o); o.ldx = qd; o.mode = EP_PARTIAL; o.max_splits = GEMM_MAX_SPLITS; o.part = part;
-    HE(run_gemm(c, o, M, qd, {{c->ad_wo, d}}, &so));
+    HE(run_gemm(c, o, M, qd, {{adw.wo, d}}, &so));
     RowFixParams rs{};  // s = h + W_O attn (Eq. 2): fp32 state and storage copy for the MLP
     rs.M = M; rs.d = d; rs.part = part; rs.S = so; rs.ldp = d;
     rs.resid = c->at<float>(L.d_hin); rs.ldr = d;
@@ -944,7 +951,11 @@ clover_status clover_pack_weight(const clover_config* cfg, size_t i, const void*
   hipStream_t st = (hipStream_t)hip_stream;
   hipError_t e;
   const std::string& nm = s[i].name;
-  const bool qk = nm.rfind("ad.", 0) != 0 && nm.size() > 3 &&
+  // Q/K projections of the target and Augmenting Block layers carry rotary (tile-local
+  // rotary packing); the Attention Decoder's (ad.* or ad{j}.*) do not
+  const bool decoder = nm.size() > 3 && nm.compare(0, 2, "ad") == 0 &&
+                       (nm[2] == '.' || (nm[2] >= '0' && nm[2] <= '9'));
+  const bool qk = !decoder && nm.size() > 3 &&
                   (nm.compare(nm.size() - 3, 3, ".wq") == 0 || nm.compare(nm.size() - 3, 3, ".wk") == 0);
   if (s[i].matrix)
     e = launch_pack(cfg->dtype, src, (int)s[i].rows, (int)s[i].cols, dst, qk ? cfg->head_dim : 0, st);
@@ -1006,7 +1017,11 @@ clover_status clover_init(const clover_config* cfg, void* const* weights, void* 
     c->layers.push_back(p);
   }
   if (!is_medusa(*cfg)) {
-    c->ad_norm = c->w[k++]; c->ad_wq = c->w[k++]; c->ad_wk = c->w[k++]; c->ad_wv = c->w[k++]; c->ad_wo = c->w[k++];
+    for (int j = 0; j < (cfg->ad_per_head ? cfg->n_spec_heads : 1); ++j) {
+      clover_ctx::AdPtrs a;
+      a.norm = c->w[k++]; a.wq = c->w[k++]; a.wk = c->w[k++]; a.wv = c->w[k++]; a.wo = c->w[k++];
+      c->ad.push_back(a);
+    }
   }
   for (int j = 0; j < cfg->n_spec_heads; ++j) {
     c->head_w1.push_back(c->w[k++]);

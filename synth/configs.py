@@ -36,6 +36,7 @@ class CloverConfig:
     ab: str = "default"
     # key set of the Attention Decoder: "single" {e}, "two" {RMSNorm(h), e}, "path" {e_0..}
     ad_keys: str = "single"
+    ad_per_head: bool = False  # one Attention Decoder per head instead of one shared
 
     @property
     def ab_kind(self) -> str:

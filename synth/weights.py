@@ -33,10 +33,11 @@ def weight_specs(c: CloverConfig) -> List[Tuple[str, Tuple[int, ...]]]:
     specs += [("final_norm", (d,)), ("lm_head", (V, d))]
     if c.ab_kind != "none":  # the Augmenting Block's halves
         specs += _layer_specs("ab", c, attn=c.ab_kind in ("full", "attn"), mlp=c.ab_kind in ("full", "mlp"))
-    if c.draft != "medusa":  # Attention Decoder: Clover heads only
+    if c.draft != "medusa":  # Attention Decoder: Clover heads only; shared, or one per head
         qd = c.n_heads * c.head_dim
-        specs += [("ad.norm", (d,)), ("ad.wq", (qd, d)), ("ad.wk", (qd, d)), ("ad.wv", (qd, d)),
-                  ("ad.wo", (d, qd))]
+        for pre in ([f"ad{j}" for j in range(c.n_spec_heads)] if c.ad_per_head else ["ad"]):
+            specs += [(f"{pre}.norm", (d,)), (f"{pre}.wq", (qd, d)), (f"{pre}.wk", (qd, d)),
+                      (f"{pre}.wv", (qd, d)), (f"{pre}.wo", (d, qd))]
     for j in range(c.n_spec_heads):
         specs += [(f"head{j}.w1", (d, d)), (f"head{j}.b1", (d,))]
     return specs

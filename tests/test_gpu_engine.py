@@ -440,19 +440,21 @@ def test_medusa_bf16_batch_of_three_within_tolerance():
             break
 
 
-@pytest.mark.parametrize("draft,ab,ad_keys", [("clover", "attn", "single"), ("clover", "mlp", "single"),
-                                              ("clover", "none", "single"), ("medusa", "full", "single"),
-                                              ("clover", "default", "two"), ("clover", "default", "path")])
-def test_speculator_variants_match_oracle(draft, ab, ad_keys):
+@pytest.mark.parametrize("draft,ab,ad_keys,per_head", [
+    ("clover", "attn", "single", False), ("clover", "mlp", "single", False),
+    ("clover", "none", "single", False), ("medusa", "full", "single", False),
+    ("clover", "default", "two", False), ("clover", "default", "path", False),
+    ("clover", "default", "two", True)])
+def test_speculator_variants_match_oracle(draft, ab, ad_keys, per_head):
     """The Augmenting Block variants of Sec. 4.4 (attention half, MLP half, none) under the
     Clover draft, the Augmenting Block feeding parallel heads (Clover without Attention
     Decoder and Regressive Connection), and the two-token and root-path key sets of the
-    Attention Decoder: tiny fp32, six steps, draft logits of every frontier row and verify
-    logits within 1e-4, candidate and verify trees exact, tokens equal to the oracle's and
-    to greedy decoding."""
+    Attention Decoder, and one decoder per head: tiny fp32, six steps, draft logits of every
+    frontier row and verify logits within 1e-4, candidate and verify trees exact, tokens
+    equal to the oracle's and to greedy decoding."""
     P = need_gpu()
-    note(f"engine variant draft={draft} ab={ab} ad_keys={ad_keys}")
-    cfg = synth.get_config("tiny_fp32").with_(draft=draft, ab=ab, ad_keys=ad_keys)
+    note(f"engine variant draft={draft} ab={ab} ad_keys={ad_keys} per_head={per_head}")
+    cfg = synth.get_config("tiny_fp32").with_(draft=draft, ab=ab, ad_keys=ad_keys, ad_per_head=per_head)
     w = synth.make_weights(cfg, seed=1, perturb=True)
     eng = _engine(P, cfg, w)
     o = oracle.make_oracle(cfg, w)

@@ -74,3 +74,27 @@ def test_key_sets_keep_greedy_output(ad_keys, seed):
     prompt = synth.make_prompt(cfg, seq=seed, n=12)
     spec, _ = o.generate(prompt, 14)
     assert spec == o.base.greedy_generate(prompt, 14)
+
+
+def test_per_head_decoders_with_equal_weights_draft_like_the_shared_one():
+    """Reading A6: one Attention Decoder shared by the heads, or one per head.  Per-head
+    decoders whose weights all equal the shared decoder's draft exactly what the shared
+    one drafts; giving head 2 its own weights changes depth 2 and leaves depth 1 alone."""
+    cfg, w, o = _make("two", seed=6)
+    cph = cfg.with_(ad_per_head=True)
+    wph = {k: v for k, v in w.items() if not k.startswith("ad.")}
+    for j in range(cfg.n_spec_heads):
+        for f in ("norm", "wq", "wk", "wv", "wo"):
+            wph[f"ad{j}.{f}"] = w[f"ad.{f}"]
+    assert sorted(wph) == sorted(n for n, _ in synth.weight_specs(cph))
+    prompt = synth.make_prompt(cfg, n=9)
+    a = o.draft(o.prefill(prompt))
+    oph = CloverOracle(cph, wph)
+    b = oph.draft(oph.prefill(prompt))
+    for f in ("token", "parent", "lp"):
+        assert np.array_equal(getattr(a, f), getattr(b, f))
+    wph["ad1.wv"] = wph["ad1.wv"] * 2.0
+    oph2 = CloverOracle(cph, wph)
+    c = oph2.draft(oph2.prefill(prompt))
+    assert np.array_equal(c.row_logits[0], a.row_logits[0])            # depth 1: decoder ad0
+    assert not np.allclose(c.row_logits[1], a.row_logits[1])           # depth 2: decoder ad1
