@@ -773,15 +773,23 @@ hipError_t enq_draft(clover_ctx* c, int B) {
     float* part = c->at<float>(L.gpart);
     float* part2 = c->at<float>(L.gpart2);
     int sq = 0, skv = 0, so = 0, sh = 0;
-    GemmParams q{};
-    q.X = c->at<void>(L.d_a); q.ldx = d; q.mode = EP_PARTIAL; q.max_splits = GEMM_MAX_SPLITS; q.part = part;
-    HE(run_gemm(c, q, M, d, {{adw.wq, qd}}, &sq));
+    // With the single key (Eq. 1 read literally) the softmax weight is exactly 1, so the
+    // decoder's output is W_V e: the Q and K projections cannot change it and are skipped.
+    const bool values_only = cf.ad_keys == CLOVER_AD_KEYS_SINGLE;
+    if (!values_only) {
+      GemmParams q{};
+      q.X = c->at<void>(L.d_a); q.ldx = d; q.mode = EP_PARTIAL; q.max_splits = GEMM_MAX_SPLITS; q.part = part;
+      HE(run_gemm(c, q, M, d, {{adw.wq, qd}}, &sq));
+    }
     GemmParams kv{};
     kv.X = two ? c->at<void>(L.d_a) : c->at<void>(L.d_e); kv.ldx = d; kv.mode = EP_PARTIAL;
     kv.max_splits = GEMM_MAX_SPLITS; kv.part = part2;
-    HE(run_gemm(c, kv, two ? 2 * M : M, d, {{adw.wk, qd}, {adw.wv, qd}}, &skv));
+    if (values_only)
+      HE(run_gemm(c, kv, M, d, {{adw.wv, qd}}, &skv));
+    else
+      HE(run_gemm(c, kv, two ? 2 * M : M, d, {{adw.wk, qd}, {adw.wv, qd}}, &skv));
     AdAttnParams aa{};
-    aa.q = part; aa.Sq = sq; aa.kv = part2; aa.Skv = skv;
+    aa.q = part; aa.Sq = sq; aa.kv = part2; aa.Skv = skv; aa.values_only = values_only;
     aa.M = M; aa.F = F; aa.n_heads = cf.n_heads; aa.hd = cf.head_dim;
     aa.keys = cf.ad_keys; aa.depth = j - 1; aa.out = c->at<void>(L.d_o);
     if (cf.ad_keys == CLOVER_AD_KEYS_PATH) {

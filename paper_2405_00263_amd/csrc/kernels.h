@@ -172,6 +172,10 @@ enum AdKeys : int { AD_KEYS_SINGLE = 0, AD_KEYS_TWO = 1, AD_KEYS_PATH = 2 };
 struct AdAttnParams {
   const float* q; int Sq;
   const float* kv; int Skv;
+  // AD_KEYS_SINGLE only: kv holds values alone, [Skv][M][H*hd], and q is unused.  With one
+  // key the softmax weight is exactly 1 and the output is the value, so the query and key
+  // projections are not computed.
+  int values_only;
   int M, F, n_heads, hd, keys, depth;
   float* kv_path;                 // AD_KEYS_PATH: [sum_d B*nodes(d)][2*H*hd] fp32
   int kv_path_off[8], path_nodes[8], anc_div[8];

@@ -180,51 +180,74 @@ hipError_t launch_argmax(const float* logits, int M, int V, int* out, unsigned l
 }
 
 // ---- top-k with log-softmax, two stages ---------------------------------------------------
-// Stage 1: each (row, chunk) workgroup finds its chunk's k best (value desc, index asc)
-// by k rounds of block argmax over register-resident elements, and the chunk's
-// (max, sum exp(x - max)).  Stage 2: one workgroup per row merges the chunk lists the
-// same way and combines the chunk sums in chunk order into the log-sum-exp.
+// Stage 1: each (row, chunk) workgroup finds its chunk's k best (value desc, index asc) and
+// the chunk's (max, sum exp(x - max)).  Stage 2: one workgroup per row merges the chunk
+// lists the same way and combines the chunk sums in chunk order into the log-sum-exp.
+// Both stages select inside each wave first (k rounds of a wave-wide argmax over register-
+// resident candidates, no barrier), then one wave selects among the waves' lists, so a
+// stage costs two barriers whatever k is.
 static constexpr int KMAX = 16;
 static constexpr int TOPK_EPT = 16;  // elements per thread in stage 1
 static constexpr int TOPK_S2 = 4;    // candidates per thread in stage 2
+static constexpr int TOPK_WAVES = RED_THREADS / 64;
+static_assert(TOPK_WAVES * KMAX <= 64, "one candidate per lane when the waves' lists merge");
 
-__device__ void block_best(float& v, int& i, float* sv, int* si) {
-  for (int o = 32; o > 0; o >>= 1) {
-    const float ov = __shfl_xor(v, o);
-    const int oi = __shfl_xor(i, o);
-    if (better(ov, oi, v, i)) { v = ov; i = oi; }
+// The k best of the wave's candidates (each lane holds N, index INT_MAX = empty) into
+// res_v/res_i[0..k) (written by lane 0), best first.  The candidates taken are emptied.
+template <int N>
+__device__ __forceinline__ void wave_topk(float (&v)[N], int (&ix)[N], int k, float* res_v, int* res_i) {
+  for (int r = 0; r < k; ++r) {
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+#pragma unroll
+    for (int u = 0; u < N; ++u)
+      if (better(v[u], ix[u], bv, bi)) { bv = v[u]; bi = ix[u]; }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(bv, o);
+      const int oi = __shfl_xor(bi, o);
+      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+    }
+    if ((threadIdx.x & 63) == 0) { res_v[r] = bv; res_i[r] = bi; }
+#pragma unroll
+    for (int u = 0; u < N; ++u)
+      if (ix[u] == bi && bi != 0x7fffffff) { v[u] = -INFINITY; ix[u] = 0x7fffffff; }
   }
-  const int w = threadIdx.x >> 6;
-  __syncthreads();
-  if ((threadIdx.x & 63) == 0) { sv[w] = v; si[w] = i; }
-  __syncthreads();
-  v = sv[0]; i = si[0];
-  for (int q = 1; q < RED_THREADS / 64; ++q)
-    if (better(sv[q], si[q], v, i)) { v = sv[q]; i = si[q]; }
+}
+
+// Lists of the workgroup's waves (s_v/s_i [TOPK_WAVES][KMAX]) merged by wave 0 into
+// res_v/res_i[0..k).
+__device__ __forceinline__ void merge_wave_lists(int k, const float* s_v, const int* s_i, float* res_v,
+                                                 int* res_i) {
+  if (threadIdx.x >= 64) return;
+  const int lane = threadIdx.x, w = lane / KMAX, r = lane % KMAX;
+  float v[1] = {(w < TOPK_WAVES && r < k) ? s_v[w * KMAX + r] : -INFINITY};
+  int ix[1] = {(w < TOPK_WAVES && r < k) ? s_i[w * KMAX + r] : 0x7fffffff};
+  wave_topk<1>(v, ix, k, res_v, res_i);
 }
 
 __global__ __launch_bounds__(RED_THREADS) void topk_stage1_kernel(const float* __restrict__ logits, int V, int k,
                                                                    int nch, float* __restrict__ pv,
                                                                    int* __restrict__ pi, float* __restrict__ pms) {
-  __shared__ float sv[RED_THREADS / 64], sred[RED_THREADS / 64];
-  __shared__ int si[RED_THREADS / 64];
+  __shared__ float sred[RED_THREADS / 64];
+  __shared__ float s_v[TOPK_WAVES * KMAX];
+  __shared__ int s_i[TOPK_WAVES * KMAX];
   const int m = blockIdx.x, ch = blockIdx.y;
   const int per = (V + nch - 1) / nch;
   const int c0 = ch * per, c1 = min(V, c0 + per);
   const float* row = logits + (size_t)m * V;
   float v[TOPK_EPT];
-  uint32_t taken = 0u;
+  int ix[TOPK_EPT];
   float mx = -INFINITY;
 #pragma unroll
   for (int u = 0; u < TOPK_EPT; ++u) {
     const int i = c0 + threadIdx.x + u * RED_THREADS;
     v[u] = i < c1 ? row[i] : -INFINITY;
+    ix[u] = i < c1 ? i : 0x7fffffff;
+    mx = fmaxf(mx, v[u]);
   }
-#pragma unroll
-  for (int u = 0; u < TOPK_EPT; ++u) mx = fmaxf(mx, v[u]);
   // chunk max and sum of exponentials
-  float bm = mx;
-  for (int o = 32; o > 0; o >>= 1) bm = fmaxf(bm, __shfl_xor(bm, o));
+  float bm = warp_max(mx);
   const int w = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) sred[w] = bm;
   __syncthreads();
@@ -234,6 +257,8 @@ __global__ __launch_bounds__(RED_THREADS) void topk_stage1_kernel(const float* _
 #pragma unroll
   for (int u = 0; u < TOPK_EPT; ++u) se += (v[u] == -INFINITY) ? 0.f : expf(v[u] - cmax);
   se = warp_sum(se);
+  // the wave's k best, then the chunk's from the waves' lists
+  wave_topk<TOPK_EPT>(v, ix, k, s_v + w * KMAX, s_i + w * KMAX);
   __syncthreads();
   if ((threadIdx.x & 63) == 0) sred[w] = se;
   __syncthreads();
@@ -243,32 +268,15 @@ __global__ __launch_bounds__(RED_THREADS) void topk_stage1_kernel(const float* _
     pms[((size_t)m * nch + ch) * 2] = cmax;
     pms[((size_t)m * nch + ch) * 2 + 1] = tot;
   }
-  // k rounds of block argmax; the owner of the winner masks it out
-  for (int r = 0; r < k; ++r) {
-    float bv = -INFINITY;
-    int bi = 0x7fffffff;
-#pragma unroll
-    for (int u = 0; u < TOPK_EPT; ++u) {
-      const int i = c0 + threadIdx.x + u * RED_THREADS;
-      if (i < c1 && !((taken >> u) & 1u) && better(v[u], i, bv, bi)) { bv = v[u]; bi = i; }
-    }
-    block_best(bv, bi, sv, si);  // bi == INT_MAX: the chunk has fewer than k elements
-    if (threadIdx.x == 0) {
-      pv[((size_t)m * nch + ch) * k + r] = bv;
-      pi[((size_t)m * nch + ch) * k + r] = bi;
-    }
-#pragma unroll
-    for (int u = 0; u < TOPK_EPT; ++u)
-      if (c0 + (int)threadIdx.x + u * RED_THREADS == bi) taken |= 1u << u;
-  }
+  merge_wave_lists(k, s_v, s_i, pv + ((size_t)m * nch + ch) * k, pi + ((size_t)m * nch + ch) * k);
 }
 
 __global__ __launch_bounds__(RED_THREADS) void topk_stage2_kernel(const TopkParams p, int nch,
                                                                    const float* __restrict__ pv,
                                                                    const int* __restrict__ pi,
                                                                    const float* __restrict__ pms) {
-  __shared__ float sv[RED_THREADS / 64];
-  __shared__ int si[RED_THREADS / 64];
+  __shared__ float s_v[TOPK_WAVES * KMAX];
+  __shared__ int s_i[TOPK_WAVES * KMAX];
   __shared__ float res_v[KMAX];
   __shared__ int res_i[KMAX];
   __shared__ float s_lse;
@@ -292,18 +300,10 @@ __global__ __launch_bounds__(RED_THREADS) void topk_stage2_kernel(const TopkPara
     }
     s_lse = M + logf(S);
   }
-  for (int r = 0; r < k; ++r) {
-    float bv = -INFINITY;
-    int bi = 0x7fffffff;
-#pragma unroll
-    for (int u = 0; u < TOPK_S2; ++u)
-      if (better(cv[u], ci[u], bv, bi)) { bv = cv[u]; bi = ci[u]; }
-    block_best(bv, bi, sv, si);
-    if (threadIdx.x == 0) { res_v[r] = bv; res_i[r] = bi; }
-#pragma unroll
-    for (int u = 0; u < TOPK_S2; ++u)
-      if (ci[u] == bi) { cv[u] = -INFINITY; ci[u] = 0x7fffffff; }
-  }
+  const int w = threadIdx.x >> 6;
+  wave_topk<TOPK_S2>(cv, ci, k, s_v + w * KMAX, s_i + w * KMAX);
+  __syncthreads();
+  merge_wave_lists(k, s_v, s_i, res_v, res_i);
   __syncthreads();
   if (threadIdx.x < k) {
     const int r = threadIdx.x;
@@ -561,6 +561,17 @@ template <typename S>
 __global__ __launch_bounds__(64) void ad_attn_kernel(const AdAttnParams p) {
   const int f = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
   const int qd = p.n_heads * p.hd, M = p.M, hd = p.hd;
+  if (p.values_only) {  // one key: the output is its value (weight exactly 1)
+#pragma unroll
+    for (int u = 0; u < AD_DPL; ++u) {
+      const int i = lane + 64 * u;
+      if (i >= hd) continue;
+      float v = 0.f;
+      for (int s = 0; s < p.Skv; ++s) v += p.kv[((size_t)s * M + f) * qd + h * hd + i];
+      reinterpret_cast<S*>(p.out)[(size_t)f * qd + h * hd + i] = St<S>::from_f(v);
+    }
+    return;
+  }
   const int kvrows = p.keys == AD_KEYS_TWO ? 2 * M : M;
   // split-K sum of one key/value row of the K|V GEMM for this lane's dims
   auto sum_kv = [&](int row, float* k, float* v) {
@@ -656,6 +667,7 @@ hipError_t launch_ad_attn(int dtype, const AdAttnParams& p, hipStream_t st) {
   if (p.hd > 64 * AD_DPL || p.keys < 0 || p.keys > AD_KEYS_PATH) return hipErrorInvalidValue;
   if (p.keys == AD_KEYS_PATH && (p.depth < 0 || p.depth >= AD_MAX_KEYS - 1 || p.depth >= 8 || !p.kv_path))
     return hipErrorInvalidValue;
+  if (p.values_only && p.keys != AD_KEYS_SINGLE) return hipErrorInvalidValue;
   dim3 grid(p.M, p.n_heads);
   if (dtype == 1)
     hipLaunchKernelGGL(ad_attn_kernel<bf16_t>, grid, dim3(64), 0, st, p);
