@@ -109,6 +109,14 @@ typedef struct {
   int32_t ad_keys;      /* clover_ad_keys (Clover draft) */
   int32_t ad_per_head;  /* 0: one Attention Decoder shared by all heads (Eq. 1 has no head
                            index); 1: one per head (weights ad{j}.* for depth j + 1) */
+  float temperature;    /* 0: greedy decoding (the target's argmax, Sec. 2.1).  > 0: the target
+                           samples its next token from softmax(logits / temperature) at the
+                           prompt's end and at every tree node (Gumbel-max over Philox4x32-10
+                           draws, counter (token id, tree node, step of the sequence, slot), key
+                           (sample_seed, 0 for tree nodes / 1 for the prompt's end)); acceptance
+                           follows the child carrying the node's sample, so every emitted token
+                           is a sample of the target given the tokens before it */
+  uint32_t sample_seed;
 } clover_config;
 
 #define CLOVER_FLAG_KEEP_LOGITS 1 /* keep draft and verify logits of the last step readable */

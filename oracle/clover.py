@@ -35,6 +35,7 @@ from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
 
+from . import sampling
 from .model import BaseModel, LayerWeights, Precision, layer_forward, logsumexp, rmsnorm, silu
 
 
@@ -169,6 +170,8 @@ class SeqState:
     ab_kv: Optional[Tuple[np.ndarray, np.ndarray]]     # Augmenting Block cache (None: no attention)
     h0: np.ndarray                                     # AB output at position L-1
     t0: int                                            # next token (root of the next tree)
+    slot: int = 0                                      # sequence slot (sampling counters)
+    steps: int = 0                                     # speculate-and-verify steps committed
 
     @property
     def L(self) -> int:
@@ -207,14 +210,22 @@ class CloverOracle:
                              self.prec, attn=attn, mlp=self.ab_kind in ("full", "mlp"))
 
     # -- prefill (Sec. 1: the prompt is processed in one pass and yields the first token) ---
-    def prefill(self, prompt: Sequence[int]) -> SeqState:
+    # -- the target's choice of token: greedy argmax, or a sample (oracle/sampling.py) -----
+    def target_token(self, logits: np.ndarray, domain: int, step: int, slot: int, node: int) -> int:
+        tau = float(getattr(self.cfg, "temperature", 0.0))
+        if tau <= 0.0:
+            return int(np.argmax(logits))
+        return sampling.sample_token(logits, tau, int(getattr(self.cfg, "sample_seed", 0)), domain, step,
+                                     slot, node)
+
+    def prefill(self, prompt: Sequence[int], slot: int = 0) -> SeqState:
         n = len(prompt)
         causal = np.tril(np.ones((n, n), dtype=bool))
         x, kv = self.base.forward_rows(prompt, np.arange(n), None, causal)
-        t0 = int(np.argmax(self.base.logits(x[-1:])[0]))
+        t0 = self.target_token(self.base.logits(x[-1:])[0], sampling.DOMAIN_PREFILL, 0, slot, 0)
         h, k, v = self.ab_forward(x, np.arange(n), self.base.empty_kv(), causal)
         return SeqState(tokens=list(prompt), kv=kv, ab_kv=None if k is None else (k, v),
-                        h0=h[-1].copy(), t0=t0)
+                        h0=h[-1].copy(), t0=t0, slot=slot)
 
     # -- drafting (Sec. 3) ---------------------------------------------------------------
     def head_logits(self, j: int, s: np.ndarray) -> np.ndarray:
@@ -278,7 +289,13 @@ class CloverOracle:
     def verify(self, st: SeqState, tree: Tree) -> VerifyOut:
         x, kv = self.base.forward_rows(tree.tokens, tree.pos, st.kv, tree.mask)
         logits = self.base.logits(x)
-        return VerifyOut(logits=logits, target=np.argmax(logits, axis=1), x_last=x, kv=kv)
+        tau = float(getattr(self.cfg, "temperature", 0.0))
+        if tau > 0.0:  # node i's draw: counter (token, i, steps of the sequence, slot)
+            target = sampling.sample_tokens(logits, tau, int(getattr(self.cfg, "sample_seed", 0)),
+                                            sampling.DOMAIN_VERIFY, st.steps, st.slot, np.arange(len(logits)))
+        else:
+            target = np.argmax(logits, axis=1)
+        return VerifyOut(logits=logits, target=target, x_last=x, kv=kv)
 
     # -- commit: compaction of the accepted KV entries and the Augmenting Block ------------
     def commit(self, st: SeqState, tree: Tree, ver: VerifyOut, acc: List[int], bonus: int):
@@ -293,6 +310,7 @@ class CloverOracle:
         st.h0 = h[-1].copy()
         st.tokens.extend(int(t) for t in tree.tokens[acc])
         st.t0 = bonus
+        st.steps += 1
 
     def step_tree(self, st: SeqState, tree: Tree):
         """Verify a given tree, accept, commit.  Returns (emitted, acc, verify output)."""

@@ -41,7 +41,8 @@ class ConfigC(ctypes.Structure):
                 ("max_context", ctypes.c_int32), ("kv_block", ctypes.c_int32),
                 ("prefill_chunk", ctypes.c_int32), ("flags", ctypes.c_int32),
                 ("draft_mode", ctypes.c_int32), ("ab_mode", ctypes.c_int32),
-                ("ad_keys", ctypes.c_int32), ("ad_per_head", ctypes.c_int32)]
+                ("ad_keys", ctypes.c_int32), ("ad_per_head", ctypes.c_int32),
+                ("temperature", ctypes.c_float), ("sample_seed", ctypes.c_uint32)]
 
 
 class TimingsC(ctypes.Structure):
@@ -139,6 +140,8 @@ def make_config(cfg, max_batch: Optional[int] = None, max_context: Optional[int]
     c.ab_mode = AB_MODES[getattr(cfg, "ab", "default")]
     c.ad_keys = AD_KEYS[getattr(cfg, "ad_keys", "single")]
     c.ad_per_head = int(bool(getattr(cfg, "ad_per_head", False)))
+    c.temperature = float(getattr(cfg, "temperature", 0.0))
+    c.sample_seed = int(getattr(cfg, "sample_seed", 0)) & 0xFFFFFFFF
     return c
 
 

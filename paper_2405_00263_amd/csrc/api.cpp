@@ -133,6 +133,7 @@ bool check_config(const clover_config* c, std::string& why) {
   if (c->ab_mode < CLOVER_AB_DEFAULT || c->ab_mode > CLOVER_AB_NONE) return fail("ab_mode out of range");
   if (c->ad_keys < CLOVER_AD_KEYS_SINGLE || c->ad_keys > CLOVER_AD_KEYS_PATH) return fail("ad_keys out of range");
   if (c->ad_per_head != 0 && c->ad_per_head != 1) return fail("ad_per_head must be 0 or 1");
+  if (!(c->temperature >= 0.f) || c->temperature > 1e30f) return fail("temperature must be finite and >= 0");
   const int kc = kc_of(c->dtype);
   if (c->n_layers < 1 || c->n_layers > 1024) return fail("n_layers out of range");
   if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128) return fail("head_dim must be 32, 64 or 128");
@@ -165,6 +166,7 @@ struct Layout {
   size_t pool_bytes;
   size_t kpool, vpool, pool_ptrs, block_table, seq_len, seq_ids;
   size_t x, xa, xn, qbuf, obuf, act, vlogits, row_tok, row_pos, row_slot, row_seq, amax;
+  size_t sample_step;  // per slot: speculate-and-verify steps done since its prefill (sampling counters)
   size_t rope_cs;  // [Mmax][hd/2] (cos, sin) of the current rows' positions
   size_t h0, t0, cand_token, cand_parent, cand_depth, cand_lp;
   size_t tree_token, tree_parent, tree_depth, tree_pos, tree_mask, target, acc, acc_len, out_tokens;
@@ -209,6 +211,7 @@ Layout make_layout(const clover_config& c) {
   L.block_table = take(sizeof(int) * (size_t)c.max_batch * L.mbps);
   L.seq_len = take(sizeof(int) * c.max_batch);
   L.seq_ids = take(sizeof(int) * c.max_batch);
+  L.sample_step = take(sizeof(int) * c.max_batch);  // zeroed at init with the state
   L.x = take(4 * (size_t)L.Mmax * d);
   L.xa = take(4 * (size_t)L.Mmax * d);
   L.xn = take((size_t)L.es * L.Mmax * d);
@@ -553,6 +556,20 @@ clover_status ensure_blocks(clover_ctx* c, int slot, int upto) {
     if (e_ != hipSuccess) return e_;    \
   } while (0)
 
+// LM-head argmax keys of the target's choices: plain argmax (greedy), or with temperature a
+// Gumbel-max sample per row (GemmParams::inv_temp).  domain 0: tree nodes (row m is node
+// m % rows_per_seq of sequence slot_of_row[m]); 1: the token after the prompt.
+void set_sampling(clover_ctx* c, GemmParams& lm, uint32_t domain, const int* slot_of_row, int rows_per_seq) {
+  const clover_config& cf = c->cfg;
+  if (!(cf.temperature > 0.f)) return;
+  lm.inv_temp = 1.0f / cf.temperature;
+  lm.samp_seed = cf.sample_seed;
+  lm.samp_domain = domain;
+  lm.samp_slot = slot_of_row;
+  lm.samp_step = c->at<int>(c->L.sample_step);
+  lm.samp_rows = rows_per_seq;
+}
+
 // Verify forward for the batch in seq_ids (tree already in device buffers): all target
 // layers over the tree, final norm, LM head, greedy argmax, then the Augmenting Block
 // over the tree.
@@ -584,6 +601,7 @@ hipError_t enq_verify(clover_ctx* c, int B, int max_keys) {
   lm.X = c->at<void>(L.xn); lm.ldx = d; lm.mode = EP_PARTIAL; lm.max_splits = 1;
   lm.part = c->at<float>(L.vlogits);
   lm.amax_part = c->at<unsigned long long>(L.amax_part);
+  set_sampling(c, lm, 0, c->at<int>(L.row_seq), T);
   int lm_groups = 0;
   HE(run_gemm(c, lm, M, d, {{c->lm_head, cf.vocab}}, nullptr, &lm_groups));
   {
@@ -611,6 +629,7 @@ hipError_t enq_accept(clover_ctx* c, int B) {
   ap.acc = c->at<int>(L.acc); ap.acc_len = c->at<int>(L.acc_len);
   ap.out_tokens = c->at<int>(L.out_tokens); ap.t0 = c->at<int>(L.t0);
   ap.ab_out = c->at<float>(L.xa); ap.d = d; ap.h0 = c->at<float>(L.h0);
+  ap.step_ctr = c->at<int>(L.sample_step);
   {
     ProfScope ps(c, CLOVER_KSTAT_OTHER, 0, 0);
     HE(launch_accept(ap, c->st));
@@ -1122,6 +1141,7 @@ clover_status clover_prefill(clover_ctx* c, int32_t seq, const int32_t* tokens, 
   std::vector<int> meta(4 * (size_t)C);
   c->host_ids.assign(1, seq);
   HIPCK(c, hipMemcpyAsync(c->at<int>(L.seq_ids), c->host_ids.data(), sizeof(int), hipMemcpyHostToDevice, c->st));
+  HIPCK(c, hipMemsetAsync(c->at<int>(L.sample_step) + seq, 0, sizeof(int), c->st));  // a new sequence's draws
   for (int c0 = 0; c0 < n; c0 += C) {
     const int rows = std::min(C, n - c0);
     for (int i = 0; i < rows; ++i) {
@@ -1155,6 +1175,7 @@ clover_status clover_prefill(clover_ctx* c, int32_t seq, const int32_t* tokens, 
       lm.X = (const char*)c->at<char>(L.xn) + (size_t)(rows - 1) * d * L.es; lm.ldx = d;
       lm.mode = EP_PARTIAL; lm.max_splits = 1; lm.part = c->at<float>(L.vlogits);
       lm.amax_part = c->at<unsigned long long>(L.amax_part);
+      set_sampling(c, lm, 1, c->at<int>(L.seq_ids), 1);  // the first token: row 0 is sequence seq
       int lm_groups = 0;
       HIPCK(c, run_gemm(c, lm, 1, d, {{c->lm_head, cf.vocab}}, nullptr, &lm_groups));
       HIPCK(c, launch_argmax_groups(c->at<unsigned long long>(L.amax_part), lm_groups, 1, c->at<int>(L.amax), c->st));
@@ -1293,7 +1314,8 @@ clover_status clover_debug_read(clover_ctx* c, const char* name, void* host_dst,
       {"tree_depth", L.tree_depth, 4 * B * T}, {"tree_pos", L.tree_pos, 4 * B * T},
       {"tree_mask", L.tree_mask, 8 * B * T * L.W}, {"target", L.target, 4 * B * T},
       {"acc", L.acc, 4 * B * (H + 1)}, {"acc_len", L.acc_len, 4 * B}, {"h0", L.h0, 4 * B * cf.d_model},
-      {"t0", L.t0, 4 * B}, {"verify_logits", L.vlogits, 4 * B * T * (size_t)cf.vocab},
+      {"t0", L.t0, 4 * B}, {"sample_step", L.sample_step, 4 * B},
+      {"verify_logits", L.vlogits, 4 * B * T * (size_t)cf.vocab},
       {"x_last", L.x, 4 * B * T * (size_t)cf.d_model}, {"ab_out", L.xa, 4 * B * T * (size_t)cf.d_model}};
   std::vector<std::string> dn;
   for (int j = 1; j <= L.H; ++j) dn.push_back("draft_logits" + std::to_string(j));

@@ -241,8 +241,9 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(const GemmParams p) {
       for (int t = 0; t < MT; ++t)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
+          const int m = min(m0 + t * 16 + 4 * (lane >> 4) + r, p.M - 1);  // rows past M: not stored
           const unsigned long long k =
-              row16_amax_key(active ? acc[t][r] : -INFINITY, active ? n : 0x7fffffff);
+              row16_amax_key(active ? amax_value(p, acc[t][r], m, n) : -INFINITY, active ? n : 0x7fffffff);
           if ((lane & 15) == 0) s_key[wave * MROWS + t * 16 + 4 * (lane >> 4) + r] = k;
         }
       __syncthreads();

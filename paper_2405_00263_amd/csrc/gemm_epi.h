@@ -51,4 +51,14 @@ __device__ __forceinline__ void qkv_store(const GemmParams& p, int m, int pc, fl
   }
 }
 
+// The value the LM-head argmax keys rank for output (row m, column n): the logit itself, or
+// with sampling on the logit over the temperature plus the row's Gumbel noise for n.
+__device__ __forceinline__ float amax_value(const GemmParams& p, float v, int m, int n) {
+  if (p.inv_temp == 0.f) return v;
+  const int slot = p.samp_slot[m];
+  const uint32_t x = philox4x32_10_w0((uint32_t)n, (uint32_t)(m % p.samp_rows), (uint32_t)p.samp_step[slot],
+                                      (uint32_t)slot, p.samp_seed, p.samp_domain);
+  return v * p.inv_temp + gumbel_from_bits(x);
+}
+
 }  // namespace clover

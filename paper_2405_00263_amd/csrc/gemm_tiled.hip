@@ -206,12 +206,15 @@ __global__ __launch_bounds__(WR * TWAVES * 64) void tiled_kernel(const GemmParam
           // this lane's best over its tiles (tiles ascend in column: strict > keeps the lowest)
           float v = -INFINITY;
           int n = 0x7fffffff;
+          const int m = min(m0 + wrow * WM + t * 16 + 4 * (lane >> 4) + i, p.M - 1);  // rows past M: not stored
 #pragma unroll
-          for (int j = 0; j < TW; ++j)
-            if (act[j] && acc[t][j][i] > v) {
-              v = acc[t][j][i];
+          for (int j = 0; j < TW; ++j) {
+            const float a = act[j] ? amax_value(p, acc[t][j][i], m, otile[j] * 16 + ccol) : -INFINITY;
+            if (act[j] && a > v) {
+              v = a;
               n = otile[j] * 16 + ccol;
             }
+          }
           const unsigned long long k = row16_amax_key(v, n);
           if (ccol == 0) s_key[wave * BM + wrow * WM + t * 16 + 4 * (lane >> 4) + i] = k;
         }

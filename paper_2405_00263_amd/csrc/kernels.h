@@ -35,6 +35,16 @@ struct GemmParams {
   // EP_PARTIAL with one split: optional per-(column group, row) argmax keys [ngroups][M]
   // of the output (amax_key order), reduced by launch_argmax_groups; null: off
   unsigned long long* amax_part;
+  // Sampling with the argmax keys (amax_part): they rank logit * inv_temp + Gumbel noise,
+  // so each row's argmax is a sample of softmax(logit / temperature) (Gumbel-max); inv_temp
+  // 0 keeps the plain argmax.  The noise of row m, column v is the Philox word for counter
+  // (v, m % samp_rows, samp_step[slot], slot), slot = samp_slot[m], key (samp_seed,
+  // samp_domain).  The partial/logit outputs stay the plain logits.
+  float inv_temp;
+  uint32_t samp_seed, samp_domain;
+  const int* samp_slot;
+  const int* samp_step;
+  int samp_rows;
   int mode;
   void* out_s; int ldos;
   // EP_QKV
@@ -202,6 +212,7 @@ struct AcceptParams {
   int* acc; int* acc_len; int* out_tokens; int* t0;
   const float* ab_out; int d; float* h0;      // AB output rows [nbatch*T][d]
   const float* x_last; float* x_keep;          // optional
+  int* step_ctr;                               // optional per-slot step counter, +1 per step
 };
 hipError_t launch_accept(AcceptParams& p, hipStream_t st);
 

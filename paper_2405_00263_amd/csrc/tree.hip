@@ -146,6 +146,7 @@ __global__ __launch_bounds__(TREE_THREADS) void accept_kernel(const AcceptParams
   if (threadIdx.x == 0) {
     p.acc_len[slot] = A;
     if (p.t0) p.t0[slot] = bonus;
+    if (p.step_ctr) p.step_ctr[slot] += 1;  // the sampled targets' draws move on
   }
   if (!p.h0) return;
   const float* src = p.ab_out + (size_t)(b * T + cur) * p.d;

@@ -37,6 +37,8 @@ class CloverConfig:
     # key set of the Attention Decoder: "single" {e}, "two" {RMSNorm(h), e}, "path" {e_0..}
     ad_keys: str = "single"
     ad_per_head: bool = False  # one Attention Decoder per head instead of one shared
+    temperature: float = 0.0   # 0: greedy; > 0: the target samples (speculative sampling)
+    sample_seed: int = 0
 
     @property
     def ab_kind(self) -> str:

@@ -482,3 +482,63 @@ def test_speculator_variants_match_oracle(draft, ab, ad_keys, per_head):
         assert ours == ref, (step, ours, ref)
         out += ours
     assert out == o.base.greedy_generate(prompt, len(out))
+
+
+@pytest.mark.parametrize("which", ["tiny_fp32", "small_bf16_t128"])
+def test_sampled_targets_match_oracle_sampler(which):
+    """Speculative sampling (temperature 0.8): every tree node's target is a Gumbel-max draw
+    fused into the LM head's argmax epilogue.  On the GPU's own verify logits the oracle's
+    sampler (its own Philox4x32-10 and Gumbel transform) reproduces every target exactly
+    wherever the top two perturbed scores are not within 1e-4 of each other; the step counter
+    of each slot advances once per step; end to end, tokens equal the oracle's while no draw
+    is that close.  Two sequences (slots 0 and 1); the bf16 case verifies 2 x 128 rows on the
+    register-blocked kernel."""
+    P = need_gpu()
+    note(f"engine sampling {which}")
+    if which == "tiny_fp32":
+        cfg, w = _tiny(batch=2, temperature=0.8, sample_seed=1234)
+        tol = 1e-4
+    else:
+        cfg = _bf16_small().with_(batch=2, topk=(8, 4, 4), tree_tokens=128, max_context=1024,
+                                  temperature=0.8, sample_seed=77)
+        w = synth.make_weights(cfg, seed=9, perturb=True)
+        tol = 2e-2
+    from oracle import sampling
+    eng = _engine(P, cfg, w)
+    o = oracle.CloverOracle(cfg, w)
+    T, V = cfg.tree_tokens, cfg.vocab
+    states, same = [], [True, True]
+    for s in range(2):
+        prompt = synth.make_prompt(cfg, seq=s, n=60 + 17 * s)
+        t0 = eng.prefill(s, prompt)
+        st = o.prefill(prompt, slot=s)
+        states.append(st)
+        if t0 != st.t0:  # only a near-tie among the perturbed scores may separate them
+            sc = np.sort(sampling.gumbel_scores(o.base.logits(o.base.forward_rows(prompt, np.arange(len(prompt)), None,
+                         np.tril(np.ones((len(prompt),) * 2, dtype=bool)))[0][-1:])[0], cfg.temperature,
+                         cfg.sample_seed, 1, 0, s, 0))
+            assert sc[-1] - sc[-2] < 2 * tol / cfg.temperature, s
+            same[s] = False
+    near = 0
+    for k in range(4):
+        got = eng.step([0, 1])
+        assert list(eng.debug("sample_step", np.int32, (2,))) == [k + 1, k + 1]
+        vl = eng.debug("verify_logits", np.float32, (2 * T, V)).reshape(2, T, V)
+        tg = eng.debug("target", np.int32, (2 * T,)).reshape(2, T)
+        for s in range(2):
+            scores = sampling.gumbel_scores(vl[s], cfg.temperature, cfg.sample_seed, 0, k, s, np.arange(T))
+            want = np.argmax(scores, axis=1)
+            top2 = np.sort(scores, axis=1)[:, -2:]
+            clear = (top2[:, 1] - top2[:, 0]) >= 1e-4
+            near += int(np.sum(~clear))
+            assert np.array_equal(tg[s][clear], want[clear]), (k, s)
+            if same[s]:
+                ref, det = o.step(states[s])
+                sc = np.sort(sampling.gumbel_scores(det["ver"].logits, cfg.temperature, cfg.sample_seed, 0, k, s,
+                                                    np.arange(T)), axis=1)
+                if np.min(sc[:, -1] - sc[:, -2]) >= 2 * tol / cfg.temperature and \
+                        np.array_equal(eng.debug("tree_token", np.int32, (2, T))[s], det["tree"].tokens):
+                    assert got[s] == ref, (k, s)
+                else:
+                    same[s] = False
+    note(f"sampling {which}: {near} near-tie draws skipped")
