@@ -226,6 +226,8 @@ def main():
                     help="override the Augmenting Block variant (Sec. 4.4)")
     ap.add_argument("--ad-keys", default="", choices=["", "single", "two", "path"],
                     help="override the Attention Decoder's key set (Eq. 1 readings)")
+    ap.add_argument("--temperature", type=float, default=-1.0,
+                    help="override the sampling temperature (0: greedy; > 0: speculative sampling)")
     ap.add_argument("--surface", action="store_true",
                     help="batch x tree-size cost surface instead of the headline line (one JSON line per cell)")
     ap.add_argument("--surface-batches", default="1,2,4,8,16")
@@ -258,6 +260,8 @@ def main():
         over["ab"] = args.ab
     if args.ad_keys:
         over["ad_keys"] = args.ad_keys
+    if args.temperature >= 0:
+        over["temperature"] = args.temperature
     if over:
         cfg = cfg.with_(**over)
     torch.cuda.set_device(0)
@@ -326,7 +330,7 @@ def main():
         "dtype": cfg.dtype,
         "data": "synthetic: random-init N(0,0.02) weights, uniform-random prompt tokens",
         "config": {"workload": cfg.name, "speculator": cfg.draft, "augmenting_block": cfg.ab_kind,
-                   "decoder_keys": cfg.ad_keys,
+                   "decoder_keys": cfg.ad_keys, "temperature": cfg.temperature,
                    "n_layers": cfg.n_layers, "d_model": d,
                    "n_heads": cfg.n_heads, "n_kv_heads": cfg.n_kv_heads, "head_dim": cfg.head_dim,
                    "ffn_dim": F, "vocab": V, "spec_heads": cfg.n_spec_heads, "topk": list(cfg.topk),

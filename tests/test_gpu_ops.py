@@ -77,6 +77,9 @@ ATT_CASES = [
     ("f32", 200, 64, 4, 4, 64, True), ("bf16", 1024, 64, 8, 8, 128, False), ("bf16", 1, 1, 4, 4, 128, False),
     ("bf16", 3000, 64, 8, 1, 128, False), ("bf16", 77, 128, 4, 2, 64, False), ("bf16", 256, 256, 2, 2, 128, True),
     ("bf16", 4096, 64, 4, 4, 128, False),
+    # the context sweep's longest cells and the largest context the kernel takes (65536 keys)
+    ("bf16", 32768, 64, 8, 8, 128, False), ("bf16", 16384, 128, 8, 1, 128, False),
+    ("bf16", 65472, 64, 2, 2, 128, False),
 ]
 
 
