@@ -38,7 +38,11 @@
 namespace clover {
 
 static constexpr int STAGE_CHUNKS = 4;   // chunks of X per LDS stage
-static constexpr int PF = 16;            // weight fragments in flight per wave (16 KB)
+// Weight fragments in flight per wave (8 KB).  A sweep of 8, 16, 24 and 32 (and of 2- and
+// 4-chunk stages) on MI355X put 8 first on every 64-row shape: the shallower ring leaves
+// 112-130 VGPRs, so two 8-wave (or 6-wave) workgroups share a compute unit, and two
+// workgroups' loads in flight beat one workgroup's deeper ring.
+static constexpr int PF = 8;
 static constexpr int RING = PF / STAGE_CHUNKS;  // stages covered by the prefetch ring
 static_assert(RING % 2 == 0, "stages alternate between two LDS buffers inside a superstage");
 
