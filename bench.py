@@ -147,10 +147,53 @@ def verify_weight_bytes(cfg):
     return cfg.n_layers * layer_w + ab_w + V * d * es
 
 
+def verify_kv_bytes(cfg, contexts):
+    """KV-cache bytes one verify forward moves besides the weights: every committed key and
+    value of each sequence read once per attention layer (the target layers, plus the
+    Augmenting Block when it has an attention half), and the tree's own keys and values
+    written once."""
+    es = 2 if cfg.dtype == "bf16" else 4
+    kvd = cfg.n_kv_heads * cfg.head_dim
+    layers = cfg.n_layers + (1 if cfg.ab_kind in ("full", "attn") else 0)
+    read = sum(2 * c * kvd * es for c in contexts) * layers
+    write = 2 * cfg.batch * cfg.tree_tokens * kvd * es * layers
+    return read + write
+
+
+def measured_copy_gbps(torch, nbytes=1 << 30, reps=10):
+    """Device-to-device copy rate on this GPU (bytes read + written per second), the
+    achievable-bandwidth reference the roofline is also compared against."""
+    src = torch.empty(nbytes // 2, dtype=torch.bfloat16, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del src, dst
+    torch.cuda.empty_cache()
+    return 2.0 * nbytes / (ms * 1e-3) / 1e9
+
+
+def _pct(v, q):
+    """Percentile q (0..100) of the list v by linear interpolation."""
+    v = sorted(v)
+    if not v:
+        return 0.0
+    x = (len(v) - 1) * q / 100.0
+    lo = int(x)
+    hi = min(lo + 1, len(v) - 1)
+    return v[lo] + (v[hi] - v[lo]) * (x - lo)
+
+
 def surface(args):
-    """Batch x tree-size cost surface of one step (Sec. 1 and 4.2 of the
-    paper argue that speculation pays while the verify stays memory-bound and loses its
-    edge as batch and tree grow towards the compute bound).
+    """Batch x tree-size cost surface of one step (Sec. 1 and 4.2 of the paper argue that
+    speculation pays while the verify stays memory-bound and loses its edge as batch and
+    tree grow towards the compute bound).
 
     One JSON line per cell: batch B, tree tokens T, the per-phase latencies, and the verify
     forward's weight-stream rate and matrix arithmetic rate (2 flops per weight per verify
@@ -234,7 +277,7 @@ def main():
     ap.add_argument("--surface-trees", default="4,16,32,64,128")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
               "(each sequence is independent, so more GPUs would each run their own batch)",
               file=sys.stderr)
         sys.exit(2)
@@ -316,6 +359,11 @@ def main():
     med = {k: statistics.median(v) for k, v in phase.items()}
     d, F, V = cfg.d_model, cfg.ffn_dim, cfg.vocab
     verify_wbytes = verify_weight_bytes(cfg)
+    # context at the middle of the timed steps (each step commits about one token per
+    # sequence with random-init heads)
+    mid_ctx = [c + args.warmup + args.steps // 2 for c in ctx_start]
+    verify_kvbytes = verify_kv_bytes(cfg, mid_ctx)
+    copy_gbps = measured_copy_gbps(torch)
     result = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -340,7 +388,11 @@ def main():
         "draft_ms": round(med["draft_ms"], 4),
         "accept_ms": round(med["accept_ms"], 4),
         "step_ms_events": round(med["total_ms"], 4),
+        "step_ms_p10_p50_p90": [round(_pct(phase["total_ms"], q), 4) for q in (10, 50, 90)],
+        "verify_ms_p10_p50_p90": [round(_pct(phase["verify_ms"], q), 4) for q in (10, 50, 90)],
         "verify_weight_GBps": round(verify_wbytes / (med["verify_ms"] * 1e-3) / 1e9, 1),
+        "verify_effective_GBps": round((verify_wbytes + verify_kvbytes) / (med["verify_ms"] * 1e-3) / 1e9, 1),
+        "measured_copy_GBps": round(copy_gbps, 1),
         "tokens_emitted_per_step": round(emitted / (args.steps * cfg.batch), 3),
         "roofline": {
             "bound": "mfma" if mfma_bound else "hbm",
@@ -352,6 +404,7 @@ def main():
             "kernel": ("verify-forward GEMMs (register-blocked tiled_kernel)" if mfma_bound
                        else "verify-forward GEMMs (streaming gemm_kernel)"),
             "weight_stream_GBps": round(achieved, 1),
+            "frac_of_measured_copy": None if mfma_bound else round(achieved / copy_gbps, 4),
             "timed_steps": kt_steps,
             "launches": g["launches"],
             "avg_launch_us": round(1e3 * g["total_ms"] / max(g["launches"], 1), 3),

@@ -4,6 +4,7 @@ Every call recompiles all sources; objects go to ``_build/`` next to this file a
 shared library to ``libclover.so`` in this directory.
 """
 import os
+import re
 import subprocess
 import sys
 from concurrent.futures import ThreadPoolExecutor
@@ -15,6 +16,8 @@ BUILD = os.path.join(HERE, "_build")
 ARCH = "gfx950"
 SOURCES = ["gemm.hip", "gemm_tiled.hip", "attention.hip", "rows.hip", "tree.hip", "api.cpp"]
 CFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
+          # per-kernel resource report, read by _check_no_scratch
+          "-Rpass-analysis=kernel-resource-usage",
           # packed fp32 instructions stay off (see the project notes on gfx950 correctness)
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-Wno-unused-command-line-argument"]
@@ -34,6 +37,24 @@ def _run(cmd):
     return r.stdout
 
 
+def _check_no_scratch(report: str, source: str):
+    """Fail the build if a kernel uses private (scratch) memory: in these kernels that only
+    happens when an accumulator array is indexed at run time, which moves it out of
+    registers and slows the kernel several-fold."""
+    name = None
+    bad = []
+    for line in report.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+            continue
+        m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m and int(m.group(1)) > 0:
+            bad.append(f"{name}: {m.group(1)} bytes/lane")
+    if bad:
+        raise RuntimeError(f"{source}: kernels using scratch memory:\n  " + "\n  ".join(bad))
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     hipcc = _hipcc()
@@ -43,9 +64,12 @@ def build(verbose: bool = False) -> str:
         objs.append(o)
         cmds.append([hipcc, *CFLAGS, "-c", os.path.join(SRC, s), "-o", o])
     with ThreadPoolExecutor(max_workers=min(len(cmds), os.cpu_count() or 4)) as ex:
-        for out in ex.map(_run, cmds):
-            if verbose and out.strip():
-                print(out)
+        for src, out in zip(SOURCES, ex.map(_run, cmds)):
+            _check_no_scratch(out, src)
+            if verbose:
+                warn = "\n".join(l for l in out.splitlines() if "remark:" not in l)
+                if warn.strip():
+                    print(warn)
     tmp = OUT + ".tmp"
     _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
     os.replace(tmp, OUT)

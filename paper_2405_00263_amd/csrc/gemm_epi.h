@@ -51,14 +51,33 @@ __device__ __forceinline__ void qkv_store(const GemmParams& p, int m, int pc, fl
   }
 }
 
+// Gumbel-max score of one logit: the logit times the float32 reciprocal of the temperature,
+// plus standard Gumbel noise from the counter (column n, row, step, slot) under the key
+// (seed, domain).  The product and the sum round separately (no fused multiply-add), as
+// float32 arithmetic written out does.
+__device__ __forceinline__ float gumbel_score(float v, float inv_temp, uint32_t n, uint32_t row, uint32_t step,
+                                              uint32_t slot, uint32_t seed, uint32_t domain) {
+#pragma clang fp contract(off)
+  const uint32_t x = philox4x32_10_w0(n, row, step, slot, seed, domain);
+  const float scaled = v * inv_temp;
+  return scaled + gumbel_from_bits(x);
+}
+
+// The same score behind a call, for epilogues with many outputs per lane: inlining the
+// generator at every output makes the epilogue too long to unroll, and the accumulators
+// would then be indexed at run time (private memory).
+__device__ __noinline__ float gumbel_score_call(float v, float inv_temp, uint32_t n, uint32_t row, uint32_t step,
+                                                uint32_t slot, uint32_t seed, uint32_t domain) {
+  return gumbel_score(v, inv_temp, n, row, step, slot, seed, domain);
+}
+
 // The value the LM-head argmax keys rank for output (row m, column n): the logit itself, or
 // with sampling on the logit over the temperature plus the row's Gumbel noise for n.
 __device__ __forceinline__ float amax_value(const GemmParams& p, float v, int m, int n) {
   if (p.inv_temp == 0.f) return v;
   const int slot = p.samp_slot[m];
-  const uint32_t x = philox4x32_10_w0((uint32_t)n, (uint32_t)(m % p.samp_rows), (uint32_t)p.samp_step[slot],
-                                      (uint32_t)slot, p.samp_seed, p.samp_domain);
-  return v * p.inv_temp + gumbel_from_bits(x);
+  return gumbel_score(v, p.inv_temp, (uint32_t)n, (uint32_t)(m % p.samp_rows), (uint32_t)p.samp_step[slot],
+                      (uint32_t)slot, p.samp_seed, p.samp_domain);
 }
 
 }  // namespace clover

@@ -32,7 +32,7 @@ namespace clover {
 static constexpr int TWAVES = 4;  // waves per row of waves (column groups per workgroup)
 static constexpr int TSC = 2;     // 32-wide k chunks per LDS stage
 
-template <int MT, int TW, int RING, int WR, bool AMAX>
+template <int MT, int TW, int RING, int WR, int AMAX>
 __global__ __launch_bounds__(WR * TWAVES * 64) void tiled_kernel(const GemmParams p) {
   using S = bf16_t;
   using T = St<S>;
@@ -195,7 +195,7 @@ __global__ __launch_bounds__(WR * TWAVES * 64) void tiled_kernel(const GemmParam
           if (m < p.M) out[(size_t)m * p.N + n] = acc[t][j][i];
         }
     }
-    if constexpr (AMAX) {
+    if constexpr (AMAX != 0) {
       // each row's best (value, column) over this group's columns: tiles, lanes, waves
       __syncthreads();  // the LDS stages are no longer read
       unsigned long long* s_key = reinterpret_cast<unsigned long long*>(smem);  // [TWAVES][BM]
@@ -207,9 +207,17 @@ __global__ __launch_bounds__(WR * TWAVES * 64) void tiled_kernel(const GemmParam
           float v = -INFINITY;
           int n = 0x7fffffff;
           const int m = min(m0 + wrow * WM + t * 16 + 4 * (lane >> 4) + i, p.M - 1);  // rows past M: not stored
+          uint32_t sslot = 0, sstep = 0;
+          if constexpr (AMAX == 2) {
+            sslot = (uint32_t)p.samp_slot[m];
+            sstep = (uint32_t)p.samp_step[sslot];
+          }
 #pragma unroll
           for (int j = 0; j < TW; ++j) {
-            const float a = act[j] ? amax_value(p, acc[t][j][i], m, otile[j] * 16 + ccol) : -INFINITY;
+            float a = acc[t][j][i];
+            if constexpr (AMAX == 2)
+              a = gumbel_score_call(a, p.inv_temp, (uint32_t)(otile[j] * 16 + ccol), (uint32_t)(m % p.samp_rows),
+                                    sstep, sslot, p.samp_seed, p.samp_domain);
             if (act[j] && a > v) {
               v = a;
               n = otile[j] * 16 + ccol;
@@ -343,7 +351,10 @@ GemmPlan plan_tiled_forced(int M, int ntiles, int nchunks, bool swiglu, int mt, 
 
 template <int MT, int TW, int RING, int WR>
 static void launch_shape(const GemmPlan& pl, GemmParams& p, hipStream_t st, const LaunchTiming* lt) {
-  auto kern = p.amax_part ? tiled_kernel<MT, TW, RING, WR, true> : tiled_kernel<MT, TW, RING, WR, false>;
+  // argmax epilogue: greedy (1) or Gumbel-max sampling (2), separate instantiations so the
+  // greedy one carries no generator code
+  auto kern = !p.amax_part ? tiled_kernel<MT, TW, RING, WR, 0>
+              : p.inv_temp != 0.f ? tiled_kernel<MT, TW, RING, WR, 2> : tiled_kernel<MT, TW, RING, WR, 1>;
   dim3 grid(8 * ((pl.ngroups * pl.S + 7) / 8) * pl.mchunks), block(WR * TWAVES * 64);
   if (lt) hipExtLaunchKernelGGL(kern, grid, block, (uint32_t)pl.lds_bytes, st, lt->start, lt->stop, 0, p);
   else hipLaunchKernelGGL(kern, grid, block, pl.lds_bytes, st, p);
