@@ -330,7 +330,7 @@ struct clover_ctx {
   int* pin_out = nullptr;   // ... and of the emitted tokens [max_batch][H+1]
   std::string err;
   bool dead = false;
-  hipEvent_t ev[4];
+  hipEvent_t ev[4] = {};
   clover_timings tim{};
   int last_nbatch = 0;
   // per-launch profiling (CLOVER_FLAG_PROFILE)
@@ -1063,7 +1063,7 @@ clover_status clover_init(const clover_config* cfg, void* const* weights, void* 
   c->bt_host.assign((size_t)cfg->max_batch * L.mbps, 0);
   auto fail = [&](hipError_t e, const char* what) {
     set_global_err("init: %s: %s", what, hipGetErrorString(e));
-    delete c;
+    clover_destroy(c);  // releases whatever was created so far
     return CLOVER_ERR_DEVICE;
   };
   hipError_t e;
@@ -1095,7 +1095,8 @@ clover_status clover_init(const clover_config* cfg, void* const* weights, void* 
 void clover_destroy(clover_ctx* ctx) {
   if (!ctx) return;
   (void)hipStreamSynchronize(ctx->st);
-  for (int i = 0; i < 4; ++i) (void)hipEventDestroy(ctx->ev[i]);
+  for (int i = 0; i < 4; ++i)
+    if (ctx->ev[i]) (void)hipEventDestroy(ctx->ev[i]);
   for (auto e : ctx->pev) (void)hipEventDestroy(e);
   for (auto& g : ctx->graphs)
     for (hipGraphExec_t x : {g.draft, g.verify, g.accept})
