@@ -194,6 +194,36 @@ static_assert(TOPK_WAVES * KMAX <= 64, "one candidate per lane when the waves' l
 
 // The k best of the wave's candidates (each lane holds N, index INT_MAX = empty) into
 // res_v/res_i[0..k) (written by lane 0), best first.  The candidates taken are emptied.
+// The wave's best (value, index) pair under `better`, left in every lane: rotations inside
+// each 16-lane row (DPP), then the row pairs 16 and 32 lanes apart swapped in (VALU lane
+// swaps) -- no LDS-routed shuffles.  `better` is a total order, so the result does not
+// depend on the order of the comparisons.
+__device__ __forceinline__ void wave_best_step(float& bv, int& bi, float ov, int oi) {
+  if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+}
+__device__ __forceinline__ void wave_best(float& bv, int& bi) {
+  wave_best_step(bv, bi, __int_as_float(dpp_row_ror<8>(__float_as_int(bv))), dpp_row_ror<8>(bi));
+  wave_best_step(bv, bi, __int_as_float(dpp_row_ror<4>(__float_as_int(bv))), dpp_row_ror<4>(bi));
+  wave_best_step(bv, bi, __int_as_float(dpp_row_ror<2>(__float_as_int(bv))), dpp_row_ror<2>(bi));
+  wave_best_step(bv, bi, __int_as_float(dpp_row_ror<1>(__float_as_int(bv))), dpp_row_ror<1>(bi));
+  {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(bv), __float_as_uint(bv), false, false);
+    const auto b = __builtin_amdgcn_permlane16_swap((unsigned)bi, (unsigned)bi, false, false);
+    float v0 = __uint_as_float(a[0]);
+    int i0 = (int)b[0];
+    wave_best_step(v0, i0, __uint_as_float(a[1]), (int)b[1]);
+    bv = v0; bi = i0;
+  }
+  {
+    const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(bv), __float_as_uint(bv), false, false);
+    const auto b = __builtin_amdgcn_permlane32_swap((unsigned)bi, (unsigned)bi, false, false);
+    float v0 = __uint_as_float(a[0]);
+    int i0 = (int)b[0];
+    wave_best_step(v0, i0, __uint_as_float(a[1]), (int)b[1]);
+    bv = v0; bi = i0;
+  }
+}
+
 template <int N>
 __device__ __forceinline__ void wave_topk(float (&v)[N], int (&ix)[N], int k, float* res_v, int* res_i) {
   for (int r = 0; r < k; ++r) {
@@ -202,12 +232,7 @@ __device__ __forceinline__ void wave_topk(float (&v)[N], int (&ix)[N], int k, fl
 #pragma unroll
     for (int u = 0; u < N; ++u)
       if (better(v[u], ix[u], bv, bi)) { bv = v[u]; bi = ix[u]; }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float ov = __shfl_xor(bv, o);
-      const int oi = __shfl_xor(bi, o);
-      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-    }
+    wave_best(bv, bi);
     if ((threadIdx.x & 63) == 0) { res_v[r] = bv; res_i[r] = bi; }
 #pragma unroll
     for (int u = 0; u < N; ++u)
