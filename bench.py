@@ -19,6 +19,7 @@ bandwidth against the 8 TB/s peak (HIP events around every launch in the timed
 region) and the CPU oracle's throughput on a bounded sample of the same workload.
 """
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -224,6 +225,8 @@ def surface(args):
         for _ in range(args.warmup):
             eng.step(seqs)
         ph = {"draft_ms": [], "verify_ms": [], "total_ms": []}
+        gc.collect()
+        gc.disable()  # no garbage-collector pause inside the timed steps
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for _ in range(args.steps):
@@ -233,6 +236,7 @@ def surface(args):
                 ph[k].append(tm[k])
         torch.cuda.synchronize()
         step_ms = 1e3 * (time.perf_counter() - t0) / args.steps
+        gc.enable()
         med = {k: statistics.median(v) for k, v in ph.items()}
         wb = verify_weight_bytes(cfg)
         params = wb / (2 if cfg.dtype == "bf16" else 4)
@@ -328,6 +332,11 @@ def main():
     eng.reset_kernel_stats()
     phase = {"draft_ms": [], "verify_ms": [], "accept_ms": [], "total_ms": []}
     emitted = 0
+    # Python's cyclic garbage collector can stop this loop for tens of milliseconds (a
+    # full collection over the interpreter's objects); it runs before, not inside, the
+    # timed steps
+    gc.collect()
+    gc.disable()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -338,6 +347,7 @@ def main():
             phase[k].append(tm[k])
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    gc.enable()
     ms_per_step = 1e3 * elapsed / args.steps
     T = cfg.tree_tokens
     value = cfg.batch * T * args.steps / elapsed

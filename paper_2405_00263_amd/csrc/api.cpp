@@ -323,7 +323,8 @@ struct clover_ctx {
   std::vector<int> seq_len;                  // -1 inactive
   std::vector<std::vector<int>> seq_blocks;  // physical KV blocks per slot
   std::vector<int> free_blocks;
-  std::vector<int> bt_host;
+  int* bt_host = nullptr;  // pinned host copy of the block table [max_batch][mbps]: the step's
+                           // block-table updates are copied from it like the other pinned staging
   std::vector<int> host_ids, host_len;
   int* pin_ids = nullptr;   // pinned host staging of the step's sequence ids [max_batch]
   int* pin_len = nullptr;   // ... and of the committed lengths [max_batch]
@@ -543,7 +544,7 @@ clover_status ensure_blocks(clover_ctx* c, int slot, int upto) {
     bl.push_back(c->free_blocks.back());
     c->free_blocks.pop_back();
   }
-  int* row = c->bt_host.data() + (size_t)slot * c->L.mbps;
+  int* row = c->bt_host + (size_t)slot * c->L.mbps;
   for (int i = first; i < need; ++i) row[i] = bl[i];
   HIPCK(c, hipMemcpyAsync(c->at<int>(c->L.block_table) + (size_t)slot * c->L.mbps + first,
                           row + first, sizeof(int) * (need - first), hipMemcpyHostToDevice, c->st));
@@ -1060,7 +1061,6 @@ clover_status clover_init(const clover_config* cfg, void* const* weights, void* 
   c->seq_len.assign(cfg->max_batch, -1);
   c->seq_blocks.assign(cfg->max_batch, {});
   for (int b = L.nblocks - 1; b >= 0; --b) c->free_blocks.push_back(b);
-  c->bt_host.assign((size_t)cfg->max_batch * L.mbps, 0);
   auto fail = [&](hipError_t e, const char* what) {
     set_global_err("init: %s: %s", what, hipGetErrorString(e));
     clover_destroy(c);  // releases whatever was created so far
@@ -1073,8 +1073,10 @@ clover_status clover_init(const clover_config* cfg, void* const* weights, void* 
   const size_t H1 = (size_t)c->L.H + 1;
   if ((e = hipHostMalloc((void**)&c->pin_ids, sizeof(int) * cfg->max_batch, hipHostMallocDefault)) != hipSuccess ||
       (e = hipHostMalloc((void**)&c->pin_len, sizeof(int) * cfg->max_batch, hipHostMallocDefault)) != hipSuccess ||
-      (e = hipHostMalloc((void**)&c->pin_out, sizeof(int) * cfg->max_batch * H1, hipHostMallocDefault)) != hipSuccess)
+      (e = hipHostMalloc((void**)&c->pin_out, sizeof(int) * cfg->max_batch * H1, hipHostMallocDefault)) != hipSuccess ||
+      (e = hipHostMalloc((void**)&c->bt_host, sizeof(int) * (size_t)cfg->max_batch * L.mbps, hipHostMallocDefault)) != hipSuccess)
     return fail(e, "pinned staging");
+  std::memset(c->bt_host, 0, sizeof(int) * (size_t)cfg->max_batch * L.mbps);
   // zero the KV pools (attention reads whole 16-key blocks), counters and state
   if ((e = hipMemsetAsync(c->ws, 0, L.pool_ptrs, c->st)) != hipSuccess) return fail(e, "memset pools");
   if ((e = hipMemsetAsync(c->ws + L.block_table, 0, L.x - L.block_table, c->st)) != hipSuccess) return fail(e, "memset state");
@@ -1102,7 +1104,7 @@ void clover_destroy(clover_ctx* ctx) {
     for (hipGraphExec_t x : {g.draft, g.verify, g.accept})
       if (x) (void)hipGraphExecDestroy(x);
   if (ctx->cap_st) (void)hipStreamDestroy(ctx->cap_st);
-  for (int* p : {ctx->pin_ids, ctx->pin_len, ctx->pin_out})
+  for (int* p : {ctx->pin_ids, ctx->pin_len, ctx->pin_out, ctx->bt_host})
     if (p) (void)hipHostFree(p);
   delete ctx;
 }
