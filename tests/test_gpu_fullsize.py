@@ -7,7 +7,9 @@ Workloads (bf16, HIP-graph replay, the engine's default):
 - llama7b_b8: the same model, 8 sequences with seeded prompt lengths in 2048..4096 on
   the paged KV cache, 512 verify rows;
 - large_gqa_b1: 80 layers, d_model 8192, 64 query / 8 KV heads of 128, SwiGLU 28672,
-  4 Clover heads with top-k (8, 4, 2, 2), batch 1, 2048-token prompt.
+  4 Clover heads with top-k (8, 4, 2, 2), batch 1, 2048-token prompt;
+- llama7b_b8 with speculative sampling at temperature 0.8 (`bench.py --workload llama7b_b8
+  --temperature 0.8`): the 512-row LM head's sampled argmax epilogue at full size.
 
 The float64 oracle cannot run these forwards in a test, so it recomputes sampled
 outputs one by one from the GPU's own inputs to that stage, and the discrete stages
@@ -18,7 +20,9 @@ are checked exactly, for every sequence of the batch:
 - top-k children of every frontier row of every depth, their cumulative log-probs, and
   the truncated tree and its ancestor mask, from the GPU's draft logits;
 - verify: final norm + LM head on sampled tree rows from the residual after the last
-  layer, and target = argmax of every row;
+  layer, and target = argmax of every row (with sampling: on sampled rows, the oracle's
+  Gumbel-max draw from the GPU's logits, wherever the top two perturbed scores are not
+  within 1e-4);
 - acceptance from the tree and targets, and the emitted tokens;
 - KV compaction: layer 0's committed K/V rows of the accepted nodes equal the oracle's
   layer-0 K/V of those tokens at their committed positions (embedding, RMSNorm, QKV,
@@ -37,7 +41,7 @@ from tests.gpu_util import need_gpu, note
 pytestmark = pytest.mark.gpu
 
 LOGIT_TOL = 2e-2  # bf16 workloads: max-abs on logits
-WORKLOADS = ["llama7b_b1", "llama7b_b8", "large_gqa_b1"]
+WORKLOADS = ["llama7b_b1", "llama7b_b8", "large_gqa_b1", "llama7b_b8@0.8"]
 
 
 def _f64(t):
@@ -47,7 +51,10 @@ def _f64(t):
 @pytest.fixture(scope="module", params=WORKLOADS)
 def run(request):
     P = need_gpu()
-    cfg = synth.get_config(request.param)
+    name, _, temp = request.param.partition("@")
+    cfg = synth.get_config(name)
+    if temp:
+        cfg = cfg.with_(temperature=float(temp), sample_seed=31)
     B, T, H, V, d = cfg.batch, cfg.tree_tokens, cfg.n_spec_heads, cfg.vocab, cfg.d_model
     lens = [cfg.prompt_len[0]] if B == 1 else synth.make_prompt_lengths(cfg)
     note(f"full-size workload {cfg.name}: weights on device, prompts {lens}")
@@ -68,6 +75,7 @@ def run(request):
     note("one graph-replayed step")
     eng.step(seqs)  # warm-up step: captures the graphs
     t0 = eng.debug("t0", np.int32, (B,))
+    sample_step = eng.debug("sample_step", np.int32, (B,))  # the counters the next step draws with
     h0 = eng.debug("h0", np.float32, (B, d)).astype(np.float64)
     L = [eng.seq_len(b) for b in seqs]
     out = eng.step(seqs)
@@ -76,7 +84,7 @@ def run(request):
         F *= k
         ncand += F
     r = {
-        "cfg": cfg, "B": B, "t0": t0, "h0": h0, "L": L, "out": out,
+        "cfg": cfg, "B": B, "t0": t0, "h0": h0, "L": L, "out": out, "sample_step": sample_step,
         "cand_token": eng.debug("cand_token", np.int32, (B, ncand)),
         "cand_parent": eng.debug("cand_parent", np.int32, (B, ncand)),
         "cand_depth": eng.debug("cand_depth", np.int32, (B, ncand)),
@@ -173,10 +181,21 @@ def test_fullsize_topk_lp_and_tree_exact(run):
 
 def test_fullsize_verify_lm_head_rows_and_targets(run):
     r = run
+    cfg = r["cfg"]
     rows = [0, 1, 9, 33, 63]
     for b in range(r["B"]):
         vl = r["verify_logits"][b]
-        assert np.array_equal(r["target"][b], np.argmax(vl, axis=1)), b
+        if cfg.temperature > 0:
+            # the draws of sampled rows: node n of sequence slot b at this step's counter
+            from oracle import sampling
+            sc = sampling.gumbel_scores(vl[rows], cfg.temperature, cfg.sample_seed, sampling.DOMAIN_VERIFY,
+                                        int(r["sample_step"][b]), b, np.asarray(rows))
+            want = np.argmax(sc, axis=1)
+            top2 = np.sort(sc, axis=1)[:, -2:]
+            clear = (top2[:, 1] - top2[:, 0]) >= 1e-4
+            assert np.array_equal(r["target"][b][rows][clear], want[clear]), b
+        else:
+            assert np.array_equal(r["target"][b], np.argmax(vl, axis=1)), b
         ref = _lm_logits(r, r["x_last"][b][rows])
         err = float(np.max(np.abs(vl[rows] - ref)))
         note(f"{r['cfg'].name} verify LM-head rows {rows} of sequence {b}: max |err| {err:.3e}")
