@@ -75,6 +75,28 @@ def _prompt_lengths(cfg):
     return synth.make_prompt_lengths(cfg)
 
 
+def _tiny_single_thread():
+    """The oracle on the small fp32 workload (2 layers, d_model 256, 41-token trees,
+    128-token prompt), single-threaded: prefill, then all 16 steps."""
+    import synth
+    import oracle
+    from threadpoolctl import threadpool_limits
+
+    cfg = synth.get_config("tiny_fp32")
+    w = synth.make_weights(cfg, seed=0, device="cpu")
+    o = oracle.make_oracle(cfg, w)
+    prompt = synth.make_prompt(cfg, n=cfg.prompt_len[0])
+    steps = 16
+    with threadpool_limits(1):
+        st = o.prefill(prompt)
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            o.step(st)
+        dt = time.perf_counter() - t0
+    return {"value": round(steps * cfg.tree_tokens / dt, 2), "unit": "tree-tokens/s", "cores": 1,
+            "sample": f"{steps} oracle steps of tiny_fp32 after its {cfg.prompt_len[0]}-token prefill, one thread"}
+
+
 def cpu_baseline(cfg, seed=0):
     """The oracle, as written, on a bounded sample of the workload.
 
@@ -133,6 +155,7 @@ def cpu_baseline(cfg, seed=0):
         "sample": (f"{n_step} oracle steps of a 1-layer slice of {cfg.name} (T={T}, context {L}), "
                    f"mean {t_step:.2f}s, + {cfg.n_layers - 1} oracle decoder layers over the "
                    f"{T} tree rows {t_layers:.2f}s = {total:.2f}s per full step (float64 NumPy)"),
+        "single_thread_tiny": _tiny_single_thread(),
     }
 
 
