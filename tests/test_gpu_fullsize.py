@@ -9,14 +9,17 @@ Workloads (bf16, HIP-graph replay, the engine's default):
 - large_gqa_b1: 80 layers, d_model 8192, 64 query / 8 KV heads of 128, SwiGLU 28672,
   4 Clover heads with top-k (8, 4, 2, 2), batch 1, 2048-token prompt;
 - llama7b_b8 with speculative sampling at temperature 0.8 (`bench.py --workload llama7b_b8
-  --temperature 0.8`): the 512-row LM head's sampled argmax epilogue at full size.
+  --temperature 0.8`): the 512-row LM head's sampled argmax epilogue at full size;
+- llama7b_b1_medusa (`bench.py --draft medusa`): the Medusa heads on x_N of the last
+  committed token and their Cartesian-product tree, at the 7B shape.
 
 The float64 oracle cannot run these forwards in a test, so it recomputes sampled
 outputs one by one from the GPU's own inputs to that stage, and the discrete stages
 are checked exactly, for every sequence of the batch:
 
 - draft: the root's head-1 logits (Regressive Connection, Attention Decoder, head MLP,
-  final norm, shared LM head) from h0 and t0 (Sec. 3.1-3.4);
+  final norm, shared LM head) from h0 and t0 (Sec. 3.1-3.4); for Medusa every head's
+  logits (head MLP on h0, final norm, shared LM head);
 - top-k children of every frontier row of every depth, their cumulative log-probs, and
   the truncated tree and its ancestor mask, from the GPU's draft logits;
 - verify: final norm + LM head on sampled tree rows from the residual after the last
@@ -41,7 +44,7 @@ from tests.gpu_util import need_gpu, note
 pytestmark = pytest.mark.gpu
 
 LOGIT_TOL = 2e-2  # bf16 workloads: max-abs on logits
-WORKLOADS = ["llama7b_b1", "llama7b_b8", "large_gqa_b1", "llama7b_b8@0.8"]
+WORKLOADS = ["llama7b_b1", "llama7b_b8", "large_gqa_b1", "llama7b_b8@0.8", "llama7b_b1_medusa"]
 
 
 def _f64(t):
@@ -61,8 +64,10 @@ def run(request):
     w = synth.make_weights(cfg, seed=0, device="cuda")
     # the oracle's copies of what the sampled checks read, taken before packing frees the
     # device sources (the large model's weights and their packed copies would not both fit)
-    names = ["final_norm", "lm_head", "ad.norm", "ad.wq", "ad.wk", "ad.wv", "ad.wo",
-             "head0.w1", "head0.b1"] + [f"layer0.{f}" for f in LayerWeights.__dataclass_fields__]
+    medusa = cfg.draft == "medusa"
+    heads = [f"head{j}.{k}" for j in range(cfg.n_spec_heads if medusa else 1) for k in ("w1", "b1")]
+    names = (["final_norm", "lm_head"] + ([] if medusa else ["ad.norm", "ad.wq", "ad.wk", "ad.wv", "ad.wo"])
+             + heads + [f"layer0.{f}" for f in LayerWeights.__dataclass_fields__])
     host = {n: _f64(w[n]) for n in names}
     emb = w["emb"].cpu()
     eng = P.CloverEngine(cfg, w, max_batch=B, max_context=max(lens) + 256, free_source=True)
@@ -104,7 +109,8 @@ def run(request):
     }
     F = 1
     for j in range(1, H + 1):
-        r[f"draft_logits{j}"] = eng.debug(f"draft_logits{j}", np.float32, (B * F, V)).reshape(B, F, V)
+        rows = 1 if medusa else F  # Medusa: one row per head and sequence, whatever the depth
+        r[f"draft_logits{j}"] = eng.debug(f"draft_logits{j}", np.float32, (B * rows, V)).reshape(B, rows, V)
         F *= cfg.topk[j - 1]
     r["kv0"], r["emb_rows"] = [], []
     for b in seqs:
@@ -128,6 +134,14 @@ def test_fullsize_draft_root_row_matches_oracle(run):
     r = run
     cfg, w = r["cfg"], r["w"]
     prec = oracle.model.Precision(cfg.dtype)
+    if cfg.draft == "medusa":
+        for b in range(r["B"]):
+            for j in range(cfg.n_spec_heads):
+                rr = head_mlp(r["h0"][b], w[f"head{j}.w1"], w[f"head{j}.b1"], prec)
+                err = float(np.max(np.abs(r[f"draft_logits{j + 1}"][b][0] - _lm_logits(r, rr)[0])))
+                note(f"{cfg.name} Medusa head {j + 1} of sequence {b}: max |err| {err:.3e}")
+                assert err <= LOGIT_TOL, (b, j)
+        return
     for b in range(r["B"]):
         e = rc_embed(w["lm_head"], int(r["t0"][b]))
         s = attention_decoder(r["h0"][b], e, w, cfg.n_heads, cfg.head_dim, cfg.rms_eps, prec)
@@ -153,7 +167,8 @@ def test_fullsize_topk_lp_and_tree_exact(run):
             dl = r[f"draft_logits{j}"][b]
             nxt = []
             for f, node in enumerate(frontier):
-                logits = dl[f].astype(np.float64)
+                # Medusa: every node of the depth expands with the head's one list
+                logits = dl[0 if cfg.draft == "medusa" else f].astype(np.float64)
                 want = topk_ids(logits, k)
                 logp = logits - logsumexp(logits)
                 for c in range(k):
