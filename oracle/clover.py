@@ -27,8 +27,12 @@ Test infrastructure only.  Follows Sec. 3 of the paper:
   node decides which child, if any, is kept; the accepted path plus one bonus
   token is emitted, so outputs equal plain greedy decoding.
 
-Parity unpinned: the composition AB -> AD -> MLP -> LM head beyond the
-single-key closed form (the architecture figure is not available).
+Pinned parts of the head composition: the single-key closed form of the Attention
+Decoder, and the reduction with identity heads (no Augmenting Block, zero decoder
+output projection, an MLP that adds nothing), where every node's head logits must be
+the target's own next-token logits after the prompt.  Parity unpinned: the order of
+the Attention Decoder and the MLP inside a head, and the MLP's form, beyond these
+(the architecture figure is not available).
 """
 from dataclasses import dataclass, field
 from typing import Dict, List, Optional, Sequence, Tuple

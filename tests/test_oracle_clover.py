@@ -169,3 +169,50 @@ def test_tiny_workload_sixteen_steps_equal_greedy():
         o.step(st)
     n_new = st.L - len(prompt) + 1
     assert st.tokens[len(prompt):] + [st.t0] == o.base.greedy_generate(prompt, n_new)
+
+
+@pytest.mark.parametrize("draft", ["clover", "medusa"])
+def test_identity_heads_draft_the_targets_next_token_logits(draft):
+    """Sec. 3.3-3.4: the heads share the target's final norm and LM head and read the
+    state of the last committed token.  With no Augmenting Block, a zero decoder output
+    projection (the decoder then adds exactly zero) and head MLPs that add nothing
+    (W1 = 0, b1 = -200: SiLU(-200) is about -3e-85, below half an ulp of any state entry),
+    every node's head logits must be the target's own next-token logits after the prompt,
+    as a plain causal forward of the prompt gives them.  So every node of depth j-1 gets
+    the target's top-k_j as children, with the target's log-probabilities added in fp32,
+    and the root is the target's greedy choice."""
+    import torch
+    cfg = synth.tiny_test_config(draft=draft, ab="none", topk=(3, 2, 2), tree_tokens=12)
+    w = synth.make_weights(cfg, seed=9, perturb=True)
+    if draft == "clover":
+        w["ad.wo"] = w["ad.wo"] * 0
+    for j in range(cfg.n_spec_heads):
+        w[f"head{j}.w1"] = w[f"head{j}.w1"] * 0
+        w[f"head{j}.b1"] = torch.full_like(w[f"head{j}.b1"], -200.0)
+    o = oracle.make_oracle(cfg, w)
+    prompt = synth.make_prompt(cfg, n=13)
+    st = o.prefill(prompt)
+    ref = o.base.forward_full(prompt)[-1]
+    assert st.t0 == int(np.argmax(ref))
+    logp = (ref - oracle.logsumexp(ref)).astype(np.float32)
+    c = o.draft(st)
+    if draft == "medusa":
+        for lg in c.head_logits:
+            assert np.max(np.abs(lg - ref)) <= 1e-12
+    else:
+        assert len(c.row_logits) > 0
+        for lg in c.row_logits.values():
+            assert np.max(np.abs(lg - ref)) <= 1e-12
+    idx = 1
+    level = [0]
+    for j, k in enumerate(cfg.topk, start=1):
+        want = np.lexsort((np.arange(len(ref)), -ref))[:k]
+        nxt = []
+        for n in level:
+            for t in want:
+                assert c.depth[idx] == j and c.parent[idx] == n and c.token[idx] == t
+                assert c.lp[idx] == np.float32(np.float32(c.lp[n]) + logp[t])
+                nxt.append(idx)
+                idx += 1
+        level = nxt
+    assert idx == len(c.token)

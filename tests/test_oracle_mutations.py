@@ -134,3 +134,29 @@ def test_acceptance_pin_catches_wrong_index():
     tokens, parent, target = [9, 4, 6, 5], [-1, 0, 0, 2], [6, 4, 5, 0]
     assert oracle.accept(tokens, parent, target)[0] == _brute_accept(tokens, parent, target) == [0, 2, 3]
     assert accept_own(tokens, parent, target)[0] != _brute_accept(tokens, parent, target)
+
+
+def _prefill_state_of_wrong_row(self, prompt, slot=0):
+    st = _PREFILL(self, prompt, slot)
+    n = len(prompt)
+    x, _ = self.base.forward_rows(prompt, np.arange(n), None, np.tril(np.ones((n, n), dtype=bool)))
+    st.h0 = x[-2].copy()  # the state of the token before the last committed one
+    return st
+
+
+def _head_logits_without_final_norm(self, j, s):
+    r = oc.head_mlp(s, self.w[f"head{j}.w1"], self.w[f"head{j}.b1"], self.prec)
+    return self.prec.store(r[None, :])[0] @ self.w["lm_head"].T
+
+
+_PREFILL = oc.CloverOracle.prefill
+
+
+@pytest.mark.parametrize("draft", ["clover", "medusa"])
+@pytest.mark.parametrize("attr,mut", [("prefill", _prefill_state_of_wrong_row),
+                                      ("head_logits", _head_logits_without_final_norm)])
+def test_identity_head_pin_catches(monkeypatch, draft, attr, mut):
+    from tests.test_oracle_clover import test_identity_heads_draft_the_targets_next_token_logits as pin
+    monkeypatch.setattr(oc.CloverOracle, attr, mut)
+    with pytest.raises(AssertionError):
+        pin(draft)
