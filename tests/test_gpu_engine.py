@@ -542,3 +542,39 @@ def test_sampled_targets_match_oracle_sampler(which):
                 else:
                     same[s] = False
     note(f"sampling {which}: {near} near-tie draws skipped")
+
+
+def test_context_fills_then_step_is_refused_and_slot_is_reused():
+    """A sequence steps until its next tree no longer fits (committed tokens + T >
+    max_context): every step before that matches the oracle, the refused step returns
+    CAPACITY and leaves the sequence as it was, and a released slot takes a new prompt."""
+    P = need_gpu()
+    note("engine capacity: fill one sequence's context")
+    cfg, w = _tiny(batch=1)
+    T, cap = cfg.tree_tokens, 200
+    eng = _engine(P, cfg, w, max_context=cap)
+    o = oracle.CloverOracle(cfg, w)
+    prompt = synth.make_prompt(cfg, n=cap - T - 6)
+    st = o.prefill(prompt)
+    assert eng.prefill(0, prompt) == st.t0
+    steps = 0
+    while True:
+        L = eng.seq_len(0)
+        if L + T > cap:
+            with pytest.raises(P.CloverError) as e:
+                eng.step([0])
+            assert e.value.status == 2
+            assert eng.seq_len(0) == L
+            break
+        assert eng.step([0])[0] == o.step(st)[0], steps
+        assert eng.seq_len(0) == st.L
+        steps += 1
+        assert steps < 10
+    assert steps >= 1
+    eng.release(0)
+    prompt2 = synth.make_prompt(cfg, seq=1, n=40)
+    st2 = o.prefill(prompt2)
+    assert eng.prefill(0, prompt2) == st2.t0
+    for _ in range(3):
+        assert eng.step([0])[0] == o.step(st2)[0]
+    eng.close()
