@@ -293,7 +293,7 @@ def main():
     ap.add_argument("--draft", default="", choices=["", "clover", "medusa"],
                     help="override the speculator: Clover heads or the Medusa baseline")
     ap.add_argument("--ab", default="", choices=["", "default", "full", "attn", "mlp", "none"],
-                    help="override the Augmenting Block variant (Sec. 4.4)")
+                    help="override the Augmenting Block variant (Sec. 4.3)")
     ap.add_argument("--ad-keys", default="", choices=["", "single", "two", "path"],
                     help="override the Attention Decoder's key set (Eq. 1 readings)")
     ap.add_argument("--temperature", type=float, default=-1.0,

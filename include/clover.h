@@ -47,14 +47,14 @@ typedef enum { CLOVER_F32 = 0, CLOVER_BF16 = 1 } clover_dtype;
  *    Regressive Connection and Attention Decoder on every frontier node, the head's MLP
  *    and the shared LM head; the tree grows one regressive depth per head.
  *  CLOVER_DRAFT_MEDUSA: the Medusa baseline the paper compares against (Sec. 1, 2.3;
- *    Sec. 4.4: Clover without Attention Decoder, Regressive Connection and Augmenting
+ *    Sec. 4.3: Clover without Attention Decoder, Regressive Connection and Augmenting
  *    Block): every head reads the target's last hidden state of the last committed
  *    token, head j's top-k tokens become the depth-j children of every depth-(j-1) node
  *    (Cartesian product), and all heads share one LM-head pass.  There is no Augmenting
  *    Block and no Attention Decoder, so their weights are absent from the weight list. */
 typedef enum { CLOVER_DRAFT_CLOVER = 0, CLOVER_DRAFT_MEDUSA = 1 } clover_draft_mode;
 
-/* Augmenting Block variants explored in Sec. 4.4: a whole pre-norm transformer layer
+/* Augmenting Block variants explored in Sec. 4.3: a whole pre-norm transformer layer
  * (attention and MLP halves), the attention half only, the MLP half only, or none (the
  * heads then read x_N, the residual after the target's last layer).  Its output at the
  * last committed token is the drafting state h_0.  CLOVER_AB_DEFAULT is CLOVER_AB_FULL

@@ -11,12 +11,11 @@ GPU path stores in bf16 (weights, GEMM inputs, rotated queries and the KV
 cache) are rounded to bf16 at the same points (``Precision.store``), so the
 two sides differ only by accumulation order and fp32-vs-fp64 rounding.
 
-Parity status per function (see each docstring): everything is pinned by an
-invariant test except the composition of the Clover draft components
-(Augmenting Block -> Attention Decoder -> head MLP -> shared LM head), whose
-exact wiring comes from readings of Sec. 3 because the architecture figure is
-not available: "parity unpinned" beyond the single-key closed form and the
-node-count checks.
+Parity status per function (see each docstring): every function is pinned by an
+invariant test.  The composition of the Clover draft (Augmenting Block -> Attention
+Decoder -> head MLP -> shared LM head) is pinned by closed forms (single-key decoder,
+identity heads, the path sum of W_O W_V e along each root path); its wiring itself
+comes from readings of Sec. 3, because the architecture figure is not available.
 """
 from .model import (Precision, rmsnorm, rope, attention, silu, logsumexp,  # noqa: F401
                     LayerWeights, layer_forward, BaseModel)

@@ -27,12 +27,17 @@ Test infrastructure only.  Follows Sec. 3 of the paper:
   node decides which child, if any, is kept; the accepted path plus one bonus
   token is emitted, so outputs equal plain greedy decoding.
 
-Pinned parts of the head composition: the single-key closed form of the Attention
-Decoder, and the reduction with identity heads (no Augmenting Block, zero decoder
-output projection, an MLP that adds nothing), where every node's head logits must be
-the target's own next-token logits after the prompt.  Parity unpinned: the order of
-the Attention Decoder and the MLP inside a head, and the MLP's form, beyond these
-(the architecture figure is not available).
+Pins of the head composition (tests/test_oracle_clover.py): the single-key closed form
+of the Attention Decoder; the reduction with identity heads (no Augmenting Block, zero
+decoder output projection, an MLP that adds nothing), where every node's head logits
+must be the target's own next-token logits after the prompt; and the path-sum closed
+form, where with the single key, no Augmenting Block and head MLPs W1_j = alpha_j I
+every drafted row must equal W_lm RMSNorm_f(s + SiLU(alpha_j s + b1_j)) with
+s = h_0 + sum of W_O W_V e(tok) over the node's root path.  That one fixes the
+recursion of the decoder state, the token embedded at each depth, the head used at
+each depth, the order of decoder and MLP and the MLP's residual form; planted mistakes
+in each fail it.  What remains a reading rather than a pinned fact is the choice of
+these forms themselves (the architecture figure is not available).
 """
 from dataclasses import dataclass, field
 from typing import Dict, List, Optional, Sequence, Tuple
@@ -202,7 +207,7 @@ class CloverOracle:
 
     # -- Augmenting Block -------------------------------------------------------------------
     def ab_forward(self, x_rows, pos, ab_kv, tail_visible):
-        """Sec. 3.3 (and the variants of Sec. 4.4): the whole layer, its attention or MLP half,
+        """Sec. 3.3 (and the variants of Sec. 4.3): the whole layer, its attention or MLP half,
         or none (the rows pass through).  Returns (h, k_new, v_new); k/v None without attention."""
         c = self.cfg
         if self.ab_kind == "none":

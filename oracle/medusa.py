@@ -3,7 +3,7 @@
 The paper measures Clover against Medusa decoding (Sec. 1, Sec. 2.3, Sec. 4):
 parallel MLP heads that all read the hidden state of the last transformer block,
 head j speculating the token j places past the next one, and a token tree that
-is the Cartesian product of the heads' candidates.  Sec. 4.4 states that Clover
+is the Cartesian product of the heads' candidates.  Sec. 4.3 states that Clover
 with the Attention Decoder, the Regressive Connection and the Augmenting Block
 removed is that architecture, so the heads here are the Clover head block
 without the Attention Decoder and the Regressive Connection:
@@ -11,7 +11,7 @@ without the Attention Decoder and the Regressive Connection:
 * every head reads the drafting state h_0 of the last committed token: x_N (the
   residual after the last base layer) when there is no Augmenting Block -- the
   Medusa baseline -- or the Augmenting Block's output when one is configured
-  (Clover without Attention Decoder and Regressive Connection, Sec. 4.4);
+  (Clover without Attention Decoder and Regressive Connection, Sec. 4.3);
 * head j: r_j = h + SiLU(W1_j h + b1_j), logits_j = W_lm RMSNorm_f(r_j) with the
   target's final norm and shared LM head;
 * depth-j children of every depth-(j-1) node are head j's top-k_j tokens (value
@@ -24,8 +24,9 @@ Pins: speculative output equals greedy autoregressive output (the acceptance
 rule makes this hold for any draft); every depth-j node's children carry exactly
 head j's top-k_j tokens and log-probabilities (Cartesian structure); node
 counts; Clover with its output projections zeroed drafts the same trees.  The
-head block itself is the Clover head block (same readings), so its parity
-status is that of the Clover heads: parity unpinned beyond these.
+head block itself is the Clover head block (same readings), pinned by the identity
+heads reduction and by the path-sum closed form of the Clover oracle (its head MLP and
+shared LM head are the ones used here).
 """
 import numpy as np
 

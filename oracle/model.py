@@ -118,7 +118,7 @@ def layer_forward(x: np.ndarray, pos: np.ndarray, lw: LayerWeights, k_prefix: np
     The new rows see all ``k_prefix``/``v_prefix`` keys and the new rows' own keys
     where ``tail_visible`` is set.  Returns (x_out, k_new, v_new) with k_new after
     rotary, both in storage precision (what a KV cache holds).  ``attn`` / ``mlp``
-    keep the attention / MLP half (the Augmenting Block variants of Sec. 4.4); without
+    keep the attention / MLP half (the Augmenting Block variants of Sec. 4.3); without
     the attention half k_new and v_new are None.
     """
     k = v = None

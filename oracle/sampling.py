@@ -40,9 +40,15 @@ def philox4x32_10_w0(c0, c1, c2, c3, k0: int, k1: int) -> np.ndarray:
 
 
 def uniform_from_bits(x) -> np.ndarray:
-    """U in (0, 1) from the top 24 bits of each 32-bit word (exact in float32)."""
-    return ((np.asarray(x, dtype=np.uint32) >> np.uint32(8)).astype(np.float32) + np.float32(0.5)) \
-        * np.float32(2.0 ** -24)
+    """U = (m + 1/2) / 2^23 with m the top 23 bits of each 32-bit word.
+
+    m + 1/2 needs at most 24 significant bits, so the sum and the scaling are exact in
+    float32, and U runs over the midpoints 2^-24, 3 * 2^-24, ..., 1 - 2^-24: strictly
+    inside (0, 1), which keeps both logarithms of the Gumbel transform finite.  (With
+    the top 24 bits the sum m + 1/2 would need 25 bits and round, up to 1.0 for the
+    largest words.)"""
+    return ((np.asarray(x, dtype=np.uint32) >> np.uint32(9)).astype(np.float32) + np.float32(0.5)) \
+        * np.float32(2.0 ** -23)
 
 
 def gumbel_from_bits(x) -> np.ndarray:

@@ -713,7 +713,7 @@ hipError_t enq_tree(clover_ctx* c, int B);
 // Medusa draft (the paper's baseline, Sec. 2.3): every head reads the state h_0 of the last
 // committed token -- x_N, or the Augmenting Block's output when one is configured; head j:
 // r = h + SiLU(W1_j h + b1_j), logits = W_lm RMSNorm_f(r) -- the Clover head block without
-// Attention Decoder and Regressive Connection (Sec. 4.4).  The heads' rows share one
+// Attention Decoder and Regressive Connection (Sec. 4.3).  The heads' rows share one
 // LM-head pass; their top-k lists span the candidate tree as a Cartesian product.
 hipError_t enq_draft_medusa(clover_ctx* c, int B) {
   const clover_config& cf = c->cfg;

@@ -161,8 +161,10 @@ __device__ __forceinline__ uint32_t philox4x32_10_w0(uint32_t c0, uint32_t c1, u
   return c0;
 }
 
-// Standard Gumbel noise -log(-log(u)) from the top 24 bits of a 32-bit word, u in (0, 1).
+// Standard Gumbel noise -log(-log(u)) from a 32-bit word: u = (m + 1/2) * 2^-23 with m the
+// top 23 bits.  m + 1/2 fits the 24-bit float significand, so u is exact and lies in
+// [2^-24, 1 - 2^-24]: both logarithms stay finite.
 __device__ __forceinline__ float gumbel_from_bits(uint32_t x) {
-  const float u = ((float)(x >> 8) + 0.5f) * 5.9604644775390625e-08f;  // 2^-24
+  const float u = ((float)(x >> 9) + 0.5f) * 1.1920928955078125e-07f;  // 2^-23
   return -logf(-logf(u));
 }

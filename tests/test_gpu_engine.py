@@ -185,9 +185,83 @@ def _bf16_small():
                               tree_tokens=20, batch=1, prompt_len=(100, 100), steps=6, max_context=512)
 
 
+def _margin_k(logits, k):
+    """Gap between the k-th and (k+1)-th largest values (the top-k decision's margin)."""
+    v = np.sort(logits)[::-1]
+    return float(v[k - 1] - v[k]) if k < len(v) else np.inf
+
+
+def teacher_forced_step(eng, o, states, tol, stats):
+    """One step of every sequence 0..B-1 on the GPU, with the oracle teacher-forced onto it.
+
+    Each oracle drafts from its own state; draft logits are compared for every depth whose
+    frontier nodes (the candidates of all shallower depths) agree with the GPU's, and where
+    they disagree the oracle's own top-k decision there must be a near tie (margin < 2 tol).
+    The oracle then verifies the GPU's tree (all T rows compared), checks that its own
+    acceptance agrees with the GPU's unless a target is a near tie, and commits the GPU's
+    accepted path and bonus, so the next step starts from the same tokens on both sides and
+    every step is compared.  stats counts compared rows and near-tie decisions."""
+    c = o.cfg
+    B, T, V, H = len(states), c.tree_tokens, c.vocab, c.n_spec_heads
+    got = eng.step(list(range(B)))
+    n_cand = 1 + c.n_candidates()
+    gtok = eng.debug("cand_token", np.int32, (eng.c.max_batch, n_cand))
+    trees = eng.debug("tree_token", np.int32, (eng.c.max_batch, T))
+    parents = eng.debug("tree_parent", np.int32, (eng.c.max_batch, T))
+    vl = eng.debug("verify_logits", np.float32, (B * T, V))
+    accs = eng.debug("acc", np.int32, (eng.c.max_batch, H + 1))
+    alen = eng.debug("acc_len", np.int32, (eng.c.max_batch,))
+    medusa = getattr(c, "draft", "clover") == "medusa"
+    F = 1
+    dl = []
+    for j in range(1, H + 1):
+        rows = B if medusa else B * F
+        dl.append(eng.debug(f"draft_logits{j}", np.float32, (rows, V)))
+        F *= c.topk[j - 1]
+    for b, st in enumerate(states):
+        cands = o.draft(st)
+        F, base = 1, 0
+        for j in range(1, H + 1):
+            if medusa:
+                err = float(np.max(np.abs(dl[j - 1][b] - cands.head_logits[j - 1])))
+                assert err < tol, (b, j, err)
+                stats["draft_rows"] += 1
+                continue
+            if not np.array_equal(gtok[b, :base + F], cands.token[:base + F]):
+                # a near tie in a shallower top-k made different frontier nodes
+                assert min(_margin_k(cands.row_logits[n], c.topk[cands.depth[n]])
+                           for n in cands.row_logits if cands.depth[n] < j - 1) < 2 * tol, (b, j)
+                stats["draft_ties"] += 1
+                break
+            for f in range(F):
+                err = float(np.max(np.abs(dl[j - 1][b * F + f] - cands.row_logits[base + f])))
+                assert err < tol, (b, j, f, err)
+                stats["draft_rows"] += 1
+            base += F
+            F *= c.topk[j - 1]
+        tree = o.planted_tree(st, trees[b], parents[b])
+        ver = o.verify(st, tree)
+        err = float(np.max(np.abs(vl[b * T:(b + 1) * T] - ver.logits)))
+        assert err < tol, (b, err)
+        stats["verify_rows"] += T
+        acc_g = [int(a) for a in accs[b, :alen[b]]]
+        acc_o, bonus_o = oracle.accept(tree.tokens, tree.parent, ver.target)
+        emitted_g = got[b]
+        assert emitted_g == [int(tree.tokens[i]) for i in acc_g[1:]] + [emitted_g[-1]]
+        if acc_o != acc_g or bonus_o != emitted_g[-1]:
+            top2 = np.sort(ver.logits[sorted(set(acc_o) | set(acc_g))], axis=1)[:, -2:]
+            assert float(np.min(top2[:, 1] - top2[:, 0])) < 2 * tol, (b, acc_o, acc_g)
+            stats["target_ties"] += 1
+        o.commit(st, tree, ver, acc_g, emitted_g[-1])
+        stats["steps"] += 1
+    return got
+
+
 def test_bf16_small_model_within_tolerance():
-    """bf16 storage: logits within 2e-2 of the oracle (which rounds at the same
-    storage points); discrete results compared while no decision is a near tie."""
+    """bf16 storage: draft and verify logits within 2e-2 of the oracle (which rounds at
+    the same storage points) at every step; the oracle is teacher-forced onto the GPU's
+    trees and accepted paths, and its own discrete decisions must agree wherever they are
+    not near ties."""
     P = need_gpu()
     note("engine bf16 small")
     cfg = _bf16_small()
@@ -198,32 +272,12 @@ def test_bf16_small_model_within_tolerance():
     t0 = eng.prefill(0, prompt)
     st = o.prefill(prompt)
     assert t0 == st.t0
-    tol = 2e-2
-    for step in range(6):
-        ours = eng.step([0])[0]
-        ref, det = o.step(st)
-        cands = det["cands"]
-        F, base = 1, 0
-        for j in range(1, cfg.n_spec_heads + 1):
-            dl = eng.debug(f"draft_logits{j}", np.float32, (F, cfg.vocab))
-            for f in range(F):
-                err = np.max(np.abs(dl[f] - cands.row_logits[base + f]))
-                assert err < tol, (step, j, f, err)
-            base += F
-            F *= cfg.topk[j - 1]
-        T = cfg.tree_tokens
-        same_tree = np.array_equal(eng.debug("tree_token", np.int32, (1, T))[0], det["tree"].tokens)
-        if not same_tree:
-            # only a near tie in the draft may separate the trees
-            margins = [np.sort(l)[::-1] for l in cands.row_logits.values()]
-            assert min(m[k - 1] - m[k] for m, k in zip(margins, [cfg.topk[cands.depth[n]] for n in cands.row_logits])) < 2 * tol
-            break
-        vl = eng.debug("verify_logits", np.float32, (T, cfg.vocab))
-        assert np.max(np.abs(vl - det["ver"].logits)) < tol
-        top2 = np.sort(det["ver"].logits, axis=1)[:, -2:]
-        if np.min(top2[:, 1] - top2[:, 0]) < 2 * tol:
-            break
-        assert ours == ref, step
+    stats = dict(steps=0, draft_rows=0, verify_rows=0, draft_ties=0, target_ties=0)
+    for _ in range(6):
+        teacher_forced_step(eng, o, [st], 2e-2, stats)
+    note(f"bf16 small: {stats}")
+    assert stats["steps"] == 6 and stats["verify_rows"] == 6 * cfg.tree_tokens
+    assert stats["draft_rows"] >= 6 * 5  # at least the root and depth-1 rows of every step
 
 
 def _kv_close(got, ref, layer=0):
@@ -282,10 +336,13 @@ def test_bf16_128_row_verify_and_chunked_prefill():
     top2 = np.sort(ver.logits, axis=1)[:, -2:]
     if np.min(top2[:, 1] - top2[:, 0]) >= 4e-2:  # no near tie decides a target
         assert got == ref
-        for j, node in enumerate(acc):
-            for which in (0, 1):
-                g = eng.debug_kv(0, 0, L + j, bool(which))
-                assert _kv_close(g, st.kv[0][which][L + j].reshape(-1)), (j, which)
+    # the committed K/V of the GPU's accepted path are its tree nodes' K/V (the oracle's
+    # tree-node values, taken at the GPU's own acceptance)
+    acc_g = eng.debug("acc", np.int32, (1, cfg.n_spec_heads + 1))[0][:len(got)]
+    for j, node in enumerate(acc_g):
+        for which in (0, 1):
+            g = eng.debug_kv(0, 0, L + j, bool(which))
+            assert _kv_close(g, ver.kv[0][which][node].reshape(-1)), (j, which)
 
 
 def test_bf16_batch_of_eight_verify_rows():
@@ -403,7 +460,8 @@ def test_medusa_tiny_fp32_sixteen_steps_match_oracle_and_greedy():
 
 def test_medusa_bf16_batch_of_three_within_tolerance():
     """bf16 Medusa over three sequences of different lengths: each sequence's head logits
-    within 2e-2 of its oracle; trees and tokens compared while no decision is a near tie."""
+    and verify logits within 2e-2 of its oracle at every step, with the oracle
+    teacher-forced onto the GPU's trees and accepted paths."""
     P = need_gpu()
     note("engine medusa bf16 batch 3")
     cfg = _bf16_small().with_(draft="medusa", batch=3)
@@ -416,28 +474,12 @@ def test_medusa_bf16_batch_of_three_within_tolerance():
         prompt = synth.make_prompt(cfg, seq=s, n=lens[s])
         assert eng.prefill(s, prompt) == (st := o.prefill(prompt)).t0
         states.append(st)
-    B, T, V = 3, cfg.tree_tokens, cfg.vocab
-    for step in range(3):
-        got = eng.step([0, 1, 2])
-        trees = eng.debug("tree_token", np.int32, (B, T))
-        vl = eng.debug("verify_logits", np.float32, (B * T, V))
-        heads = [eng.debug(f"draft_logits{j}", np.float32, (B, V)) for j in range(1, cfg.n_spec_heads + 1)]
-        same = True
-        for b in range(B):
-            ref, det = o.step(states[b])
-            for j in range(cfg.n_spec_heads):
-                assert float(np.max(np.abs(heads[j][b] - det["cands"].head_logits[j]))) < 2e-2, (step, b, j)
-            if not np.array_equal(trees[b], det["tree"].tokens):
-                same = False
-                continue
-            assert float(np.max(np.abs(vl[b * T:(b + 1) * T] - det["ver"].logits))) < 2e-2
-            top2 = np.sort(det["ver"].logits, axis=1)[:, -2:]
-            if np.min(top2[:, 1] - top2[:, 0]) >= 4e-2:
-                assert got[b] == ref, (step, b)
-            else:
-                same = False
-        if not same:
-            break
+    stats = dict(steps=0, draft_rows=0, verify_rows=0, draft_ties=0, target_ties=0)
+    for _ in range(3):
+        teacher_forced_step(eng, o, states, 2e-2, stats)
+    note(f"medusa bf16 batch 3: {stats}")
+    assert stats["steps"] == 9 and stats["draft_rows"] == 9 * cfg.n_spec_heads
+    assert stats["verify_rows"] == 9 * cfg.tree_tokens
 
 
 @pytest.mark.parametrize("draft,ab,ad_keys,per_head", [
@@ -446,7 +488,7 @@ def test_medusa_bf16_batch_of_three_within_tolerance():
     ("clover", "default", "two", False), ("clover", "default", "path", False),
     ("clover", "default", "two", True)])
 def test_speculator_variants_match_oracle(draft, ab, ad_keys, per_head):
-    """The Augmenting Block variants of Sec. 4.4 (attention half, MLP half, none) under the
+    """The Augmenting Block variants of Sec. 4.3 (attention half, MLP half, none) under the
     Clover draft, the Augmenting Block feeding parallel heads (Clover without Attention
     Decoder and Regressive Connection), and the two-token and root-path key sets of the
     Attention Decoder, and one decoder per head: tiny fp32, six steps, draft logits of every

@@ -9,9 +9,10 @@ from oracle import Precision, attention, logsumexp, rmsnorm, rope
 from oracle.model import BaseModel
 
 
-def _torch_forward_full(cfg, w, tokens):
+def _torch_forward_full(cfg, w, tokens, residual=False):
     """Independent float64 torch implementation: SDPA with a boolean mask, torch rms_norm,
-    complex-number rotary, F.silu."""
+    complex-number rotary, F.silu.  Returns the logits of every row, or with residual=True
+    the residual stream after the last layer (before the final norm)."""
     W = {k: v.double() for k, v in w.items()}
     n, hd, H, Hk = len(tokens), cfg.head_dim, cfg.n_heads, cfg.n_kv_heads
     x = W["emb"][torch.tensor(tokens)]
@@ -36,6 +37,8 @@ def _torch_forward_full(cfg, w, tokens):
         x = x + o.transpose(0, 1).reshape(n, H * hd) @ W[p + "wo"].T
         m = F.rms_norm(x, (cfg.d_model,), W[p + "mlp_norm"], cfg.rms_eps)
         x = x + (F.silu(m @ W[p + "w_gate"].T) * (m @ W[p + "w_up"].T)) @ W[p + "w_down"].T
+    if residual:
+        return x.numpy()
     xf = F.rms_norm(x, (cfg.d_model,), W["final_norm"], cfg.rms_eps)
     return (xf @ W["lm_head"].T).numpy()
 

@@ -216,3 +216,59 @@ def test_identity_heads_draft_the_targets_next_token_logits(draft):
                 idx += 1
         level = nxt
     assert idx == len(c.token)
+
+
+def _rms(x, g, eps):
+    return x / np.sqrt(np.mean(x * x) + eps) * g
+
+
+def path_sum_pin(alphas=(0.7, -1.3, 2.1), seed=11):
+    """Closed form of the Clover draft (Sec. 3.1 Regressive Connection; Sec. 3.2 Eq. 1-2
+    and the recursion of h_i; Sec. 3.4 shared LM head).  With the single-key decoder the
+    softmax weight is exactly 1, so each depth adds W_O W_V e(token) to the state it
+    receives, and the state passed on is the decoder's output.  Without an Augmenting
+    Block, h_0 is the target's residual at the last prompt row.  So the decoder output at
+    node n is
+
+        s(n) = h_0 + sum over the tokens m on n's root path (root and n included) of
+               W_O W_V e(tok_m),  e(t) = W_lm[t] / ||W_lm[t]||,
+
+    and the head of n's depth (head j for nodes of depth j, 0-based) turns it into logits
+    W_lm RMSNorm_f(s + SiLU(W1_j s + b1_j)).  With W1_j = alpha_j I the MLP acts element by
+    element, so a mix-up of heads, a missing residual or a swapped order of decoder and MLP
+    changes the values.  Returns the largest error over every drafted row."""
+    import torch
+    cfg = synth.tiny_test_config(ab="none", topk=(3, 2, 2), tree_tokens=12)
+    w = synth.make_weights(cfg, seed=seed, perturb=True)
+    d = cfg.d_model
+    for j, a in enumerate(alphas[:cfg.n_spec_heads]):
+        w[f"head{j}.w1"] = torch.eye(d) * a
+    o = CloverOracle(cfg, w)
+    prompt = synth.make_prompt(cfg, n=11)
+    st = o.prefill(prompt)
+    # h_0 without an Augmenting Block: the residual after the last target layer at the
+    # prompt's last row, from the torch float64 forward that pins the base model
+    from tests.test_oracle_base import _torch_forward_full
+    h0 = _torch_forward_full(cfg, w, prompt, residual=True)[-1]
+    W = {k: v.double().numpy() for k, v in w.items()}
+    ov = W["ad.wo"] @ W["ad.wv"]
+    c = o.draft(st)
+    err = float(np.max(np.abs(st.h0 - h0)))
+    for n, logits in c.row_logits.items():
+        s = h0.copy()
+        m = n
+        while m >= 0:
+            row = W["lm_head"][c.token[m]]
+            s = s + ov @ (row / np.linalg.norm(row))
+            m = c.parent[m]
+        j = int(c.depth[n])
+        z = W[f"head{j}.w1"][0, 0] * s + W[f"head{j}.b1"]  # alpha_j as stored (fp32)
+        r = s + z / (1 + np.exp(-z))
+        want = W["lm_head"] @ _rms(r, W["final_norm"], cfg.rms_eps)
+        err = max(err, float(np.max(np.abs(logits - want))))
+    assert len(c.row_logits) == 1 + 3 + 6
+    return err
+
+
+def test_clover_draft_equals_path_sum_closed_form():
+    assert path_sum_pin() < 1e-10

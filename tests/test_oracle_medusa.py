@@ -4,7 +4,7 @@ Each pin holds by the method's definition, not by retyping the oracle:
 - greedy speculative output equals greedy autoregressive output (Sec. 1, 2.1);
 - the candidate tree is the Cartesian product of the heads' top-k sets (Sec. 1, 2.3):
   brute force over every root path;
-- Sec. 4.4: Clover with the Attention Decoder, the Regressive Connection and the
+- Sec. 4.3: Clover with the Attention Decoder, the Regressive Connection and the
   Augmenting Block removed is Medusa.  With their output projections zeroed the
   Augmenting Block and the Attention Decoder are exactly the identity, so the Clover
   oracle then drafts the very tree the Medusa oracle drafts, step after step.
@@ -70,7 +70,7 @@ def test_medusa_tree_is_cartesian_product(topk):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_clover_without_its_three_components_is_medusa(dtype):
-    """Sec. 4.4: zero the Augmenting Block's attention and MLP output projections and the
+    """Sec. 4.3: zero the Augmenting Block's attention and MLP output projections and the
     Attention Decoder's output projection; the Clover oracle's candidate trees, verify
     trees and emitted tokens then equal the Medusa oracle's on the same base and heads."""
     cfg_m = synth.tiny_test_config(draft="medusa", dtype=dtype, topk=(3, 2, 2), tree_tokens=12)
@@ -120,7 +120,7 @@ def _same(a, b):
 @pytest.mark.parametrize("variant,zeroed", [("attn", ("ab.w_down",)), ("mlp", ("ab.wo",)),
                                             ("none", ("ab.wo", "ab.w_down"))])
 def test_augmenting_block_variants_are_the_full_block_with_a_half_removed(variant, zeroed):
-    """Sec. 4.4 explores the Augmenting Block as a whole layer, its attention half, its MLP
+    """Sec. 4.3 explores the Augmenting Block as a whole layer, its attention half, its MLP
     half, or none.  A half contributes exactly nothing when its output projection is zero,
     so each variant must draft, verify and emit exactly what the full block does with the
     other half's output projection zeroed."""
@@ -135,7 +135,7 @@ def test_augmenting_block_variants_are_the_full_block_with_a_half_removed(varian
 
 
 def test_medusa_heads_on_the_augmenting_block_are_clover_without_ad_and_rc():
-    """Sec. 4.4: Clover without the Attention Decoder (and with it the Regressive
+    """Sec. 4.3: Clover without the Attention Decoder (and with it the Regressive
     Connection) keeps the Augmenting Block and drafts with parallel heads.  The Clover
     oracle with a zero decoder output projection drafts exactly that Cartesian tree."""
     cfg_m = synth.tiny_test_config(draft="medusa", ab="full", topk=(3, 2, 2), tree_tokens=12)

@@ -160,3 +160,51 @@ def test_identity_head_pin_catches(monkeypatch, draft, attr, mut):
     monkeypatch.setattr(oc.CloverOracle, attr, mut)
     with pytest.raises(AssertionError):
         pin(draft)
+
+
+def _mutated_method(cls, name, old, new):
+    """A copy of cls.name with one planted mistake: the source text old replaced by new
+    (old must occur exactly once, so the mutation tracks the oracle's text)."""
+    import inspect
+    import textwrap
+    src = textwrap.dedent(inspect.getsource(getattr(cls, name)))
+    assert src.count(old) == 1, (name, old)
+    ns = dict(vars(oc))
+    exec(compile(src.replace(old, new), f"<mutated {name}>", "exec"), ns)
+    return ns[name]
+
+
+# plausible mistakes in the Clover draft composition (Sec. 3.1, 3.2 Eq. 1-2)
+_DRAFT_MUTATIONS = {
+    # no recursion: every depth's decoder reads h_0 instead of its parent's output
+    "no_recursion": ("draft", "state[len(depth) - 1] = s", "state[len(depth) - 1] = st.h0"),
+    # the root token's embedding at every depth instead of the node's own token
+    "root_token_embedded": ("ad_keys", 'e = rc_embed(self.w["lm_head"], token[n])',
+                            'e = rc_embed(self.w["lm_head"], token[0])'),
+    # the next depth receives the head MLP's output instead of the decoder's
+    "mlp_output_propagated": ("draft", "state[len(depth) - 1] = s",
+                              'state[len(depth) - 1] = head_mlp(s, self.w[f"head{j - 1}.w1"], '
+                              'self.w[f"head{j - 1}.b1"], self.prec)'),
+    # depth j drafted with the next head's MLP
+    "wrong_head": ("draft", "logits = self.head_logits(j - 1, s)",
+                   "logits = self.head_logits(j % c.n_spec_heads, s)"),
+}
+
+
+@pytest.mark.parametrize("which", sorted(_DRAFT_MUTATIONS))
+def test_path_sum_pin_catches(monkeypatch, which):
+    from tests.test_oracle_clover import path_sum_pin
+    assert path_sum_pin() < 1e-10
+    name, old, new = _DRAFT_MUTATIONS[which]
+    monkeypatch.setattr(oc.CloverOracle, name, _mutated_method(oc.CloverOracle, name, old, new))
+    assert path_sum_pin() > 1e-6
+
+
+def _head_mlp_no_residual(s, w1, b1, prec):
+    return om.silu(prec.store(s) @ w1.T + b1)
+
+
+def test_path_sum_pin_catches_mlp_without_residual(monkeypatch):
+    from tests.test_oracle_clover import path_sum_pin
+    monkeypatch.setattr(oc, "head_mlp", _head_mlp_no_residual)
+    assert path_sum_pin() > 1e-6

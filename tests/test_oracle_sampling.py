@@ -49,6 +49,26 @@ def test_philox_words_are_uniform():
     assert np.mean(x == y) < 1e-3 and np.mean(x == z) < 1e-3
 
 
+def test_uniform_mapping_is_exact_and_open_at_the_extreme_words():
+    """U must stay strictly inside (0, 1) for every 32-bit word, so the Gumbel noise is
+    finite; the extremes are the words with the top 23 bits all zero or all one, which a
+    uniform sample of 2^17 words almost never reaches."""
+    words = np.array([0, 0x1FF, 0x200, 0xFFFFFE00, 0xFFFFFF00, 0xFFFFFFFF], dtype=np.uint32)
+    u = sampling.uniform_from_bits(words)
+    assert u.dtype == np.float32
+    assert np.all(u > 0) and np.all(u < 1)
+    # exact: U = (m + 1/2) / 2^23 with m = word >> 9, compared in float64
+    m = (words >> np.uint32(9)).astype(np.float64)
+    assert np.array_equal(u.astype(np.float64), (m + 0.5) / 2.0 ** 23)
+    assert float(u[0]) == 2.0 ** -24 and float(u[-1]) == 1.0 - 2.0 ** -24
+    with np.errstate(all="raise"):
+        g = sampling.gumbel_from_bits(words)
+    assert np.all(np.isfinite(g))
+    # monotone in the top 23 bits: words 0, 0x200 and 0xFFFFFFFF give rising noise, and
+    # the low 9 bits do not matter (0xFFFFFE00 and 0xFFFFFFFF share their top 23 bits)
+    assert g[0] < g[2] < g[5] and g[3] == g[5] and g[0] == g[1]
+
+
 def test_gumbel_max_samples_the_softmax():
     rng = np.random.default_rng(0)
     logits = rng.standard_normal(12).astype(np.float32) * 1.5
