@@ -296,6 +296,9 @@ def main():
                     help="override the Augmenting Block variant (Sec. 4.3)")
     ap.add_argument("--ad-keys", default="", choices=["", "single", "two", "path"],
                     help="override the Attention Decoder's key set (Eq. 1 readings)")
+    ap.add_argument("--regressive", default="", choices=["", "attention", "mlp"],
+                    help="override the Clover draft's regressive block: the Attention Decoder or the "
+                         "MLP over [RMSNorm(h); e] of the components ablation (Sec. 4.3)")
     ap.add_argument("--temperature", type=float, default=-1.0,
                     help="override the sampling temperature (0: greedy; > 0: speculative sampling)")
     ap.add_argument("--surface", action="store_true",
@@ -330,6 +333,8 @@ def main():
         over["ab"] = args.ab
     if args.ad_keys:
         over["ad_keys"] = args.ad_keys
+    if args.regressive:
+        over["regressive"] = args.regressive
     if args.temperature >= 0:
         over["temperature"] = args.temperature
     if over:
@@ -411,7 +416,8 @@ def main():
         "dtype": cfg.dtype,
         "data": "synthetic: random-init N(0,0.02) weights, uniform-random prompt tokens",
         "config": {"workload": cfg.name, "speculator": cfg.draft, "augmenting_block": cfg.ab_kind,
-                   "decoder_keys": cfg.ad_keys, "temperature": cfg.temperature,
+                   "decoder_keys": cfg.ad_keys, "regressive_block": cfg.regressive,
+                   "temperature": cfg.temperature,
                    "n_layers": cfg.n_layers, "d_model": d,
                    "n_heads": cfg.n_heads, "n_kv_heads": cfg.n_kv_heads, "head_dim": cfg.head_dim,
                    "ffn_dim": F, "vocab": V, "spec_heads": cfg.n_spec_heads, "topk": list(cfg.topk),

@@ -80,6 +80,16 @@ typedef enum {
   CLOVER_AD_KEYS_PATH = 2    /* { e_0, ..., e_{i-1} } along the root path */
 } clover_ad_keys;
 
+/* Regressive block of the Clover draft.  The Attention Decoder (Sec. 3.2, Eq. 1-2) is the
+ * paper's choice; its ablation (Sec. 3.2 last paragraph, Sec. 4.3 "Ablations on
+ * Components") replaces it by an MLP over the two input vectors concatenated:
+ *   h_i = h_{i-1} + SiLU(W_r [RMSNorm_r(h_{i-1}); e_{i-1}] + b_r),
+ * W_r of shape [d_model, 2 d_model] (weights rb.norm, rb.w, rb.b), shared by the heads. */
+typedef enum {
+  CLOVER_REGRESSIVE_ATTENTION = 0, /* Attention Decoder (default) */
+  CLOVER_REGRESSIVE_MLP = 1        /* MLP over [RMSNorm_r(h); e] */
+} clover_regressive;
+
 #define CLOVER_MAX_HEADS 8
 
 /* Model and decoding configuration.  The target model is a pre-norm decoder
@@ -117,9 +127,16 @@ typedef struct {
                            follows the child carrying the node's sample, so every emitted token
                            is a sample of the target given the tokens before it */
   uint32_t sample_seed;
+  int32_t regressive;   /* clover_regressive (Clover draft); with CLOVER_REGRESSIVE_MLP, ad_keys
+                           must be single and ad_per_head 0 */
 } clover_config;
 
-#define CLOVER_FLAG_KEEP_LOGITS 1 /* keep draft and verify logits of the last step readable */
+#define CLOVER_FLAG_KEEP_LOGITS 1 /* the verify and prefill LM heads also store their fp32 logits,
+                                     readable as "verify_logits" until the next step or prefill;
+                                     without it they store only the per-row argmax keys the
+                                     target's choices need, and "verify_logits" keeps whatever
+                                     an earlier flagged call left (the draft logits are always
+                                     stored: top-k reads them) */
 #define CLOVER_FLAG_PROFILE 2     /* time every kernel launch with HIP events (clover_kernel_stats);
                                      implies CLOVER_FLAG_EAGER */
 #define CLOVER_FLAG_EAGER 4       /* launch the step's kernels one by one instead of replaying the
@@ -139,7 +156,8 @@ clover_status clover_check_config(const clover_config* cfg);
  * (Sec. 3.2, Eq. 1-2), head{j}.* the per-head MLP layers; lm_head is shared by all
  * heads and supplies the Regressive Connection embeddings (Sec. 3.4).  With
  * CLOVER_DRAFT_MEDUSA the ad.* entries are left out; with ad_per_head they are
- * ad{j}.{norm,wq,wk,wv,wo} for each head j instead of one ad.* set; the ab.* entries are those of the
+ * ad{j}.{norm,wq,wk,wv,wo} for each head j instead of one ad.* set; with CLOVER_REGRESSIVE_MLP
+ * they are rb.{norm [d], w [d, 2d], b [d]} instead of ad.*; the ab.* entries are those of the
  * Augmenting Block's halves that clover_ab_mode keeps (attn_norm, wq, wk, wv, wo for the
  * attention half, mlp_norm, w_gate, w_up, w_down for the MLP half). */
 size_t clover_weight_count(const clover_config* cfg);
@@ -224,6 +242,16 @@ clover_status clover_debug_read(clover_ctx* ctx, const char* name, void* host_ds
 clover_status clover_debug_kv(clover_ctx* ctx, int32_t seq, int32_t layer, int32_t pos,
                               int32_t which_v, float* host_out);
 
+/* Residual-stream trace (test hook for layer-by-layer parity).  While dev_buf is set, every
+ * prefill chunk, step and planted-tree verify of rows rows writes f32 [n_layers + 2][rows]
+ * [d_model] into dev_buf (device, caller-owned): slot l < n_layers holds the residual stream
+ * entering target layer l (embedding for l = 0), slot n_layers the residual after the last
+ * layer (x_N) and slot n_layers + 1 the Augmenting Block's output (x_N without one).  Rows
+ * are those of the launch (batch order, tree nodes in order).  Traced calls launch eagerly
+ * and fail with CAPACITY (state unchanged) when (n_layers + 2) * rows * d_model * 4 exceeds
+ * bytes.  dev_buf NULL switches the trace off. */
+clover_status clover_debug_trace(clover_ctx* ctx, float* dev_buf, size_t bytes);
+
 typedef struct {
   float draft_ms, verify_ms, accept_ms, total_ms; /* last step, measured with HIP events */
   int32_t steps;
@@ -307,6 +335,21 @@ clover_status clover_op_tree_build(const int32_t* cand_token, const int32_t* can
 clover_status clover_op_accept(const int32_t* tokens, const int32_t* parent, const int32_t* target,
                                int32_t T, int32_t max_depth, int32_t* acc, int32_t* acc_len,
                                int32_t* bonus, void* hip_stream);
+
+/* KV compaction after acceptance (the step's commit; Sec. 2.1 keeps only the accepted
+ * path): for every layer, the K and V rows of tree slot L + acc[j] move to slot L + j,
+ * j = 0..A-1.  A destination may be an earlier source (acc[j] >= j), so every source is
+ * read before any destination is written; slots other than L..L+A-1 are untouched.
+ * kcache / vcache: device pools [n_layers][n_blocks][n_kv][16 * head_dim] in the library's
+ * paged layout (storage dtype); block_table: host [n_table] physical block of each 16-slot
+ * page of the sequence, each in [0, n_blocks); acc: host [A], 1 <= A <= 9, every
+ * L + max(acc[j], j) < 16 * n_table.  scratch: device memory of at least 4 * (n_table + A)
+ * bytes the call stages the two arrays in.  Synchronises hip_stream before returning.
+ * Errors: INVALID_ARG (any bound above), CAPACITY (scratch too small), DEVICE. */
+clover_status clover_op_compact(int32_t dtype, void* kcache, void* vcache, int32_t n_layers, int32_t n_blocks,
+                                int32_t n_kv, int32_t head_dim, const int32_t* block_table, int32_t n_table,
+                                int32_t L, const int32_t* acc, int32_t A, void* scratch, size_t scratch_bytes,
+                                void* hip_stream);
 
 #ifdef __cplusplus
 }

@@ -87,6 +87,15 @@ def attention_decoder(h: np.ndarray, e_keys: np.ndarray, w: Dict[str, np.ndarray
     return h + prec.store(o) @ w["ad.wo"].T
 
 
+def regressive_mlp(h: np.ndarray, e: np.ndarray, w: Dict[str, np.ndarray], eps: float,
+                   prec: Precision) -> np.ndarray:
+    """The MLP regressive block of the ablation (Sec. 3.2 last paragraph, Sec. 4.3): the two
+    input vectors concatenated, h_i = h + SiLU(W_r [RMSNorm_r(h); e] + b_r)."""
+    a = prec.store(rmsnorm(h, w["rb.norm"], eps))
+    x = np.concatenate([a, prec.store(e)])
+    return h + silu(x @ w["rb.w"].T + w["rb.b"])
+
+
 def head_mlp(s: np.ndarray, w1: np.ndarray, b1: np.ndarray, prec: Precision) -> np.ndarray:
     """Per-head residual MLP block: r = s + SiLU(W1 s + b1)."""
     return s + silu(prec.store(s) @ w1.T + b1)
@@ -244,7 +253,7 @@ class CloverOracle:
     def decoder_weights(self, j: int) -> Dict[str, np.ndarray]:
         """The Attention Decoder that drafts depth j: the shared ad.* set (Eq. 1 has no head
         index), or head j's own ad{j-1}.* set when the configuration gives each head one."""
-        if not getattr(self.cfg, "ad_per_head", False):
+        if not getattr(self.cfg, "ad_per_head", False) or getattr(self.cfg, "regressive", "attention") == "mlp":
             return self.w
         return {f"ad.{f}": self.w[f"ad{j - 1}.{f}"] for f in ("norm", "wq", "wk", "wv", "wo")}
 
@@ -276,8 +285,12 @@ class CloverOracle:
             frontier = [i for i in range(len(depth)) if depth[i] == j - 1]
             wad = self.decoder_weights(j)
             for n in frontier:
-                s = attention_decoder(state[n], self.ad_keys(state[n], n, token, parent, wad), wad,
-                                      c.n_heads, c.head_dim, c.rms_eps, self.prec)
+                if getattr(c, "regressive", "attention") == "mlp":
+                    s = regressive_mlp(state[n], rc_embed(self.w["lm_head"], token[n]), self.w, c.rms_eps,
+                                       self.prec)
+                else:
+                    s = attention_decoder(state[n], self.ad_keys(state[n], n, token, parent, wad), wad,
+                                          c.n_heads, c.head_dim, c.rms_eps, self.prec)
                 logits = self.head_logits(j - 1, s)
                 logp = logits - logsumexp(logits)
                 out.row_logits[n] = logits

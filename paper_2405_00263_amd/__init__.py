@@ -22,6 +22,7 @@ KSTAT = {"gemm_verify": 0, "gemm_draft": 1, "attention": 2, "other": 3}
 DRAFT_MODES = {"clover": 0, "medusa": 1}
 AB_MODES = {"default": 0, "full": 1, "attn": 2, "mlp": 3, "none": 4}
 AD_KEYS = {"single": 0, "two": 1, "path": 2}
+REGRESSIVE = {"attention": 0, "mlp": 1}
 
 
 class CloverError(RuntimeError):
@@ -42,7 +43,8 @@ class ConfigC(ctypes.Structure):
                 ("prefill_chunk", ctypes.c_int32), ("flags", ctypes.c_int32),
                 ("draft_mode", ctypes.c_int32), ("ab_mode", ctypes.c_int32),
                 ("ad_keys", ctypes.c_int32), ("ad_per_head", ctypes.c_int32),
-                ("temperature", ctypes.c_float), ("sample_seed", ctypes.c_uint32)]
+                ("temperature", ctypes.c_float), ("sample_seed", ctypes.c_uint32),
+                ("regressive", ctypes.c_int32)]
 
 
 class TimingsC(ctypes.Structure):
@@ -78,6 +80,7 @@ EXPORTS = {
     "clover_debug_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_char_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "clover_debug_kv": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p]),
     "clover_get_timings": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p]),
+    "clover_debug_trace": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t]),
     "clover_kernel_stats_get": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p]),
     "clover_kernel_stats_reset": (ctypes.c_int, [ctypes.c_void_p]),
     "clover_set_flags": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32]),
@@ -92,6 +95,9 @@ EXPORTS = {
     "clover_op_topk": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     "clover_op_tree_build": (ctypes.c_int, [ctypes.c_void_p] * 4 + [ctypes.c_int32] * 3 + [ctypes.c_void_p] * 6),
     "clover_op_accept": (ctypes.c_int, [ctypes.c_void_p] * 3 + [ctypes.c_int32] * 2 + [ctypes.c_void_p] * 4),
+    "clover_op_compact": (ctypes.c_int, [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p] + [ctypes.c_int32] * 4
+                          + [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
+                             ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
 }
 
 
@@ -142,6 +148,7 @@ def make_config(cfg, max_batch: Optional[int] = None, max_context: Optional[int]
     c.ad_per_head = int(bool(getattr(cfg, "ad_per_head", False)))
     c.temperature = float(getattr(cfg, "temperature", 0.0))
     c.sample_seed = int(getattr(cfg, "sample_seed", 0)) & 0xFFFFFFFF
+    c.regressive = REGRESSIVE[getattr(cfg, "regressive", "attention")]
     return c
 
 
@@ -268,6 +275,15 @@ class CloverEngine:
         _check(lib().clover_debug_kv(self.ctx, seq, layer, pos, int(which_v),
                                      out.ctypes.data_as(ctypes.c_void_p)), self.ctx)
         return out
+
+    def set_trace(self, buf):
+        """Residual-stream trace into a cuda float32 tensor [n_layers + 2][rows][d_model]
+        (None switches it off)."""
+        if buf is None:
+            _check(lib().clover_debug_trace(self.ctx, None, 0), self.ctx)
+        else:
+            _check(lib().clover_debug_trace(self.ctx, ctypes.c_void_p(buf.data_ptr()), buf.numel() * 4), self.ctx)
+        self._trace = buf
 
     def timings(self) -> dict:
         t = TimingsC()
@@ -402,3 +418,18 @@ def op_accept(tokens, parent, target, max_depth: int):
     _check(lib().clover_op_accept(_ptr(tokens), _ptr(parent), _ptr(target), tokens.shape[0], max_depth,
                                   _ptr(acc), _ptr(acc_len), _ptr(bonus), ctypes.c_void_p(_stream_handle())))
     return acc, acc_len, bonus
+
+
+def op_compact(kcache, vcache, block_table, L: int, acc):
+    """In-place KV compaction of one sequence: kcache/vcache cuda [layers][blocks][n_kv][16*hd]
+    (storage dtype, the library's paged layout); block_table and acc host int sequences."""
+    import torch
+    dt = 1 if kcache.dtype == torch.bfloat16 else 0
+    nl, nb, nkv, per = kcache.shape
+    bt = np.ascontiguousarray(np.asarray(block_table, dtype=np.int32))
+    ac = np.ascontiguousarray(np.asarray(acc, dtype=np.int32))
+    scratch = torch.empty(4 * (len(bt) + len(ac)), dtype=torch.uint8, device=kcache.device)
+    _check(lib().clover_op_compact(dt, _ptr(kcache), _ptr(vcache), nl, nb, nkv, per // 16,
+                                   bt.ctypes.data_as(ctypes.c_void_p), len(bt), L,
+                                   ac.ctypes.data_as(ctypes.c_void_p), len(ac), _ptr(scratch),
+                                   scratch.numel(), ctypes.c_void_p(_stream_handle())))

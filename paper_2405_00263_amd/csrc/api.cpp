@@ -45,6 +45,7 @@ size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 int es_of(int dtype) { return dtype == CLOVER_BF16 ? 2 : 4; }
 bool is_medusa(const clover_config& c) { return c.draft_mode == CLOVER_DRAFT_MEDUSA; }
+bool mlp_regressive(const clover_config& c) { return !is_medusa(c) && c.regressive == CLOVER_REGRESSIVE_MLP; }
 int ab_mode(const clover_config& c) {
   if (c.ab_mode != CLOVER_AB_DEFAULT) return c.ab_mode;
   return is_medusa(c) ? CLOVER_AB_NONE : CLOVER_AB_FULL;
@@ -83,7 +84,11 @@ std::vector<WSpec> weight_specs(const clover_config& c) {
   s.push_back({"final_norm", d, 0, false});
   s.push_back({"lm_head", V, d, true});
   if (has_ab(c)) layer_specs(c, "ab", s, ab_attn(c), ab_mlp(c));
-  if (!is_medusa(c)) {  // ad.* shared, or ad{j}.* per head
+  if (mlp_regressive(c)) {  // the MLP regressive block over [RMSNorm(h); e]
+    s.push_back({"rb.norm", d, 0, false});
+    s.push_back({"rb.w", d, 2 * d, true});
+    s.push_back({"rb.b", d, 0, false});
+  } else if (!is_medusa(c)) {  // ad.* shared, or ad{j}.* per head
     for (int j = 0; j < (c.ad_per_head ? c.n_spec_heads : 1); ++j) {
       const std::string pre = c.ad_per_head ? "ad" + std::to_string(j) : std::string("ad");
       s.push_back({pre + ".norm", d, 0, false});
@@ -133,6 +138,10 @@ bool check_config(const clover_config* c, std::string& why) {
   if (c->ab_mode < CLOVER_AB_DEFAULT || c->ab_mode > CLOVER_AB_NONE) return fail("ab_mode out of range");
   if (c->ad_keys < CLOVER_AD_KEYS_SINGLE || c->ad_keys > CLOVER_AD_KEYS_PATH) return fail("ad_keys out of range");
   if (c->ad_per_head != 0 && c->ad_per_head != 1) return fail("ad_per_head must be 0 or 1");
+  if (c->regressive != CLOVER_REGRESSIVE_ATTENTION && c->regressive != CLOVER_REGRESSIVE_MLP)
+    return fail("regressive must be CLOVER_REGRESSIVE_ATTENTION or CLOVER_REGRESSIVE_MLP");
+  if (c->regressive == CLOVER_REGRESSIVE_MLP && (c->ad_keys != CLOVER_AD_KEYS_SINGLE || c->ad_per_head))
+    return fail("the MLP regressive block takes no Attention Decoder key set or per-head decoders");
   if (!(c->temperature >= 0.f) || c->temperature > 1e30f) return fail("temperature must be finite and >= 0");
   const int kc = kc_of(c->dtype);
   if (c->n_layers < 1 || c->n_layers > 1024) return fail("n_layers out of range");
@@ -318,6 +327,7 @@ struct clover_ctx {
   const void *emb, *final_norm, *lm_head;
   struct AdPtrs { const void *norm, *wq, *wk, *wv, *wo; };
   std::vector<AdPtrs> ad;  // one Attention Decoder shared by the heads, or one per head
+  const void *rb_norm = nullptr, *rb_w = nullptr, *rb_b = nullptr;  // MLP regressive block
   std::vector<const void*> head_w1, head_b1;
   // host state
   std::vector<int> seq_len;                  // -1 inactive
@@ -345,6 +355,8 @@ struct clover_ctx {
   struct StepGraphs { hipGraphExec_t draft = nullptr, verify = nullptr, accept = nullptr; };
   std::vector<StepGraphs> graphs;
   bool use_graphs = true;
+  float* trace = nullptr;  // residual-stream trace (clover_debug_trace): [n_layers + 2][rows][d]
+  size_t trace_bytes = 0;
   hipStream_t cap_st = nullptr;  // private stream the phases are captured on (the caller's
                                  // stream may be the legacy default stream, which cannot be)
 
@@ -439,6 +451,13 @@ hipError_t run_gemm(clover_ctx* c, GemmParams p, int M, int K,
   return e;
 }
 
+// Residual-stream trace: copy the M rows of x into trace slot `idx` (clover_debug_trace).
+hipError_t trace_rows(clover_ctx* c, int idx, const float* x, int M) {
+  if (!c->trace) return hipSuccess;
+  const size_t n = (size_t)M * c->cfg.d_model;
+  return hipMemcpyAsync(c->trace + (size_t)idx * n, x, 4 * n, hipMemcpyDeviceToDevice, c->st);
+}
+
 // resid_norm: x += sum of pending partials; xn = RMSNorm(x) * gain (storage)
 hipError_t run_rowfix(clover_ctx* c, RowFixParams rp) {
   ProfScope ps(c, CLOVER_KSTAT_OTHER, 0, 0);
@@ -515,6 +534,7 @@ hipError_t run_layer(clover_ctx* c, const LayerPtrs& lw, int layer_idx, float* x
   rf.resid = x; rf.ldr = d; rf.out_f = x; rf.ldo = d;
   rf.gain = attn ? lw.attn_norm : lw.mlp_norm; rf.eps = cf.rms_eps; rf.out_norm = xn; rf.ldn = d;
   if ((e = run_rowfix(c, rf))) return e;
+  if (layer_idx < cf.n_layers && (e = trace_rows(c, layer_idx, x, M))) return e;  // the layer's input
   if (attn) {
     if ((e = run_attention_half(c, lw, layer_idx, M, att, max_keys, pend_out))) return e;
     if (!mlp) return hipSuccess;
@@ -557,6 +577,10 @@ clover_status ensure_blocks(clover_ctx* c, int slot, int upto) {
     if (e_ != hipSuccess) return e_;    \
   } while (0)
 
+// The verify and prefill LM heads write their fp32 logits only on request; the target's
+// choices need only the argmax keys of the epilogue.
+bool keep_logits(const clover_ctx* c) { return (c->cfg.flags & CLOVER_FLAG_KEEP_LOGITS) != 0; }
+
 // LM-head argmax keys of the target's choices: plain argmax (greedy), or with temperature a
 // Gumbel-max sample per row (GemmParams::inv_temp).  domain 0: tree nodes (row m is node
 // m % rows_per_seq of sequence slot_of_row[m]); 1: the token after the prompt.
@@ -597,10 +621,11 @@ hipError_t enq_verify(clover_ctx* c, int B, int max_keys) {
   rf.resid = x; rf.ldr = d; rf.out_f = x; rf.ldo = d; rf.out_copy_f = xa;
   rf.gain = c->final_norm; rf.eps = cf.rms_eps; rf.out_norm = c->at<void>(L.xn); rf.ldn = d;
   HE(run_rowfix(c, rf));
+  HE(trace_rows(c, cf.n_layers, x, M));
   // LM head; its epilogue leaves per-(column group, row) argmax keys, reduced per row
   GemmParams lm{};
   lm.X = c->at<void>(L.xn); lm.ldx = d; lm.mode = EP_PARTIAL; lm.max_splits = 1;
-  lm.part = c->at<float>(L.vlogits);
+  lm.part = keep_logits(c) ? c->at<float>(L.vlogits) : nullptr;  // argmax keys only otherwise
   lm.amax_part = c->at<unsigned long long>(L.amax_part);
   set_sampling(c, lm, 0, c->at<int>(L.row_seq), T);
   int lm_groups = 0;
@@ -609,13 +634,14 @@ hipError_t enq_verify(clover_ctx* c, int B, int max_keys) {
     ProfScope ps(c, CLOVER_KSTAT_OTHER, 0, 0);
     HE(launch_argmax_groups(c->at<unsigned long long>(L.amax_part), lm_groups, M, c->at<int>(L.target), c->st));
   }
-  if (!has_ab(cf)) return hipSuccess;  // xa keeps x_N: the next draft reads it
+  if (!has_ab(cf)) return trace_rows(c, cf.n_layers + 1, xa, M);  // xa keeps x_N: the next draft reads it
   // Augmenting Block over the tree (tree mask, its own KV cache)
   HE(run_layer(c, c->layers[cf.n_layers], cf.n_layers, xa, M, att, max_keys, 0, &pend, ab_attn(cf), ab_mlp(cf)));
   RowFixParams ra{};
   ra.M = M; ra.d = d; ra.part = c->at<float>(L.gpart); ra.S = pend; ra.ldp = d;
   ra.resid = xa; ra.ldr = d; ra.out_f = xa; ra.ldo = d;
-  return run_rowfix(c, ra);
+  HE(run_rowfix(c, ra));
+  return trace_rows(c, cf.n_layers + 1, xa, M);
 }
 
 // Greedy acceptance, bonus token, h_0 for the next draft, KV compaction of every layer.
@@ -761,8 +787,9 @@ hipError_t enq_draft_medusa(clover_ctx* c, int B) {
   return enq_tree(c, B);
 }
 
-// Draft (Sec. 3): per depth, Attention Decoder on the frontier (Eq. 1-2), head MLP,
-// shared final norm + LM head, top-k children; then truncation into the verify tree.
+// Draft (Sec. 3): per depth, the regressive block on the frontier (the Attention Decoder,
+// Eq. 1-2, or the MLP of the Sec. 4.3 ablation), head MLP, shared final norm + LM head,
+// top-k children; then truncation into the verify tree.
 hipError_t enq_draft(clover_ctx* c, int B) {
   if (is_medusa(c->cfg)) return enq_draft_medusa(c, B);
   const clover_config& cf = c->cfg;
@@ -782,59 +809,78 @@ hipError_t enq_draft(clover_ctx* c, int B) {
     ap.seq_ids = ids; ap.nbatch = B; ap.F = F;
     ap.cand_token = ct; ap.cand_stride = L.NC; ap.base_node = depth_base(cf, j - 1);
     ap.lm_packed = c->lm_head; ap.lm_nchunks = d / kc_of(cf.dtype);
-    const clover_ctx::AdPtrs& adw = c->ad[cf.ad_per_head ? j - 1 : 0];
-    ap.ad_norm = adw.norm; ap.eps = cf.rms_eps; ap.d = d;
-    // with the two-token key set the embeddings follow the normalised states in one [2M][d]
-    // block, so one K|V GEMM projects both
-    const bool two = cf.ad_keys == CLOVER_AD_KEYS_TWO;
-    ap.hin = c->at<float>(L.d_hin); ap.a_out = c->at<void>(L.d_a);
-    ap.e_out = two ? (void*)(c->at<char>(L.d_a) + (size_t)M * d * L.es) : c->at<void>(L.d_e);
-    HE(launch_ad_prep(cf.dtype, ap, c->st));
     float* part = c->at<float>(L.gpart);
-    float* part2 = c->at<float>(L.gpart2);
-    int sq = 0, skv = 0, so = 0, sh = 0;
-    // With the single key (Eq. 1 read literally) the softmax weight is exactly 1, so the
-    // decoder's output is W_V e: the Q and K projections cannot change it and are skipped.
-    const bool values_only = cf.ad_keys == CLOVER_AD_KEYS_SINGLE;
-    if (!values_only) {
-      GemmParams q{};
-      q.X = c->at<void>(L.d_a); q.ldx = d; q.mode = EP_PARTIAL; q.max_splits = GEMM_MAX_SPLITS; q.part = part;
-      HE(run_gemm(c, q, M, d, {{adw.wq, qd}}, &sq));
-    }
-    GemmParams kv{};
-    kv.X = two ? c->at<void>(L.d_a) : c->at<void>(L.d_e); kv.ldx = d; kv.mode = EP_PARTIAL;
-    kv.max_splits = GEMM_MAX_SPLITS; kv.part = part2;
-    if (values_only)
-      HE(run_gemm(c, kv, M, d, {{adw.wv, qd}}, &skv));
-    else
-      HE(run_gemm(c, kv, two ? 2 * M : M, d, {{adw.wk, qd}, {adw.wv, qd}}, &skv));
-    AdAttnParams aa{};
-    aa.q = part; aa.Sq = sq; aa.kv = part2; aa.Skv = skv; aa.values_only = values_only;
-    aa.M = M; aa.F = F; aa.n_heads = cf.n_heads; aa.hd = cf.head_dim;
-    aa.keys = cf.ad_keys; aa.depth = j - 1; aa.out = c->at<void>(L.d_o);
-    if (cf.ad_keys == CLOVER_AD_KEYS_PATH) {
-      // key/value rows of every depth's nodes, depth after depth; an ancestor at depth dd of
-      // a depth-(j-1) node fl has index fl / (k_dd * ... * k_{j-2}) among its depth's nodes
-      aa.kv_path = c->at<float>(L.d_kvpath);
-      int off = 0;
-      for (int dd = 0; dd < j; ++dd) {
-        aa.kv_path_off[dd] = off;
-        aa.path_nodes[dd] = frontier(cf, dd + 1);
-        off += B * frontier(cf, dd + 1);
-        int div = 1;
-        for (int t = dd; t < j - 1; ++t) div *= cf.topk[t];
-        aa.anc_div[dd] = div;
+    if (mlp_regressive(cf)) {
+      // MLP regressive block: one [M][2d] row per frontier node, RMSNorm_r(h) then e, so a
+      // single GEMM with K = 2d applies W_r to the concatenation
+      ap.ad_norm = c->rb_norm; ap.eps = cf.rms_eps; ap.d = d; ap.ld_out = 2 * d;
+      ap.hin = c->at<float>(L.d_hin); ap.a_out = c->at<void>(L.d_a);
+      ap.e_out = c->at<char>(L.d_a) + (size_t)d * L.es;
+      HE(launch_ad_prep(cf.dtype, ap, c->st));
+      GemmParams rg{};
+      rg.X = c->at<void>(L.d_a); rg.ldx = 2 * d; rg.mode = EP_PARTIAL; rg.max_splits = GEMM_MAX_SPLITS; rg.part = part;
+      int sr = 0;
+      HE(run_gemm(c, rg, M, 2 * d, {{c->rb_w, d}}, &sr));
+      RowFixParams rr{};  // s = h + SiLU(W_r [RMSNorm_r(h); e] + b_r): fp32 state and storage copy
+      rr.M = M; rr.d = d; rr.part = part; rr.S = sr; rr.ldp = d;
+      rr.resid = c->at<float>(L.d_hin); rr.ldr = d; rr.act = 1; rr.bias = c->rb_b;
+      rr.out_f = c->at<float>(L.dstate[j - 1]); rr.ldo = d; rr.out_copy_s = c->at<void>(L.d_sst);
+      HE(run_rowfix(c, rr));
+    } else {
+      const clover_ctx::AdPtrs& adw = c->ad[cf.ad_per_head ? j - 1 : 0];
+      ap.ad_norm = adw.norm; ap.eps = cf.rms_eps; ap.d = d;
+      // with the two-token key set the embeddings follow the normalised states in one [2M][d]
+      // block, so one K|V GEMM projects both
+      const bool two = cf.ad_keys == CLOVER_AD_KEYS_TWO;
+      ap.hin = c->at<float>(L.d_hin); ap.a_out = c->at<void>(L.d_a);
+      ap.e_out = two ? (void*)(c->at<char>(L.d_a) + (size_t)M * d * L.es) : c->at<void>(L.d_e);
+      HE(launch_ad_prep(cf.dtype, ap, c->st));
+      float* part2 = c->at<float>(L.gpart2);
+      int sq = 0, skv = 0, so = 0;
+      // With the single key (Eq. 1 read literally) the softmax weight is exactly 1, so the
+      // decoder's output is W_V e: the Q and K projections cannot change it and are skipped.
+      const bool values_only = cf.ad_keys == CLOVER_AD_KEYS_SINGLE;
+      if (!values_only) {
+        GemmParams q{};
+        q.X = c->at<void>(L.d_a); q.ldx = d; q.mode = EP_PARTIAL; q.max_splits = GEMM_MAX_SPLITS; q.part = part;
+        HE(run_gemm(c, q, M, d, {{adw.wq, qd}}, &sq));
       }
+      GemmParams kv{};
+      kv.X = two ? c->at<void>(L.d_a) : c->at<void>(L.d_e); kv.ldx = d; kv.mode = EP_PARTIAL;
+      kv.max_splits = GEMM_MAX_SPLITS; kv.part = part2;
+      if (values_only)
+        HE(run_gemm(c, kv, M, d, {{adw.wv, qd}}, &skv));
+      else
+        HE(run_gemm(c, kv, two ? 2 * M : M, d, {{adw.wk, qd}, {adw.wv, qd}}, &skv));
+      AdAttnParams aa{};
+      aa.q = part; aa.Sq = sq; aa.kv = part2; aa.Skv = skv; aa.values_only = values_only;
+      aa.M = M; aa.F = F; aa.n_heads = cf.n_heads; aa.hd = cf.head_dim;
+      aa.keys = cf.ad_keys; aa.depth = j - 1; aa.out = c->at<void>(L.d_o);
+      if (cf.ad_keys == CLOVER_AD_KEYS_PATH) {
+        // key/value rows of every depth's nodes, depth after depth; an ancestor at depth dd of
+        // a depth-(j-1) node fl has index fl / (k_dd * ... * k_{j-2}) among its depth's nodes
+        aa.kv_path = c->at<float>(L.d_kvpath);
+        int off = 0;
+        for (int dd = 0; dd < j; ++dd) {
+          aa.kv_path_off[dd] = off;
+          aa.path_nodes[dd] = frontier(cf, dd + 1);
+          off += B * frontier(cf, dd + 1);
+          int div = 1;
+          for (int t = dd; t < j - 1; ++t) div *= cf.topk[t];
+          aa.anc_div[dd] = div;
+        }
+      }
+      HE(launch_ad_attn(cf.dtype, aa, c->st));
+      GemmParams o{};
+      o.X = c->at<void>(L.d_o); o.ldx = qd; o.mode = EP_PARTIAL; o.max_splits = GEMM_MAX_SPLITS; o.part = part;
+      HE(run_gemm(c, o, M, qd, {{adw.wo, d}}, &so));
+      RowFixParams rs{};  // s = h + W_O attn (Eq. 2): fp32 state and storage copy for the MLP
+      rs.M = M; rs.d = d; rs.part = part; rs.S = so; rs.ldp = d;
+      rs.resid = c->at<float>(L.d_hin); rs.ldr = d;
+      rs.out_f = c->at<float>(L.dstate[j - 1]); rs.ldo = d; rs.out_copy_s = c->at<void>(L.d_sst);
+      HE(run_rowfix(c, rs));
     }
-    HE(launch_ad_attn(cf.dtype, aa, c->st));
-    GemmParams o{};
-    o.X = c->at<void>(L.d_o); o.ldx = qd; o.mode = EP_PARTIAL; o.max_splits = GEMM_MAX_SPLITS; o.part = part;
-    HE(run_gemm(c, o, M, qd, {{adw.wo, d}}, &so));
-    RowFixParams rs{};  // s = h + W_O attn (Eq. 2): fp32 state and storage copy for the MLP
-    rs.M = M; rs.d = d; rs.part = part; rs.S = so; rs.ldp = d;
-    rs.resid = c->at<float>(L.d_hin); rs.ldr = d;
-    rs.out_f = c->at<float>(L.dstate[j - 1]); rs.ldo = d; rs.out_copy_s = c->at<void>(L.d_sst);
-    HE(run_rowfix(c, rs));
+    int sh = 0;
     GemmParams hm{};
     hm.X = c->at<void>(L.d_sst); hm.ldx = d; hm.mode = EP_PARTIAL; hm.max_splits = GEMM_MAX_SPLITS; hm.part = part;
     HE(run_gemm(c, hm, M, d, {{c->head_w1[j - 1], d}}, &sh));
@@ -1044,7 +1090,9 @@ clover_status clover_init(const clover_config* cfg, void* const* weights, void* 
     if (ab_mlp(*cfg)) { p.mlp_norm = c->w[k++]; p.wg = c->w[k++]; p.wu = c->w[k++]; p.wd = c->w[k++]; }
     c->layers.push_back(p);
   }
-  if (!is_medusa(*cfg)) {
+  if (mlp_regressive(*cfg)) {
+    c->rb_norm = c->w[k++]; c->rb_w = c->w[k++]; c->rb_b = c->w[k++];
+  } else if (!is_medusa(*cfg)) {
     for (int j = 0; j < (cfg->ad_per_head ? cfg->n_spec_heads : 1); ++j) {
       clover_ctx::AdPtrs a;
       a.norm = c->w[k++]; a.wq = c->w[k++]; a.wk = c->w[k++]; a.wv = c->w[k++]; a.wo = c->w[k++];
@@ -1137,6 +1185,8 @@ clover_status clover_prefill(clover_ctx* c, int32_t seq, const int32_t* tokens, 
   if ((int64_t)n + L.T > cf.max_context) return ctx_fail(c, CLOVER_ERR_CAPACITY, "prompt of %d tokens exceeds max_context", n);
   for (int i = 0; i < n; ++i)
     if (tokens[i] < 0 || tokens[i] >= cf.vocab) return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "token %d out of range", tokens[i]);
+  if (c->trace && (size_t)(cf.n_layers + 2) * std::min(n, L.Mp) * cf.d_model * 4 > c->trace_bytes)
+    return ctx_fail(c, CLOVER_ERR_CAPACITY, "trace buffer too small for a %d-row prefill chunk", std::min(n, L.Mp));
   if ((s = ensure_blocks(c, seq, n + L.T))) return s;
   const int d = cf.d_model, C = L.Mp;
   float* x = c->at<float>(L.x);
@@ -1173,10 +1223,12 @@ clover_status clover_prefill(clover_ctx* c, int32_t seq, const int32_t* tokens, 
     rf.resid = x; rf.ldr = d; rf.out_f = x; rf.ldo = d; rf.out_copy_f = xa;
     rf.gain = c->final_norm; rf.eps = cf.rms_eps; rf.out_norm = c->at<void>(L.xn); rf.ldn = d;
     HIPCK(c, run_rowfix(c, rf));
+    HIPCK(c, trace_rows(c, cf.n_layers, x, rows));
     if (c0 + rows == n) {
       GemmParams lm{};
       lm.X = (const char*)c->at<char>(L.xn) + (size_t)(rows - 1) * d * L.es; lm.ldx = d;
-      lm.mode = EP_PARTIAL; lm.max_splits = 1; lm.part = c->at<float>(L.vlogits);
+      lm.mode = EP_PARTIAL; lm.max_splits = 1;
+      lm.part = keep_logits(c) ? c->at<float>(L.vlogits) : nullptr;
       lm.amax_part = c->at<unsigned long long>(L.amax_part);
       set_sampling(c, lm, 1, c->at<int>(L.seq_ids), 1);  // the first token: row 0 is sequence seq
       int lm_groups = 0;
@@ -1191,6 +1243,7 @@ clover_status clover_prefill(clover_ctx* c, int32_t seq, const int32_t* tokens, 
       ra.resid = xa; ra.ldr = d; ra.out_f = xa; ra.ldo = d;
       HIPCK(c, run_rowfix(c, ra));
     }
+    HIPCK(c, trace_rows(c, cf.n_layers + 1, xa, rows));
     if (c0 + rows == n)
       HIPCK(c, launch_finish_prefill(seq, c->at<int>(L.amax), xa + (size_t)(rows - 1) * d, d,
                                      c->at<int>(L.t0), c->at<float>(L.h0), c->st));
@@ -1213,9 +1266,11 @@ clover_status clover_step(clover_ctx* c, const int32_t* seqs, int32_t n_seqs, in
   const clover_config& cf = c->cfg;
   const Layout& L = c->L;
   const int B = n_seqs, d = cf.d_model, qd = cf.n_heads * cf.head_dim, H = L.H;
+  if (c->trace && (size_t)(cf.n_layers + 2) * B * L.T * d * 4 > c->trace_bytes)
+    return ctx_fail(c, CLOVER_ERR_CAPACITY, "trace buffer too small for %d verify rows", B * L.T);
   int max_keys = 0;
   if ((s = begin_batch(c, seqs, B, max_keys))) return s;
-  const bool graph = c->use_graphs;
+  const bool graph = c->use_graphs && !c->trace;  // a traced step runs its launches eagerly
   HIPCK(c, hipEventRecord(c->ev[0], c->st));
   c->in_step = true;
   c->phase = CLOVER_KSTAT_GEMM_DRAFT;
@@ -1242,6 +1297,8 @@ clover_status clover_verify_tree(clover_ctx* c, int32_t seq, const int32_t* toke
   if ((s = check_seqs(c, &seq, 1))) return s;
   if (T < 1 || T > L.T) return ctx_fail(c, CLOVER_ERR_BAD_TREE, "tree of %d tokens (max %d)", T, L.T);
   if (parents[0] != -1) return ctx_fail(c, CLOVER_ERR_BAD_TREE, "parents[0] must be -1");
+  if (c->trace && (size_t)(cf.n_layers + 2) * L.T * cf.d_model * 4 > c->trace_bytes)
+    return ctx_fail(c, CLOVER_ERR_CAPACITY, "trace buffer too small for %d verify rows", L.T);
   std::vector<int> depth(L.T, 0), tok(L.T, 0), par(L.T, -1);
   for (int i = 0; i < T; ++i) {
     if (tokens[i] < 0 || tokens[i] >= cf.vocab) return ctx_fail(c, CLOVER_ERR_BAD_TREE, "token %d out of range", tokens[i]);
@@ -1377,6 +1434,16 @@ clover_status clover_debug_kv(clover_ctx* c, int32_t seq, int32_t layer, int32_t
   return CLOVER_OK;
 }
 
+clover_status clover_debug_trace(clover_ctx* c, float* dev_buf, size_t bytes) {
+  clover_status s = check_ctx(c);
+  if (s) return s;
+  if (dev_buf && bytes < (size_t)(c->cfg.n_layers + 2) * c->cfg.d_model * 4)
+    return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "trace buffer smaller than one row per slot");
+  c->trace = dev_buf;
+  c->trace_bytes = dev_buf ? bytes : 0;
+  return CLOVER_OK;
+}
+
 clover_status clover_get_timings(clover_ctx* c, clover_timings* out) {
   clover_status s = check_ctx(c);
   if (s) return s;
@@ -1398,6 +1465,16 @@ clover_status clover_set_flags(clover_ctx* c, int32_t flags) {
   if (s) return s;
   if (flags & ~(CLOVER_FLAG_KEEP_LOGITS | CLOVER_FLAG_PROFILE | CLOVER_FLAG_EAGER))
     return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
+  if ((flags ^ c->cfg.flags) & CLOVER_FLAG_KEEP_LOGITS) {
+    // the captured verify phases bake in whether the LM head stores its logits
+    (void)hipStreamSynchronize(c->st);
+    for (auto& g : c->graphs)
+      for (hipGraphExec_t* x : {&g.draft, &g.verify, &g.accept})
+        if (*x) {
+          (void)hipGraphExecDestroy(*x);
+          *x = nullptr;
+        }
+  }
   c->cfg.flags = flags;
   c->profile = (flags & CLOVER_FLAG_PROFILE) != 0;
   c->use_graphs = !c->profile && !(flags & CLOVER_FLAG_EAGER);
@@ -1631,6 +1708,50 @@ clover_status clover_op_accept(const int32_t* tokens, const int32_t* parent, con
   hipError_t e = launch_accept(p, (hipStream_t)hip_stream);
   if (e != hipSuccess) {
     set_global_err("op_accept: %s", hipGetErrorString(e));
+    return CLOVER_ERR_DEVICE;
+  }
+  return CLOVER_OK;
+}
+
+clover_status clover_op_compact(int32_t dtype, void* kcache, void* vcache, int32_t n_layers, int32_t n_blocks,
+                                int32_t n_kv, int32_t head_dim, const int32_t* block_table, int32_t n_table,
+                                int32_t L, const int32_t* acc, int32_t A, void* scratch, size_t scratch_bytes,
+                                void* hip_stream) {
+  if ((dtype != CLOVER_F32 && dtype != CLOVER_BF16) || !kcache || !vcache || !block_table || !acc ||
+      !scratch || n_layers < 1 || n_blocks < 1 || n_table < 1 || n_kv < 1 ||
+      (head_dim != 32 && head_dim != 64 && head_dim != 128) || L < 0 || A < 1 || A > 9) {
+    set_global_err("op_compact: bad arguments");
+    return CLOVER_ERR_INVALID_ARG;
+  }
+  if (scratch_bytes < sizeof(int32_t) * (size_t)(n_table + A)) {
+    set_global_err("op_compact: scratch needs 4 * (n_table + A) bytes");
+    return CLOVER_ERR_CAPACITY;
+  }
+  for (int i = 0; i < n_table; ++i)
+    if (block_table[i] < 0 || block_table[i] >= n_blocks) {
+      set_global_err("op_compact: block_table[%d] = %d outside [0, %d)", i, block_table[i], n_blocks);
+      return CLOVER_ERR_INVALID_ARG;
+    }
+  for (int k = 0; k < A; ++k)
+    if (acc[k] < 0 || (int64_t)L + std::max(acc[k], k) >= (int64_t)n_table * 16) {
+      set_global_err("op_compact: slot L + acc[%d] or L + %d outside the block table", k, k);
+      return CLOVER_ERR_INVALID_ARG;
+    }
+  hipStream_t st = (hipStream_t)hip_stream;
+  int32_t* dev = (int32_t*)scratch;  // [block table][acc]
+  hipError_t e = hipMemcpyAsync(dev, block_table, sizeof(int32_t) * n_table, hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) e = hipMemcpyAsync(dev + n_table, acc, sizeof(int32_t) * A, hipMemcpyHostToDevice, st);
+  CompactParams cp{};
+  cp.seq_ids = nullptr; cp.nbatch = 1; cp.H = A - 1;
+  cp.acc = dev + n_table; cp.acc_len = nullptr; cp.seq_len = nullptr; cp.A_host = A; cp.L_host = L;
+  cp.kpools = nullptr; cp.vpools = nullptr; cp.nlayers = n_layers;
+  cp.kbase = kcache; cp.vbase = vcache; cp.layer_elems = (size_t)n_blocks * n_kv * 16 * head_dim;
+  cp.block_table = dev; cp.max_blocks = n_table;
+  cp.n_kv = n_kv; cp.hd = head_dim;
+  if (e == hipSuccess) e = launch_compact(dtype, cp, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);  // the host arrays may go once this returns
+  if (e != hipSuccess) {
+    set_global_err("op_compact: %s", hipGetErrorString(e));
     return CLOVER_ERR_DEVICE;
   }
   return CLOVER_OK;

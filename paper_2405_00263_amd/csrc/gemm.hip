@@ -228,7 +228,8 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(const GemmParams p) {
     // split `split` writes rows m0.. of its own [M][N] fp32 slice
     if (!AMAX && !active) return;
     const int n = (g * NW + wave) * 16 + (lane & 15);  // segments are contiguous in N
-    if (active) {
+    // with argmax keys the logits themselves are optional (p.part null: keys only)
+    if (active && (!AMAX || p.part)) {
       float* out = p.part + (size_t)split * p.M * p.N;
 #pragma unroll
       for (int t = 0; t < MT; ++t)

@@ -182,10 +182,11 @@ __global__ __launch_bounds__(WR * TWAVES * 64) void tiled_kernel(const GemmParam
   // m0 + 16t + 4*(lane/16) + i, column 16*tile + lane%16.
   const int rbase = m0 + wrow * WM + 4 * (lane >> 4), ccol = lane & 15;
   if (p.mode == EP_PARTIAL) {
+    // with argmax keys the logits themselves are optional (p.part null: keys only)
     float* out = p.part + (size_t)split * p.M * p.N;
 #pragma unroll
     for (int j = 0; j < TW; ++j) {
-      if (!act[j]) continue;
+      if (!act[j] || (AMAX != 0 && !p.part)) continue;
       const int n = otile[j] * 16 + ccol;
 #pragma unroll
       for (int t = 0; t < MT; ++t)

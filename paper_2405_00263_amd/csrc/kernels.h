@@ -31,7 +31,7 @@ struct GemmParams {
   int nseg, ntiles, N;
   int ngroups, mchunks, S, cps;
   int max_splits;  // EP_PARTIAL: upper bound on K splits (1 = unsplit)
-  float* part;     // EP_PARTIAL output [S][M][N]
+  float* part;     // EP_PARTIAL output [S][M][N]; with amax_part it may be null (keys only)
   // EP_PARTIAL with one split: optional per-(column group, row) argmax keys [ngroups][M]
   // of the output (amax_key order), reduced by launch_argmax_groups; null: off
   unsigned long long* amax_part;
@@ -167,6 +167,7 @@ struct AdPrepParams {
   const void* lm_packed; int lm_nchunks;
   const void* ad_norm; float eps; int d;
   float* hin; void* a_out; void* e_out;
+  int ld_out;                            // row stride of a_out / e_out in elements (0: d)
 };
 hipError_t launch_ad_prep(int dtype, AdPrepParams& p, hipStream_t st);
 // Attention Decoder attention (Eq. 1-2) of the M frontier rows of one depth.  Queries from
@@ -217,9 +218,11 @@ struct AcceptParams {
 hipError_t launch_accept(AcceptParams& p, hipStream_t st);
 
 struct CompactParams {
-  const int* seq_ids; int nbatch, H;
-  const int* acc; const int* acc_len; const int* seq_len;
-  void* const* kpools; void* const* vpools; int nlayers;   // device arrays of pool pointers
+  const int* seq_ids; int nbatch, H;     // seq_ids null: one sequence, slot 0
+  const int* acc; const int* acc_len; const int* seq_len;  // acc_len / seq_len null: A_host / L_host
+  int A_host, L_host;
+  void* const* kpools; void* const* vpools; int nlayers;   // device arrays of pool pointers, or
+  void* kbase; void* vbase; size_t layer_elems;             // (kpools null) pools at base + layer * layer_elems
   const int* block_table; int max_blocks;
   int n_kv, hd;
 };

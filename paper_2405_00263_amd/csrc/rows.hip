@@ -539,8 +539,9 @@ __global__ __launch_bounds__(256) void ad_prep_kernel(const AdPrepParams p) {
   se = red[1][0] + red[1][1] + red[1][2] + red[1][3];
   const float rinv = 1.0f / sqrtf(ss / (float)d + p.eps);
   const float einv = 1.0f / fmaxf(sqrtf(se), 1e-12f);
-  u32x4_t* a = reinterpret_cast<u32x4_t*>(p.a_out) + (size_t)f * nseg;
-  u32x4_t* e = reinterpret_cast<u32x4_t*>(p.e_out) + (size_t)f * nseg;
+  const size_t ld = p.ld_out ? (size_t)p.ld_out : (size_t)d;
+  u32x4_t* a = reinterpret_cast<u32x4_t*>(reinterpret_cast<S*>(p.a_out) + (size_t)f * ld);
+  u32x4_t* e = reinterpret_cast<u32x4_t*>(reinterpret_cast<S*>(p.e_out) + (size_t)f * ld);
   float* hin = p.hin + (size_t)f * d;
 #pragma unroll
   for (int i = 0; i < AD_MAXV; ++i) {

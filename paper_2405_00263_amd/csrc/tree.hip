@@ -166,11 +166,13 @@ hipError_t launch_accept(AcceptParams& p, hipStream_t st) {
 template <typename S>
 __global__ __launch_bounds__(256) void compact_kernel(const CompactParams p) {
   constexpr int MAXA = 9;
-  const int b = blockIdx.x, layer = blockIdx.y, slot = p.seq_ids[b];
-  const int A = p.acc_len[slot], L = p.seq_len[slot];
+  const int b = blockIdx.x, layer = blockIdx.y, slot = p.seq_ids ? p.seq_ids[b] : 0;
+  const int A = p.acc_len ? p.acc_len[slot] : p.A_host, L = p.seq_len ? p.seq_len[slot] : p.L_host;
   const int* acc = p.acc + (size_t)slot * (p.H + 1);
-  S* kp = reinterpret_cast<S*>(p.kpools[layer]);
-  S* vp = reinterpret_cast<S*>(p.vpools[layer]);
+  S* kp = p.kpools ? reinterpret_cast<S*>(p.kpools[layer])
+                   : reinterpret_cast<S*>(p.kbase) + (size_t)layer * p.layer_elems;
+  S* vp = p.vpools ? reinterpret_cast<S*>(p.vpools[layer])
+                   : reinterpret_cast<S*>(p.vbase) + (size_t)layer * p.layer_elems;
   const int hd = p.hd, per = p.n_kv * hd;
   for (int e = threadIdx.x; e < per; e += 256) {
     const int kvh = e / hd, d = e % hd;

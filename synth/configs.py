@@ -37,6 +37,9 @@ class CloverConfig:
     # key set of the Attention Decoder: "single" {e}, "two" {RMSNorm(h), e}, "path" {e_0..}
     ad_keys: str = "single"
     ad_per_head: bool = False  # one Attention Decoder per head instead of one shared
+    # regressive block of the Clover draft: the "attention" decoder (Eq. 1-2) or the "mlp"
+    # over [RMSNorm(h); e] of the ablation (Sec. 3.2 last paragraph, Sec. 4.3)
+    regressive: str = "attention"
     temperature: float = 0.0   # 0: greedy; > 0: the target samples (speculative sampling)
     sample_seed: int = 0
 

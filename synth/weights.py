@@ -33,7 +33,9 @@ def weight_specs(c: CloverConfig) -> List[Tuple[str, Tuple[int, ...]]]:
     specs += [("final_norm", (d,)), ("lm_head", (V, d))]
     if c.ab_kind != "none":  # the Augmenting Block's halves
         specs += _layer_specs("ab", c, attn=c.ab_kind in ("full", "attn"), mlp=c.ab_kind in ("full", "mlp"))
-    if c.draft != "medusa":  # Attention Decoder: Clover heads only; shared, or one per head
+    if c.draft != "medusa" and c.regressive == "mlp":  # MLP regressive block over [RMSNorm(h); e]
+        specs += [("rb.norm", (d,)), ("rb.w", (d, 2 * d)), ("rb.b", (d,))]
+    elif c.draft != "medusa":  # Attention Decoder: Clover heads only; shared, or one per head
         qd = c.n_heads * c.head_dim
         for pre in ([f"ad{j}" for j in range(c.n_spec_heads)] if c.ad_per_head else ["ad"]):
             specs += [(f"{pre}.norm", (d,)), (f"{pre}.wq", (qd, d)), (f"{pre}.wk", (qd, d)),
@@ -43,8 +45,12 @@ def weight_specs(c: CloverConfig) -> List[Tuple[str, Tuple[int, ...]]]:
     return specs
 
 
+def is_bias(name: str) -> bool:
+    return name.endswith(".b1") or name == "rb.b"
+
+
 def is_matrix(name: str) -> bool:
-    return not (name.endswith("norm") or name.endswith(".b1"))
+    return not (name.endswith("norm") or is_bias(name))
 
 
 def _gen(seed: int, idx: int, device) -> torch.Generator:
@@ -70,7 +76,7 @@ def make_weights(c: CloverConfig, seed: int = 0, device="cpu", perturb: bool = F
             t = torch.ones(shape, device=device)
             if perturb:
                 t = t + 0.1 * torch.randn(shape, generator=g, device=device)
-        elif name.endswith(".b1"):
+        elif is_bias(name):
             t = torch.zeros(shape, device=device)
             if perturb:
                 t = 0.02 * torch.randn(shape, generator=g, device=device)

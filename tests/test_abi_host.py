@@ -32,10 +32,15 @@ def test_every_declared_symbol_is_exported():
     assert set(names) == set(P.EXPORTS)
 
 
-@pytest.mark.parametrize("name", list(synth.CONFIGS))
-def test_weight_list_matches_synth(name):
+VARIANTS = [(n, {}) for n in synth.CONFIGS] + [
+    ("tiny_fp32", {"regressive": "mlp"}), ("llama7b_b1", {"regressive": "mlp", "ab": "none"}),
+    ("tiny_fp32", {"ad_per_head": True}), ("large_gqa_b1", {"ab": "attn"})]
+
+
+@pytest.mark.parametrize("name,kw", VARIANTS)
+def test_weight_list_matches_synth(name, kw):
     import paper_2405_00263_amd as P
-    cfg = synth.get_config(name)
+    cfg = synth.get_config(name).with_(**kw)
     c = P.make_config(cfg)
     specs = synth.weight_specs(cfg)
     assert P.weight_names(c) == [n for n, _ in specs]

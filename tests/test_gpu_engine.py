@@ -11,6 +11,8 @@ pytestmark = pytest.mark.gpu
 
 
 def _engine(P, cfg, w, **kw):
+    """An engine whose verify LM head also stores its logits (the parity checks read them)."""
+    kw.setdefault("flags", P.FLAG_KEEP_LOGITS)
     return P.CloverEngine(cfg, {k: v.cuda() for k, v in w.items()}, **kw)
 
 
@@ -385,6 +387,31 @@ def test_bf16_batch_of_eight_verify_rows():
     note(f"batch 8: {compared} sequences compared")
 
 
+@pytest.mark.parametrize("T,topk", [(64, (8, 4, 2)), (128, (16, 4, 2))])
+def test_bf16_batch_of_sixteen_verify_rows(T, topk):
+    """Sixteen sequences verify 1024 or 2048 tree rows in one forward (the batch x tree cost
+    surface's largest cells: register-blocked GEMMs at those row counts with every epilogue,
+    attention over 16 paged sequences); each sequence's draft and verify logits stay within
+    the bf16 tolerance of its oracle over two teacher-forced steps."""
+    P = need_gpu()
+    note(f"engine bf16 batch 16, T={T}")
+    cfg = _bf16_small().with_(batch=16, topk=topk, tree_tokens=T, max_context=512)
+    w = synth.make_weights(cfg, seed=12, perturb=True)
+    eng = _engine(P, cfg, w)
+    o = oracle.CloverOracle(cfg, w)
+    states = []
+    for s in range(16):
+        prompt = synth.make_prompt(cfg, seq=s, n=20 + 17 * s)
+        assert eng.prefill(s, prompt) == (st := o.prefill(prompt)).t0
+        states.append(st)
+    stats = dict(steps=0, draft_rows=0, verify_rows=0, draft_ties=0, target_ties=0)
+    for _ in range(2):
+        teacher_forced_step(eng, o, states, 2e-2, stats)
+    note(f"batch 16, T={T}: {stats}")
+    assert stats["steps"] == 32 and stats["verify_rows"] == 32 * T
+    eng.close()
+
+
 def test_graph_replay_matches_eager_launches():
     """The step's phases replay as HIP graphs captured per batch size; every replay,
     with host work and batch-size changes in between, matches eager launches bit for bit."""
@@ -393,15 +420,15 @@ def test_graph_replay_matches_eager_launches():
     cfg, w = _tiny(batch=2)
     prompts = [synth.make_prompt(cfg, seq=s, n=100 + 30 * s) for s in range(2)]
     g = _engine(P, cfg, w)
-    e = _engine(P, cfg, w, flags=P.FLAG_EAGER)
+    e = _engine(P, cfg, w, flags=P.FLAG_EAGER | P.FLAG_KEEP_LOGITS)
     for s in range(2):
         assert g.prefill(s, prompts[s]) == e.prefill(s, prompts[s])
     schedule = [[0], [0, 1], [1], [0, 1], [0], [1, 0], [0, 1]]
     for i, seqs in enumerate(schedule):
         if i == 3:
-            g.set_flags(P.FLAG_EAGER)      # eager in the middle, graphs again after
+            g.set_flags(P.FLAG_EAGER | P.FLAG_KEEP_LOGITS)  # eager in the middle, graphs again after
         if i == 5:
-            g.set_flags(0)
+            g.set_flags(P.FLAG_KEEP_LOGITS)
         a, b = g.step(seqs), e.step(seqs)
         assert a == b, (i, seqs, a, b)
         rows = len(seqs) * cfg.tree_tokens
@@ -458,6 +485,36 @@ def test_medusa_tiny_fp32_sixteen_steps_match_oracle_and_greedy():
         eng.debug_kv(0, cfg.n_layers, 0, False)  # no Augmenting Block cache in Medusa mode
 
 
+def test_logits_are_stored_only_with_keep_logits():
+    """Without CLOVER_FLAG_KEEP_LOGITS the verify LM head stores only its argmax keys: the
+    logits buffer keeps what the last flagged step wrote while the targets move on.  With
+    the flag set again (the captured graphs are rebuilt) the logits are fresh and match
+    the oracle."""
+    P = need_gpu()
+    note("engine keep-logits flag")
+    cfg, w = _tiny(batch=1)
+    eng = _engine(P, cfg, w, flags=0)
+    o = oracle.CloverOracle(cfg, w)
+    prompt = synth.make_prompt(cfg, n=90)
+    st = o.prefill(prompt)
+    assert eng.prefill(0, prompt) == st.t0
+    T, V = cfg.tree_tokens, cfg.vocab
+    eng.set_flags(P.FLAG_KEEP_LOGITS)
+    assert eng.step([0])[0] == o.step(st)[0]
+    kept = eng.debug("verify_logits", np.float32, (T, V))
+    eng.set_flags(0)
+    for _ in range(2):
+        ref, det = o.step(st)
+        assert eng.step([0])[0] == ref
+        assert np.array_equal(eng.debug("target", np.int32, (T,)), det["ver"].target)
+        assert np.array_equal(eng.debug("verify_logits", np.float32, (T, V)), kept)
+    eng.set_flags(P.FLAG_KEEP_LOGITS)
+    ref, det = o.step(st)
+    assert eng.step([0])[0] == ref
+    assert float(np.max(np.abs(eng.debug("verify_logits", np.float32, (T, V)) - det["ver"].logits))) < 1e-4
+    eng.close()
+
+
 def test_medusa_bf16_batch_of_three_within_tolerance():
     """bf16 Medusa over three sequences of different lengths: each sequence's head logits
     and verify logits within 2e-2 of its oracle at every step, with the oracle
@@ -482,21 +539,24 @@ def test_medusa_bf16_batch_of_three_within_tolerance():
     assert stats["verify_rows"] == 9 * cfg.tree_tokens
 
 
-@pytest.mark.parametrize("draft,ab,ad_keys,per_head", [
-    ("clover", "attn", "single", False), ("clover", "mlp", "single", False),
-    ("clover", "none", "single", False), ("medusa", "full", "single", False),
-    ("clover", "default", "two", False), ("clover", "default", "path", False),
-    ("clover", "default", "two", True)])
-def test_speculator_variants_match_oracle(draft, ab, ad_keys, per_head):
+@pytest.mark.parametrize("draft,ab,ad_keys,per_head,regressive", [
+    ("clover", "attn", "single", False, "attention"), ("clover", "mlp", "single", False, "attention"),
+    ("clover", "none", "single", False, "attention"), ("medusa", "full", "single", False, "attention"),
+    ("clover", "default", "two", False, "attention"), ("clover", "default", "path", False, "attention"),
+    ("clover", "default", "two", True, "attention"), ("clover", "default", "single", False, "mlp"),
+    ("clover", "none", "single", False, "mlp")])
+def test_speculator_variants_match_oracle(draft, ab, ad_keys, per_head, regressive):
     """The Augmenting Block variants of Sec. 4.3 (attention half, MLP half, none) under the
     Clover draft, the Augmenting Block feeding parallel heads (Clover without Attention
-    Decoder and Regressive Connection), and the two-token and root-path key sets of the
-    Attention Decoder, and one decoder per head: tiny fp32, six steps, draft logits of every
-    frontier row and verify logits within 1e-4, candidate and verify trees exact, tokens
-    equal to the oracle's and to greedy decoding."""
+    Decoder and Regressive Connection), the two-token and root-path key sets of the
+    Attention Decoder, one decoder per head, and the MLP regressive block of the components
+    ablation (with and without the Augmenting Block): tiny fp32, six steps, draft logits of
+    every frontier row and verify logits within 1e-4, candidate and verify trees exact,
+    tokens equal to the oracle's and to greedy decoding."""
     P = need_gpu()
-    note(f"engine variant draft={draft} ab={ab} ad_keys={ad_keys} per_head={per_head}")
-    cfg = synth.get_config("tiny_fp32").with_(draft=draft, ab=ab, ad_keys=ad_keys, ad_per_head=per_head)
+    note(f"engine variant draft={draft} ab={ab} ad_keys={ad_keys} per_head={per_head} regressive={regressive}")
+    cfg = synth.get_config("tiny_fp32").with_(draft=draft, ab=ab, ad_keys=ad_keys, ad_per_head=per_head,
+                                              regressive=regressive)
     w = synth.make_weights(cfg, seed=1, perturb=True)
     eng = _engine(P, cfg, w)
     o = oracle.make_oracle(cfg, w)

@@ -70,7 +70,8 @@ def run(request):
              + heads + [f"layer0.{f}" for f in LayerWeights.__dataclass_fields__])
     host = {n: _f64(w[n]) for n in names}
     emb = w["emb"].cpu()
-    eng = P.CloverEngine(cfg, w, max_batch=B, max_context=max(lens) + 256, free_source=True)
+    eng = P.CloverEngine(cfg, w, max_batch=B, max_context=max(lens) + 256, free_source=True,
+                         flags=P.FLAG_KEEP_LOGITS)
     del w
     torch.cuda.empty_cache()
     for b in range(B):

@@ -25,6 +25,11 @@ GEMM_CASES = [
     # register-blocked kernel: swept 7B shapes, the default rule, ragged row counts
     ("bf16", 129, 12288, 4096, True), ("bf16", 256, 4096, 11008, True), ("bf16", 300, 4096, 4096, True),
     ("bf16", 512, 22016, 4096, True), ("bf16", 200, 125696, 4096, True), ("bf16", 130, 1024, 512, False),
+    # the cost surface's largest cells: 1024 and 2048 verify rows (batch 16 x 64- and 128-token trees)
+    ("bf16", 1024, 12288, 4096, True), ("bf16", 1024, 4096, 4096, False), ("bf16", 1024, 22016, 4096, True),
+    ("bf16", 1024, 4096, 11008, True), ("bf16", 1024, 125696, 4096, True),
+    ("bf16", 2048, 12288, 4096, True), ("bf16", 2048, 4096, 4096, True), ("bf16", 2048, 22016, 4096, True),
+    ("bf16", 2048, 4096, 11008, True), ("bf16", 2048, 125696, 4096, True), ("bf16", 1500, 4096, 4096, True),
 ]
 
 
@@ -195,3 +200,74 @@ def test_acceptance_bit_exact():
         assert A == len(acc_ref)
         assert list(acc.cpu().numpy()[:A]) == acc_ref
         assert int(bonus.item()) == bonus_ref
+
+
+def _slot_view(cache, block_table, n_slots, which_v):
+    """Logical rows [slot][n_kv][hd] of a paged pool [blocks][n_kv][16*hd], read through the
+    documented in-block layouts: K in score-fragment order (chunk d // KC, lane key + 16 *
+    ((d % KC) // EPL), element d % EPL), V as [d // 16][key // 4][d % 16][key % 4]."""
+    nb, nkv, per = cache.shape
+    hd = per // 16
+    EPL = 8 if cache.dtype == np.uint16 else 4
+    KC = 4 * EPL
+    d = np.arange(hd)
+    out = np.empty((n_slots, nkv, hd), dtype=cache.dtype)
+    for s in range(n_slots):
+        blk, key = block_table[s // 16], s % 16
+        if which_v:
+            idx = (((d >> 4) * 4 + (key >> 2)) * 16 + (d & 15)) * 4 + (key & 3)
+        else:
+            idx = ((d // KC) * 64 + key + 16 * ((d % KC) // EPL)) * EPL + (d % EPL)
+        out[s] = cache[blk][:, idx]
+    return out
+
+
+@pytest.mark.parametrize("dt,acc", [("bf16", [0, 5, 9, 17]), ("bf16", [0, 1, 3, 4]), ("bf16", [0, 2, 3]),
+                                    ("bf16", [0]), ("f32", [0, 7, 8, 20, 31]), ("bf16", [0, 3, 12, 40, 63])])
+def test_compact_moves_accepted_slots_bit_exactly(dt, acc):
+    """KV compaction (the commit of Sec. 2.1): on every layer the rows of slot L + acc[j]
+    land in slot L + j byte for byte, sources that are also destinations (acc[j'] = j) are
+    read before being overwritten, and every other slot is left as it was.  The sequence's
+    pages are scattered over the pool in a shuffled order, with L crossing a page."""
+    P = need_gpu()
+    note(f"compact {dt} acc={acc}")
+    nl, nkv, hd, nb = 3, 2, 128 if dt == "bf16" else 64, 12
+    rng = np.random.default_rng(len(acc) * 31 + acc[-1])
+    table = rng.permutation(nb)[:7].astype(np.int32)
+    L = 37
+    np_dt = np.uint16 if dt == "bf16" else np.uint32
+    k0 = rng.integers(0, 2 ** (16 if dt == "bf16" else 32), size=(nl, nb, nkv, 16 * hd), dtype=np.uint64).astype(np_dt)
+    v0 = rng.integers(0, 2 ** (16 if dt == "bf16" else 32), size=(nl, nb, nkv, 16 * hd), dtype=np.uint64).astype(np_dt)
+    tdt = torch.int16 if dt == "bf16" else torch.int32
+    kc = torch.from_numpy(k0.view(np.int16 if dt == "bf16" else np.int32)).cuda()
+    vc = torch.from_numpy(v0.view(np.int16 if dt == "bf16" else np.int32)).cuda()
+    if dt == "bf16":
+        kc, vc = kc.view(torch.bfloat16), vc.view(torch.bfloat16)
+    else:
+        kc, vc = kc.view(torch.float32), vc.view(torch.float32)
+    P.op_compact(kc, vc, table, L, acc)
+    k1 = kc.view(tdt).cpu().numpy().view(np_dt)
+    v1 = vc.view(tdt).cpu().numpy().view(np_dt)
+    n_slots = 16 * len(table)
+    for layer in range(nl):
+        for which, before, after in ((0, k0, k1), (1, v0, v1)):
+            b = _slot_view(before[layer], table, n_slots, which)
+            a = _slot_view(after[layer], table, n_slots, which)
+            want = b.copy()
+            want[L + np.arange(len(acc))] = b[L + np.asarray(acc)]  # gather all, then store
+            assert np.array_equal(a, want), (layer, which)
+        # blocks outside the table are untouched
+        rest = np.setdiff1d(np.arange(nb), table)
+        assert np.array_equal(k1[layer][rest], k0[layer][rest]) and np.array_equal(v1[layer][rest], v0[layer][rest])
+
+
+def test_compact_rejects_out_of_range_arguments():
+    P = need_gpu()
+    note("compact argument checks")
+    kc = torch.zeros(1, 4, 1, 16 * 32, dtype=torch.bfloat16, device="cuda")
+    vc = torch.zeros_like(kc)
+    for table, L, acc in (([0, 4], 0, [0]), ([0, 1], 31, [0, 1]), ([0, 1], 10, [0, -1]), ([0, 1], 0, [0] * 10)):
+        with pytest.raises(P.CloverError):
+            P.op_compact(kc, vc, table, L, acc)
+    assert torch.count_nonzero(kc.float()) == 0
+

@@ -121,3 +121,21 @@ def test_bf16_rounding_matches_torch():
     ref = torch.tensor(x, dtype=torch.float32).to(torch.bfloat16).double().numpy()
     assert np.array_equal(got, ref)
     assert np.array_equal(Precision("f32").store(x), x)
+
+
+def test_bf16_precision_model_drifts_between_valid_accumulation_orders():
+    """The bf16 precision model fixes where values are rounded, not the order of each dot
+    product's sum: with float32 instead of float64 sums (both exact for one product of
+    bf16 values) a few elements round to the neighbouring bf16 value and the layers after
+    carry the difference along.  On a small bf16 model the drift is nonzero, grows with
+    depth, and stays far below the logits' own scale; at the 7B shape it reaches 0.15
+    max-abs on the logits after 32 layers (oracle/noise_floor.py)."""
+    from oracle.noise_floor import measure
+    cfg = synth.CloverConfig(name="nf", n_layers=6, d_model=512, n_heads=4, n_kv_heads=4, head_dim=128,
+                             ffn_dim=1376, vocab=2048, dtype="bf16", topk=(2,), tree_tokens=2)
+    rel, dmax, dmean = measure(cfg, rows=32, log=lambda m: None)
+    assert rel[0] > 0 and rel[-1] > rel[0]
+    assert 0 < dmean < dmax < 0.25
+    f32 = cfg.with_(dtype="f32")
+    rel32, dmax32, _ = measure(f32, n_layers=2, rows=8, log=lambda m: None)
+    assert dmax32 < 1e-3  # without bf16 rounding points the two orders agree to fp32 precision
