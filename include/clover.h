@@ -297,6 +297,18 @@ size_t clover_packed_matrix_bytes(int32_t dtype, int32_t rows, int32_t cols);
 clover_status clover_pack_matrix(int32_t dtype, const void* src, int32_t rows, int32_t cols,
                                  void* dst, void* hip_stream);
 
+/* clover_op_linear for callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops that forbid allocation): the same kernels, with the split-K
+ * partials in a 16 MiB device array the library owns (one per GPU, kept until the process
+ * ends) instead of a caller scratch buffer.  The call allocates nothing.  Shapes whose
+ * partials need more than clover_op_linear_noalloc_max_bytes() bytes (clover_op_scratch_bytes)
+ * are rejected with CLOVER_ERR_CAPACITY before anything is enqueued.  Every call on one GPU
+ * shares that GPU's array, so calls that overlap in time on one GPU (other streams, other
+ * threads) race; calls ordered on one stream do not.  Errors: INVALID_ARG, CAPACITY, DEVICE. */
+size_t clover_op_linear_noalloc_max_bytes(void);
+clover_status clover_op_linear_noalloc(int32_t dtype, const void* X, int32_t M, int32_t K, const void* Wp,
+                                       int32_t N, float* Y, void* hip_stream);
+
 /* Tree attention (Sec. 2.2) for one sequence: queries Q[T][n_heads][head_dim] at
  * positions L + depth attend to prefix keys 0..L-1 and to tree keys j with
  * mask[i][j] (ancestor-or-self of i, from parents).  Kpre/Vpre: [L][n_kv][hd] and

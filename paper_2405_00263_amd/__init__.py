@@ -95,6 +95,9 @@ EXPORTS = {
     "clover_op_topk": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     "clover_op_tree_build": (ctypes.c_int, [ctypes.c_void_p] * 4 + [ctypes.c_int32] * 3 + [ctypes.c_void_p] * 6),
     "clover_op_accept": (ctypes.c_int, [ctypes.c_void_p] * 3 + [ctypes.c_int32] * 2 + [ctypes.c_void_p] * 4),
+    "clover_op_linear_noalloc_max_bytes": (ctypes.c_size_t, []),
+    "clover_op_linear_noalloc": (ctypes.c_int, [ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                                ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]),
     "clover_op_compact": (ctypes.c_int, [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p] + [ctypes.c_int32] * 4
                           + [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
                              ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
@@ -347,6 +350,18 @@ def op_linear(X, Wp, N: int):
     scratch = torch.empty(need, dtype=torch.uint8, device=X.device)
     _check(lib().clover_op_linear(dt, _ptr(X.contiguous()), M, K, _ptr(Wp), N, _ptr(Y), _ptr(scratch),
                                   need, ctypes.c_void_p(_stream_handle())))
+    return Y
+
+
+def op_linear_noalloc(X, Wp, N: int):
+    """op_linear through the allocation-free entry point (split-K partials in the library's
+    own device array); the output tensor is the caller's."""
+    import torch
+    dt = 1 if X.dtype == torch.bfloat16 else 0
+    M, K = X.shape
+    Y = torch.empty(M, N, dtype=torch.float32, device=X.device)
+    _check(lib().clover_op_linear_noalloc(dt, _ptr(X.contiguous()), M, K, _ptr(Wp), N, _ptr(Y),
+                                          ctypes.c_void_p(_stream_handle())))
     return Y
 
 

@@ -14,7 +14,7 @@ SRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libclover.so")
 BUILD = os.path.join(HERE, "_build")
 ARCH = "gfx950"
-SOURCES = ["gemm.hip", "gemm_tiled.hip", "attention.hip", "rows.hip", "tree.hip", "api.cpp"]
+SOURCES = ["gemm.hip", "gemm_tiled.hip", "attention.hip", "rows.hip", "tree.hip", "api.cpp", "noalloc.hip"]
 CFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           # per-kernel resource report, read by _check_no_scratch
           "-Rpass-analysis=kernel-resource-usage",

@@ -38,6 +38,14 @@ void set_global_err(const char* fmt, ...) {
   g_err = buf;
 }
 
+}  // namespace
+
+namespace clover {
+void set_last_error(const char* msg) { set_global_err("%s", msg); }
+}  // namespace clover
+
+namespace {
+
 constexpr size_t ALIGN = 256;
 constexpr int GEMM_MAX_SPLITS = 8;
 constexpr int QKV_MAX_SPLITS = 2;  // Q|K|V may be split when the plan prefers it (fix-up pass)

@@ -6,6 +6,13 @@
 
 namespace clover {
 
+// Message returned by clover_last_error(NULL) after a failed context-free call.
+void set_last_error(const char* msg);
+
+}  // namespace clover
+
+namespace clover {
+
 // Optional events filled with a kernel's own start and end times (hipExtLaunchKernel), so
 // that per-launch timing excludes the dispatch gaps that marker events would include.
 struct LaunchTiming {
