@@ -141,6 +141,12 @@ typedef struct {
                                      implies CLOVER_FLAG_EAGER */
 #define CLOVER_FLAG_EAGER 4       /* launch the step's kernels one by one instead of replaying the
                                      HIP graphs captured per batch size on first use */
+#define CLOVER_FLAG_AB_COMMIT 8   /* run the Augmenting Block at commit, over each sequence's
+                                     accepted rows, for every batch size.  Without it the block
+                                     runs there only when the verify has 129 or more rows
+                                     (batch x tree_tokens), and otherwise over the whole tree as
+                                     one more layer of the verify forward, its KV compacted with
+                                     the target's: both give the same h_0 and cache */
 
 typedef struct clover_ctx clover_ctx;
 

@@ -18,6 +18,7 @@ STATUS = {0: "OK", 1: "INVALID_ARG", 2: "CAPACITY", 3: "STATE", 4: "BAD_TREE", 5
 FLAG_KEEP_LOGITS = 1
 FLAG_PROFILE = 2
 FLAG_EAGER = 4
+FLAG_AB_COMMIT = 8
 KSTAT = {"gemm_verify": 0, "gemm_draft": 1, "attention": 2, "other": 3}
 DRAFT_MODES = {"clover": 0, "medusa": 1}
 AB_MODES = {"default": 0, "full": 1, "attn": 2, "mlp": 3, "none": 4}

@@ -304,6 +304,8 @@ Layout make_layout(const clover_config& c) {
     for (int b = 1; b <= c.max_batch; ++b) {
       a.nbatch = b; a.nq = L.T;
       af = std::max(af, attention_part_floats(a));
+      a.nq = L.H + 1;  // the Augmenting Block at commit
+      af = std::max(af, attention_part_floats(a));
     }
     a.nbatch = 1;
     for (int rows = 16; rows < L.Mp + 16; rows += 16) {
@@ -589,6 +591,17 @@ clover_status ensure_blocks(clover_ctx* c, int slot, int upto) {
 // choices need only the argmax keys of the epilogue.
 bool keep_logits(const clover_ctx* c) { return (c->cfg.flags & CLOVER_FLAG_KEEP_LOGITS) != 0; }
 
+// Where the Augmenting Block runs (Sec. 3.3: it extends the committed rows).  Over the whole
+// tree as layer N+1 of the verify, its KV compacted with the others, when the verify's rows
+// are few: its weights stream once either way.  At commit, over the <= H+1 accepted rows of
+// each sequence, when the verify has enough rows (B*T >= 129, the matrix-bound regime) that
+// running the block over every tree row would cost compute the commit does not.
+constexpr int AB_COMMIT_MIN_ROWS = 129;
+bool ab_at_commit(const clover_ctx* c, int B) {
+  return has_ab(c->cfg) &&
+         ((c->cfg.flags & CLOVER_FLAG_AB_COMMIT) || B * c->L.T >= AB_COMMIT_MIN_ROWS);
+}
+
 // LM-head argmax keys of the target's choices: plain argmax (greedy), or with temperature a
 // Gumbel-max sample per row (GemmParams::inv_temp).  domain 0: tree nodes (row m is node
 // m % rows_per_seq of sequence slot_of_row[m]); 1: the token after the prompt.
@@ -642,7 +655,8 @@ hipError_t enq_verify(clover_ctx* c, int B, int max_keys) {
     ProfScope ps(c, CLOVER_KSTAT_OTHER, 0, 0);
     HE(launch_argmax_groups(c->at<unsigned long long>(L.amax_part), lm_groups, M, c->at<int>(L.target), c->st));
   }
-  if (!has_ab(cf)) return trace_rows(c, cf.n_layers + 1, xa, M);  // xa keeps x_N: the next draft reads it
+  // xa keeps x_N: the next draft reads it (no block), or the block runs at commit
+  if (!has_ab(cf) || ab_at_commit(c, B)) return trace_rows(c, cf.n_layers + 1, xa, M);
   // Augmenting Block over the tree (tree mask, its own KV cache)
   HE(run_layer(c, c->layers[cf.n_layers], cf.n_layers, xa, M, att, max_keys, 0, &pend, ab_attn(cf), ab_mlp(cf)));
   RowFixParams ra{};
@@ -652,18 +666,21 @@ hipError_t enq_verify(clover_ctx* c, int B, int max_keys) {
   return trace_rows(c, cf.n_layers + 1, xa, M);
 }
 
-// Greedy acceptance, bonus token, h_0 for the next draft, KV compaction of every layer.
-hipError_t enq_accept(clover_ctx* c, int B) {
+// Greedy acceptance, bonus token, KV compaction of every layer, h_0 for the next draft (the
+// Augmenting Block's output at the last accepted node: from the tree, or from the block run
+// here over the accepted rows).
+hipError_t enq_accept(clover_ctx* c, int B, int max_keys) {
   const clover_config& cf = c->cfg;
   const Layout& L = c->L;
   const int T = L.T, d = cf.d_model, H = L.H;
+  const bool commit = ab_at_commit(c, B);
   AcceptParams ap{};
   ap.seq_ids = c->at<int>(L.seq_ids); ap.nbatch = B; ap.T = T; ap.H = H;
   ap.tree_token = c->at<int>(L.tree_token); ap.tree_parent = c->at<int>(L.tree_parent);
   ap.target = c->at<int>(L.target);
   ap.acc = c->at<int>(L.acc); ap.acc_len = c->at<int>(L.acc_len);
   ap.out_tokens = c->at<int>(L.out_tokens); ap.t0 = c->at<int>(L.t0);
-  ap.ab_out = c->at<float>(L.xa); ap.d = d; ap.h0 = c->at<float>(L.h0);
+  ap.ab_out = c->at<float>(L.xa); ap.d = d; ap.h0 = commit ? nullptr : c->at<float>(L.h0);
   ap.step_ctr = c->at<int>(L.sample_step);
   {
     ProfScope ps(c, CLOVER_KSTAT_OTHER, 0, 0);
@@ -673,11 +690,34 @@ hipError_t enq_accept(clover_ctx* c, int B) {
   cp.seq_ids = c->at<int>(L.seq_ids); cp.nbatch = B; cp.H = H;
   cp.acc = c->at<int>(L.acc); cp.acc_len = c->at<int>(L.acc_len); cp.seq_len = c->at<int>(L.seq_len);
   cp.kpools = c->at<void*>(L.pool_ptrs); cp.vpools = c->at<void*>(L.pool_ptrs) + kv_layers(cf);
-  cp.nlayers = kv_layers(cf);
+  cp.nlayers = commit ? cf.n_layers : kv_layers(cf);  // at commit the block writes its own KV
   cp.block_table = c->at<int>(L.block_table); cp.max_blocks = L.mbps;
   cp.n_kv = cf.n_kv_heads; cp.hd = cf.head_dim;
-  ProfScope ps(c, CLOVER_KSTAT_OTHER, 0, 0);
-  return launch_compact(cf.dtype, cp, c->st);
+  {
+    ProfScope ps(c, CLOVER_KSTAT_OTHER, 0, 0);
+    HE(launch_compact(cf.dtype, cp, c->st));
+  }
+  if (!commit) return hipSuccess;
+  // the Augmenting Block over each sequence's accepted rows (x_N), causal against its cache
+  const int Mab = B * (H + 1);
+  float* xr = c->at<float>(L.x);
+  HE(launch_ab_commit_rows(c->at<int>(L.seq_ids), B, T, H, c->at<int>(L.acc), c->at<int>(L.acc_len),
+                           c->at<int>(L.seq_len), c->at<float>(L.xa), d, xr, c->at<int>(L.row_pos),
+                           c->at<int>(L.row_slot), c->at<int>(L.row_seq), c->st));
+  HE(launch_rope_table(c->at<int>(L.row_pos), Mab, cf.head_dim, cf.rope_theta, c->at<float>(L.rope_cs), c->st));
+  AttnParams att{};
+  att.seq_ids = c->at<int>(L.seq_ids);
+  att.prefix_dev = c->at<int>(L.seq_len);
+  att.rows_per_seq = H + 1; att.nq = H + 1; att.n_tail = H + 1; att.causal = 1;
+  att.nbatch = B;
+  att.part = c->at<float>(L.apart); att.part_cap = L.apart_floats;
+  int pend = 0;
+  HE(run_layer(c, c->layers[cf.n_layers], cf.n_layers, xr, Mab, att, max_keys, 0, &pend, ab_attn(cf), ab_mlp(cf)));
+  RowFixParams ra{};
+  ra.M = Mab; ra.d = d; ra.part = c->at<float>(L.gpart); ra.S = pend; ra.ldp = d;
+  ra.resid = xr; ra.ldr = d; ra.out_f = xr; ra.ldo = d;
+  HE(run_rowfix(c, ra));
+  return launch_ab_commit_h0(c->at<int>(L.seq_ids), B, H, c->at<int>(L.acc_len), xr, d, c->at<float>(L.h0), c->st);
 }
 
 // Emitted tokens to the host, one stream sync, host mirrors and phase timings.
@@ -1287,7 +1327,7 @@ clover_status clover_step(clover_ctx* c, const int32_t* seqs, int32_t n_seqs, in
   c->phase = CLOVER_KSTAT_GEMM_VERIFY;
   HIPCK(c, run_phase(c, &c->graphs[B].verify, graph, [&] { return enq_verify(c, B, max_keys); }));
   HIPCK(c, hipEventRecord(c->ev[2], c->st));
-  HIPCK(c, run_phase(c, &c->graphs[B].accept, graph, [&] { return enq_accept(c, B); }));
+  HIPCK(c, run_phase(c, &c->graphs[B].accept, graph, [&] { return enq_accept(c, B, max_keys); }));
   c->last_nbatch = B;
   s = finish_step(c, B, out_tokens, out_count);
   c->in_step = false;
@@ -1360,7 +1400,7 @@ clover_status clover_verify_tree(clover_ctx* c, int32_t seq, const int32_t* toke
   c->phase = CLOVER_KSTAT_GEMM_VERIFY;
   HIPCK(c, enq_verify(c, 1, max_keys));
   HIPCK(c, hipEventRecord(c->ev[2], c->st));
-  HIPCK(c, enq_accept(c, 1));
+  HIPCK(c, enq_accept(c, 1, max_keys));
   s = finish_step(c, 1, out_tokens, out_count);
   c->in_step = false;
   return s;
@@ -1471,10 +1511,11 @@ clover_status clover_kernel_stats_get(clover_ctx* c, int32_t kind, clover_kernel
 clover_status clover_set_flags(clover_ctx* c, int32_t flags) {
   clover_status s = check_ctx(c);
   if (s) return s;
-  if (flags & ~(CLOVER_FLAG_KEEP_LOGITS | CLOVER_FLAG_PROFILE | CLOVER_FLAG_EAGER))
+  if (flags & ~(CLOVER_FLAG_KEEP_LOGITS | CLOVER_FLAG_PROFILE | CLOVER_FLAG_EAGER | CLOVER_FLAG_AB_COMMIT))
     return ctx_fail(c, CLOVER_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
-  if ((flags ^ c->cfg.flags) & CLOVER_FLAG_KEEP_LOGITS) {
-    // the captured verify phases bake in whether the LM head stores its logits
+  if ((flags ^ c->cfg.flags) & (CLOVER_FLAG_KEEP_LOGITS | CLOVER_FLAG_AB_COMMIT)) {
+    // the captured phases bake in whether the LM head stores its logits and where the
+    // Augmenting Block runs
     (void)hipStreamSynchronize(c->st);
     for (auto& g : c->graphs)
       for (hipGraphExec_t* x : {&g.draft, &g.verify, &g.accept})

@@ -253,6 +253,14 @@ hipError_t launch_fill_i32(int* p, int v, size_t n, hipStream_t st);
 hipError_t launch_set_root(const int* seq_ids, int nbatch, const int* t0, int* cand_token,
                            int* cand_parent, int* cand_depth, float* cand_lp, int cand_stride,
                            hipStream_t st);
+// Augmenting Block at commit: gather each listed sequence's accepted rows of x_N (tree rows
+// [nbatch*T][d]) into x_rows [nbatch*(H+1)][d] with their positions / KV slots L + j, and
+// afterwards take h_0 from the block's output at the last accepted row.
+hipError_t launch_ab_commit_rows(const int* seq_ids, int nbatch, int T, int H, const int* acc, const int* acc_len,
+                                 const int* seq_len, const float* x_tree, int d, float* x_rows, int* row_pos,
+                                 int* row_slot, int* row_seq, hipStream_t st);
+hipError_t launch_ab_commit_h0(const int* seq_ids, int nbatch, int H, const int* acc_len, const float* ab_rows,
+                               int d, float* h0, hipStream_t st);
 // end of prefill: t0[slot] = argmax result, h0[slot] = AB output row
 hipError_t launch_finish_prefill(int slot, const int* amax, const float* ab_row, int d, int* t0,
                                  float* h0, hipStream_t st);

@@ -265,6 +265,53 @@ hipError_t launch_medusa_expand(const MedusaExpandParams& p, hipStream_t st) {
   return hipGetLastError();
 }
 
+// ---- Augmenting Block at commit (Sec. 3.3: the block runs over the newly committed rows) --------
+// Rows b*(H+1) + j, j = 0..H, of sequence b: the residual x_N of accepted node acc[j] (the
+// last accepted node repeated past A), at position and KV slot L + j.  Rows past A stand in
+// for a fixed launch size; their keys land in slots past the committed length, which the
+// next tree overwrites.
+__global__ void ab_commit_rows_kernel(const int* seq_ids, int T, int H, const int* acc, const int* acc_len,
+                                      const int* seq_len, const float* x_tree, int d, float* x_rows,
+                                      int* row_pos, int* row_slot, int* row_seq) {
+  const int b = blockIdx.x, j = blockIdx.y, slot = seq_ids[b];
+  const int A = acc_len[slot], L = seq_len[slot];
+  const int src = acc[(size_t)slot * (H + 1) + min(j, A - 1)];
+  const int row = b * (H + 1) + j;
+  const float4* s = reinterpret_cast<const float4*>(x_tree + (size_t)(b * T + src) * d);
+  float4* o = reinterpret_cast<float4*>(x_rows + (size_t)row * d);
+  for (int k = threadIdx.x; k < d / 4; k += blockDim.x) o[k] = s[k];
+  if (threadIdx.x == 0) {
+    row_pos[row] = L + j;
+    row_slot[row] = L + j;
+    row_seq[row] = slot;
+  }
+}
+
+hipError_t launch_ab_commit_rows(const int* seq_ids, int nbatch, int T, int H, const int* acc, const int* acc_len,
+                                 const int* seq_len, const float* x_tree, int d, float* x_rows, int* row_pos,
+                                 int* row_slot, int* row_seq, hipStream_t st) {
+  if (nbatch <= 0) return hipSuccess;
+  if (d % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(ab_commit_rows_kernel, dim3(nbatch, H + 1), dim3(256), 0, st, seq_ids, T, H, acc, acc_len,
+                     seq_len, x_tree, d, x_rows, row_pos, row_slot, row_seq);
+  return hipGetLastError();
+}
+
+// h_0 of each listed sequence: the block's output at its last accepted row b*(H+1) + A - 1
+__global__ void ab_commit_h0_kernel(const int* seq_ids, int H, const int* acc_len, const float* ab_rows, int d,
+                                    float* h0) {
+  const int b = blockIdx.x, slot = seq_ids[b];
+  const float* s = ab_rows + (size_t)(b * (H + 1) + acc_len[slot] - 1) * d;
+  for (int k = threadIdx.x; k < d; k += blockDim.x) h0[(size_t)slot * d + k] = s[k];
+}
+
+hipError_t launch_ab_commit_h0(const int* seq_ids, int nbatch, int H, const int* acc_len, const float* ab_rows,
+                               int d, float* h0, hipStream_t st) {
+  if (nbatch <= 0) return hipSuccess;
+  hipLaunchKernelGGL(ab_commit_h0_kernel, dim3(nbatch), dim3(256), 0, st, seq_ids, H, acc_len, ab_rows, d, h0);
+  return hipGetLastError();
+}
+
 __global__ void finish_prefill_kernel(int slot, const int* amax, const float* ab_row, int d, int* t0,
                                       float* h0) {
   if (threadIdx.x == 0) t0[slot] = amax[0];

@@ -68,18 +68,23 @@ def test_tiny_fp32_sixteen_steps_match_oracle_and_greedy():
                 assert np.max(np.abs(got - kv[which][pos].reshape(-1))) < 1e-4, (layer, pos, which)
 
 
-def test_planted_trees_accept_every_length():
+@pytest.mark.parametrize("ab_commit", [False, True])
+def test_planted_trees_accept_every_length(ab_commit):
+    """Planted trees force every acceptance length; greedy decoding continues exactly.  With
+    CLOVER_FLAG_AB_COMMIT the Augmenting Block runs over the accepted rows at commit instead
+    of over the tree: the next draft's state h_0 must still be the oracle's (Sec. 3.3)."""
     P = need_gpu()
-    note("engine planted trees")
+    note(f"engine planted trees, ab_commit={ab_commit}")
     cfg, w = _tiny()
     o = oracle.CloverOracle(cfg, w)
     prompt = synth.make_prompt(cfg, seq=3)
     ar = o.base.greedy_generate(prompt, 12)
     H = cfg.n_spec_heads
-    eng = _engine(P, cfg, w)
+    eng = _engine(P, cfg, w, flags=P.FLAG_KEEP_LOGITS | (P.FLAG_AB_COMMIT if ab_commit else 0))
     for A in range(1, H + 2):
         t0 = eng.prefill(0, prompt)
         assert t0 == ar[0]
+        st = o.prefill(prompt)
         toks, par, prev = [t0, (ar[1] + 1) % cfg.vocab], [-1, 0], 0
         for d in range(1, H + 1):
             toks.append(ar[d] if d < A else (ar[d] + 3) % cfg.vocab)
@@ -88,6 +93,15 @@ def test_planted_trees_accept_every_length():
         got = eng.verify_tree(0, toks, par)
         assert got == ar[1:A + 1], (A, got)
         assert eng.debug("acc_len", np.int32, (1,))[0] == A
+        o.step_tree(st, o.planted_tree(st, toks, par))
+        h0 = eng.debug("h0", np.float32, (1, cfg.d_model))[0]
+        assert np.max(np.abs(h0 - st.h0)) < 1e-4, A
+        for layer in (0, cfg.n_layers):  # a target layer and the Augmenting Block
+            for j in range(A):
+                for which in (0, 1):
+                    kv = st.kv[layer] if layer < cfg.n_layers else st.ab_kv
+                    ref = kv[which][st.L - A + j].reshape(-1)
+                    assert np.max(np.abs(eng.debug_kv(0, layer, st.L - A + j, bool(which)) - ref)) < 1e-4
         # then continue with drafted steps: still greedy
         out = []
         while len(out) < 6:
@@ -412,23 +426,28 @@ def test_bf16_batch_of_sixteen_verify_rows(T, topk):
     eng.close()
 
 
-def test_graph_replay_matches_eager_launches():
+def ab_flag(P, ab_commit):
+    return P.FLAG_AB_COMMIT if ab_commit else 0
+
+
+@pytest.mark.parametrize("ab_commit", [False, True])
+def test_graph_replay_matches_eager_launches(ab_commit):
     """The step's phases replay as HIP graphs captured per batch size; every replay,
     with host work and batch-size changes in between, matches eager launches bit for bit."""
     P = need_gpu()
     note("engine graph vs eager")
     cfg, w = _tiny(batch=2)
     prompts = [synth.make_prompt(cfg, seq=s, n=100 + 30 * s) for s in range(2)]
-    g = _engine(P, cfg, w)
-    e = _engine(P, cfg, w, flags=P.FLAG_EAGER | P.FLAG_KEEP_LOGITS)
+    g = _engine(P, cfg, w, flags=P.FLAG_KEEP_LOGITS | ab_flag(P, ab_commit))
+    e = _engine(P, cfg, w, flags=P.FLAG_EAGER | P.FLAG_KEEP_LOGITS | ab_flag(P, ab_commit))
     for s in range(2):
         assert g.prefill(s, prompts[s]) == e.prefill(s, prompts[s])
     schedule = [[0], [0, 1], [1], [0, 1], [0], [1, 0], [0, 1]]
     for i, seqs in enumerate(schedule):
         if i == 3:
-            g.set_flags(P.FLAG_EAGER | P.FLAG_KEEP_LOGITS)  # eager in the middle, graphs again after
+            g.set_flags(P.FLAG_EAGER | P.FLAG_KEEP_LOGITS | ab_flag(P, ab_commit))  # eager in the middle
         if i == 5:
-            g.set_flags(P.FLAG_KEEP_LOGITS)
+            g.set_flags(P.FLAG_KEEP_LOGITS | ab_flag(P, ab_commit))  # graphs again after
         a, b = g.step(seqs), e.step(seqs)
         assert a == b, (i, seqs, a, b)
         rows = len(seqs) * cfg.tree_tokens
