@@ -276,6 +276,67 @@ def surface(args):
         torch.cuda.empty_cache()
 
 
+def context_grid(args):
+    """Tree-size x context grid on the 7B shape at batch 1: tree sizes {16, 32, 64, 128}
+    (top-k (4,2,2), (4,3,2), (8,4,2), (16,4,2), root included) x committed contexts {512,
+    4096, 16384, 32768} filled by a real prefill of uniform-random tokens.  One JSON line per
+    cell: whole-step throughput and latency, the verify and draft (Clover heads) latencies
+    from the graph-replayed steps, then from a second pass with every launch timed by HIP
+    events: the tree-masked attention's time per layer (attention kernel plus its key-split
+    merge) and its rate over the algorithmic KV bytes (every committed key and value, and the
+    tree's, read once per layer, plus Q and O), and the verify GEMMs' weight-stream rate."""
+    import torch
+    import synth
+    import paper_2405_00263_amd as P
+
+    base = synth.get_config("llama7b_b1")
+    print(f"[grid] {len(synth.SWEEP_TREES) * len(synth.SWEEP_CONTEXTS)} cells: generating weights on device",
+          file=sys.stderr, flush=True)
+    w = synth.make_weights(base, seed=args.seed, device="cuda")
+    kt = max(3, args.steps // 2)
+    for T, topk in synth.SWEEP_TREES:
+        for L0 in synth.SWEEP_CONTEXTS:
+            cfg = base.with_(tree_tokens=T, topk=topk, prompt_len=(L0, L0))
+            H1 = cfg.n_spec_heads + 1
+            eng = P.CloverEngine(cfg, w, max_batch=1, max_context=L0 + (args.warmup + args.steps + kt) * H1 + T + 16)
+            eng.prefill(0, synth.make_prompt(cfg, n=L0))
+            for _ in range(args.warmup):
+                eng.step([0])
+            ph = {"draft_ms": [], "verify_ms": [], "total_ms": []}
+            gc.collect()
+            gc.disable()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(args.steps):
+                eng.step([0])
+                tm = eng.timings()
+                for k in ph:
+                    ph[k].append(tm[k])
+            torch.cuda.synchronize()
+            step_ms = 1e3 * (time.perf_counter() - t0) / args.steps
+            gc.enable()
+            eng.set_flags(P.FLAG_PROFILE)
+            eng.reset_kernel_stats()
+            for _ in range(kt):
+                eng.step([0])
+            eng.set_flags(0)
+            ks = eng.kernel_stats()
+            att, gv = ks["attention"], ks["gemm_verify"]
+            med = {k: statistics.median(v) for k, v in ph.items()}
+            print(json.dumps({"grid_cell": {
+                "tree_tokens": T, "topk": list(topk), "context": L0,
+                "step_ms": round(step_ms, 4), "tree_tokens_per_s": round(T / (step_ms * 1e-3), 1),
+                "verify_ms": round(med["verify_ms"], 4), "draft_ms": round(med["draft_ms"], 4),
+                "attention_us_per_layer": round(1e3 * att["total_ms"] / max(1, att["launches"]), 2),
+                "attention_GBps": round(att["bytes"] / (att["total_ms"] * 1e-3) / 1e9, 1) if att["total_ms"] else 0.0,
+                "attention_kv_MB_per_layer": round(att["bytes"] / max(1, att["launches"]) / 1e6, 2),
+                "verify_gemm_GBps": round(gv["bytes"] / (gv["total_ms"] * 1e-3) / 1e9, 1) if gv["total_ms"] else 0.0,
+            }}), flush=True)
+            eng.close()
+            del eng
+            torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -299,10 +360,14 @@ def main():
     ap.add_argument("--regressive", default="", choices=["", "attention", "mlp"],
                     help="override the Clover draft's regressive block: the Attention Decoder or the "
                          "MLP over [RMSNorm(h); e] of the components ablation (Sec. 4.3)")
+    ap.add_argument("--medusa-lm", default="", choices=["", "shared", "per_head"],
+                    help="Medusa draft: heads share the target's LM head, or each has its own (Sec. 3.4)")
     ap.add_argument("--temperature", type=float, default=-1.0,
                     help="override the sampling temperature (0: greedy; > 0: speculative sampling)")
     ap.add_argument("--surface", action="store_true",
                     help="batch x tree-size cost surface instead of the headline line (one JSON line per cell)")
+    ap.add_argument("--context-grid", action="store_true",
+                    help="tree-size x context grid at the 7B shape, batch 1 (one JSON line per cell)")
     ap.add_argument("--surface-batches", default="1,2,4,8,16")
     ap.add_argument("--surface-trees", default="4,16,32,64,128")
     args = ap.parse_args()
@@ -313,6 +378,9 @@ def main():
         sys.exit(2)
     if args.surface:
         surface(args)
+        return
+    if args.context_grid:
+        context_grid(args)
         return
 
     import torch
@@ -335,6 +403,8 @@ def main():
         over["ad_keys"] = args.ad_keys
     if args.regressive:
         over["regressive"] = args.regressive
+    if args.medusa_lm:
+        over["medusa_lm"] = args.medusa_lm
     if args.temperature >= 0:
         over["temperature"] = args.temperature
     if over:
@@ -417,6 +487,7 @@ def main():
         "data": "synthetic: random-init N(0,0.02) weights, uniform-random prompt tokens",
         "config": {"workload": cfg.name, "speculator": cfg.draft, "augmenting_block": cfg.ab_kind,
                    "decoder_keys": cfg.ad_keys, "regressive_block": cfg.regressive,
+                   "medusa_lm_heads": cfg.medusa_lm,
                    "temperature": cfg.temperature,
                    "n_layers": cfg.n_layers, "d_model": d,
                    "n_heads": cfg.n_heads, "n_kv_heads": cfg.n_kv_heads, "head_dim": cfg.head_dim,

@@ -129,6 +129,10 @@ typedef struct {
   uint32_t sample_seed;
   int32_t regressive;   /* clover_regressive (Clover draft); with CLOVER_REGRESSIVE_MLP, ad_keys
                            must be single and ad_per_head 0 */
+  int32_t medusa_lm_heads; /* Medusa draft only.  0: the heads share the target's LM head (one
+                           LM-head pass over every head's rows); 1: each head carries its own
+                           LM head, as in the original Medusa (Sec. 3.4): weights head{j}.lm
+                           [vocab, d_model], one LM-head pass per head */
 } clover_config;
 
 #define CLOVER_FLAG_KEEP_LOGITS 1 /* the verify and prefill LM heads also store their fp32 logits,
@@ -163,7 +167,8 @@ clover_status clover_check_config(const clover_config* cfg);
  * heads and supplies the Regressive Connection embeddings (Sec. 3.4).  With
  * CLOVER_DRAFT_MEDUSA the ad.* entries are left out; with ad_per_head they are
  * ad{j}.{norm,wq,wk,wv,wo} for each head j instead of one ad.* set; with CLOVER_REGRESSIVE_MLP
- * they are rb.{norm [d], w [d, 2d], b [d]} instead of ad.*; the ab.* entries are those of the
+ * they are rb.{norm [d], w [d, 2d], b [d]} instead of ad.*; with medusa_lm_heads each head's
+ * entries are head{j}.{w1,b1,lm}; the ab.* entries are those of the
  * Augmenting Block's halves that clover_ab_mode keeps (attn_norm, wq, wk, wv, wo for the
  * attention half, mlp_norm, w_gate, w_up, w_down for the MLP half). */
 size_t clover_weight_count(const clover_config* cfg);

@@ -30,11 +30,19 @@ shared LM head are the ones used here).
 """
 import numpy as np
 
-from .clover import Candidates, CloverOracle, SeqState, topk_ids
-from .model import logsumexp
+from .clover import Candidates, CloverOracle, SeqState, head_mlp, topk_ids
+from .model import logsumexp, rmsnorm
 
 
 class MedusaOracle(CloverOracle):
+    def head_logits(self, j: int, s: np.ndarray) -> np.ndarray:
+        """Head j's MLP on the state, the shared final norm, then the shared LM head or, with
+        per-head LM heads (the original Medusa, Sec. 3.4), head j's own."""
+        if getattr(self.cfg, "medusa_lm", "shared") != "per_head":
+            return super().head_logits(j, s)
+        r = head_mlp(s, self.w[f"head{j}.w1"], self.w[f"head{j}.b1"], self.prec)
+        return self.prec.store(rmsnorm(r, self.w["final_norm"], self.cfg.rms_eps)) @ self.w[f"head{j}.lm"].T
+
     def draft(self, st: SeqState) -> Candidates:
         c = self.cfg
         H = c.n_spec_heads

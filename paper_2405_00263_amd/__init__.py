@@ -24,6 +24,7 @@ DRAFT_MODES = {"clover": 0, "medusa": 1}
 AB_MODES = {"default": 0, "full": 1, "attn": 2, "mlp": 3, "none": 4}
 AD_KEYS = {"single": 0, "two": 1, "path": 2}
 REGRESSIVE = {"attention": 0, "mlp": 1}
+MEDUSA_LM = {"shared": 0, "per_head": 1}
 
 
 class CloverError(RuntimeError):
@@ -45,7 +46,7 @@ class ConfigC(ctypes.Structure):
                 ("draft_mode", ctypes.c_int32), ("ab_mode", ctypes.c_int32),
                 ("ad_keys", ctypes.c_int32), ("ad_per_head", ctypes.c_int32),
                 ("temperature", ctypes.c_float), ("sample_seed", ctypes.c_uint32),
-                ("regressive", ctypes.c_int32)]
+                ("regressive", ctypes.c_int32), ("medusa_lm_heads", ctypes.c_int32)]
 
 
 class TimingsC(ctypes.Structure):
@@ -153,6 +154,7 @@ def make_config(cfg, max_batch: Optional[int] = None, max_context: Optional[int]
     c.temperature = float(getattr(cfg, "temperature", 0.0))
     c.sample_seed = int(getattr(cfg, "sample_seed", 0)) & 0xFFFFFFFF
     c.regressive = REGRESSIVE[getattr(cfg, "regressive", "attention")]
+    c.medusa_lm_heads = MEDUSA_LM[getattr(cfg, "medusa_lm", "shared")]
     return c
 
 

@@ -54,6 +54,7 @@ size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 int es_of(int dtype) { return dtype == CLOVER_BF16 ? 2 : 4; }
 bool is_medusa(const clover_config& c) { return c.draft_mode == CLOVER_DRAFT_MEDUSA; }
 bool mlp_regressive(const clover_config& c) { return !is_medusa(c) && c.regressive == CLOVER_REGRESSIVE_MLP; }
+bool per_head_lm(const clover_config& c) { return is_medusa(c) && c.medusa_lm_heads == 1; }
 int ab_mode(const clover_config& c) {
   if (c.ab_mode != CLOVER_AB_DEFAULT) return c.ab_mode;
   return is_medusa(c) ? CLOVER_AB_NONE : CLOVER_AB_FULL;
@@ -109,6 +110,7 @@ std::vector<WSpec> weight_specs(const clover_config& c) {
   for (int j = 0; j < c.n_spec_heads; ++j) {
     s.push_back({"head" + std::to_string(j) + ".w1", d, d, true});
     s.push_back({"head" + std::to_string(j) + ".b1", d, 0, false});
+    if (per_head_lm(c)) s.push_back({"head" + std::to_string(j) + ".lm", V, d, true});
   }
   return s;
 }
@@ -148,6 +150,9 @@ bool check_config(const clover_config* c, std::string& why) {
   if (c->ad_per_head != 0 && c->ad_per_head != 1) return fail("ad_per_head must be 0 or 1");
   if (c->regressive != CLOVER_REGRESSIVE_ATTENTION && c->regressive != CLOVER_REGRESSIVE_MLP)
     return fail("regressive must be CLOVER_REGRESSIVE_ATTENTION or CLOVER_REGRESSIVE_MLP");
+  if (c->medusa_lm_heads != 0 && c->medusa_lm_heads != 1) return fail("medusa_lm_heads must be 0 or 1");
+  if (c->medusa_lm_heads == 1 && c->draft_mode != CLOVER_DRAFT_MEDUSA)
+    return fail("per-head LM heads belong to the Medusa draft (the Clover heads share the LM head)");
   if (c->regressive == CLOVER_REGRESSIVE_MLP && (c->ad_keys != CLOVER_AD_KEYS_SINGLE || c->ad_per_head))
     return fail("the MLP regressive block takes no Attention Decoder key set or per-head decoders");
   if (!(c->temperature >= 0.f) || c->temperature > 1e30f) return fail("temperature must be finite and >= 0");
@@ -339,6 +344,7 @@ struct clover_ctx {
   std::vector<AdPtrs> ad;  // one Attention Decoder shared by the heads, or one per head
   const void *rb_norm = nullptr, *rb_w = nullptr, *rb_b = nullptr;  // MLP regressive block
   std::vector<const void*> head_w1, head_b1;
+  std::vector<const void*> head_lm;  // Medusa heads' own LM heads (medusa_lm_heads)
   // host state
   std::vector<int> seq_len;                  // -1 inactive
   std::vector<std::vector<int>> seq_blocks;  // physical KV blocks per slot
@@ -812,10 +818,20 @@ hipError_t enq_draft_medusa(clover_ctx* c, int B) {
     rh.out_norm = rn + (size_t)(j - 1) * B * d * L.es; rh.ldn = d;
     HE(run_rowfix(c, rh));
   }
-  GemmParams lm{};
-  lm.X = rn; lm.ldx = d; lm.mode = EP_PARTIAL; lm.max_splits = 1;
-  lm.part = c->at<float>(L.dlogits[0]);
-  HE(run_gemm(c, lm, H * B, d, {{c->lm_head, cf.vocab}}));
+  if (per_head_lm(cf)) {
+    // the original Medusa's heads each carry an LM head (Sec. 3.4): one pass per head
+    for (int j = 0; j < H; ++j) {
+      GemmParams lm{};
+      lm.X = rn + (size_t)j * B * d * L.es; lm.ldx = d; lm.mode = EP_PARTIAL; lm.max_splits = 1;
+      lm.part = c->at<float>(L.dlogits[0]) + (size_t)j * B * cf.vocab;
+      HE(run_gemm(c, lm, B, d, {{c->head_lm[j], cf.vocab}}));
+    }
+  } else {
+    GemmParams lm{};
+    lm.X = rn; lm.ldx = d; lm.mode = EP_PARTIAL; lm.max_splits = 1;
+    lm.part = c->at<float>(L.dlogits[0]);
+    HE(run_gemm(c, lm, H * B, d, {{c->lm_head, cf.vocab}}));
+  }
   int kmax = 1;
   for (int j = 0; j < H; ++j) kmax = std::max(kmax, cf.topk[j]);
   TopkParams tp{};  // the top-k_j of head j are the first k_j of its top-kmax
@@ -1150,6 +1166,7 @@ clover_status clover_init(const clover_config* cfg, void* const* weights, void* 
   for (int j = 0; j < cfg->n_spec_heads; ++j) {
     c->head_w1.push_back(c->w[k++]);
     c->head_b1.push_back(c->w[k++]);
+    if (per_head_lm(*cfg)) c->head_lm.push_back(c->w[k++]);
   }
   c->profile = (cfg->flags & CLOVER_FLAG_PROFILE) != 0;
   c->use_graphs = !c->profile && !(cfg->flags & CLOVER_FLAG_EAGER);

@@ -40,6 +40,9 @@ class CloverConfig:
     # regressive block of the Clover draft: the "attention" decoder (Eq. 1-2) or the "mlp"
     # over [RMSNorm(h); e] of the ablation (Sec. 3.2 last paragraph, Sec. 4.3)
     regressive: str = "attention"
+    # Medusa draft: the heads "shared" the target's LM head, or each has its own ("per_head",
+    # the original Medusa, Sec. 3.4)
+    medusa_lm: str = "shared"
     temperature: float = 0.0   # 0: greedy; > 0: the target samples (speculative sampling)
     sample_seed: int = 0
 

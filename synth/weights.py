@@ -42,6 +42,8 @@ def weight_specs(c: CloverConfig) -> List[Tuple[str, Tuple[int, ...]]]:
                       (f"{pre}.wv", (qd, d)), (f"{pre}.wo", (d, qd))]
     for j in range(c.n_spec_heads):
         specs += [(f"head{j}.w1", (d, d)), (f"head{j}.b1", (d,))]
+        if c.draft == "medusa" and c.medusa_lm == "per_head":
+            specs += [(f"head{j}.lm", (V, d))]
     return specs
 
 

@@ -34,7 +34,8 @@ def test_every_declared_symbol_is_exported():
 
 VARIANTS = [(n, {}) for n in synth.CONFIGS] + [
     ("tiny_fp32", {"regressive": "mlp"}), ("llama7b_b1", {"regressive": "mlp", "ab": "none"}),
-    ("tiny_fp32", {"ad_per_head": True}), ("large_gqa_b1", {"ab": "attn"})]
+    ("tiny_fp32", {"ad_per_head": True}), ("large_gqa_b1", {"ab": "attn"}),
+    ("llama7b_b1_medusa", {"medusa_lm": "per_head"}), ("tiny_fp32_medusa", {"medusa_lm": "per_head", "ab": "full"})]
 
 
 @pytest.mark.parametrize("name,kw", VARIANTS)

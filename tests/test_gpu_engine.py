@@ -605,6 +605,34 @@ def test_speculator_variants_match_oracle(draft, ab, ad_keys, per_head, regressi
     assert out == o.base.greedy_generate(prompt, len(out))
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_medusa_per_head_lm_heads_match_oracle(dtype):
+    """The original Medusa's per-head LM heads (Sec. 3.4): one LM-head pass per head, each
+    with its own weights.  Head logits and verify logits within the dtype's tolerance over
+    four steps, trees exact, tokens equal to the oracle's (fp32) and to greedy decoding."""
+    P = need_gpu()
+    note(f"engine Medusa per-head LM heads {dtype}")
+    cfg = (synth.get_config("tiny_fp32") if dtype == "f32" else _bf16_small()).with_(
+        draft="medusa", medusa_lm="per_head", batch=2)
+    w = synth.make_weights(cfg, seed=13, perturb=True)
+    eng = _engine(P, cfg, w)
+    o = oracle.make_oracle(cfg, w)
+    tol = 1e-4 if dtype == "f32" else 2e-2
+    states = []
+    for s in range(2):
+        prompt = synth.make_prompt(cfg, seq=s, n=90 + 20 * s)
+        assert eng.prefill(s, prompt) == (st := o.prefill(prompt)).t0
+        states.append(st)
+    stats = dict(steps=0, draft_rows=0, verify_rows=0, draft_ties=0, target_ties=0)
+    for _ in range(4):
+        teacher_forced_step(eng, o, states, tol, stats)
+    note(f"Medusa per-head LM heads {dtype}: {stats}")
+    assert stats["steps"] == 8 and stats["draft_rows"] == 8 * cfg.n_spec_heads
+    if dtype == "f32":
+        assert stats["target_ties"] == 0
+    eng.close()
+
+
 @pytest.mark.parametrize("which", ["tiny_fp32", "small_bf16_t128"])
 def test_sampled_targets_match_oracle_sampler(which):
     """Speculative sampling (temperature 0.8): every tree node's target is a Gumbel-max draw

@@ -145,3 +145,50 @@ def test_medusa_heads_on_the_augmenting_block_are_clover_without_ad_and_rc():
     wm = {n: wc[n] for n, _ in synth.weight_specs(cfg_m)}
     prompt = synth.make_prompt(cfg_m, n=11)
     _same(_decode(MedusaOracle(cfg_m, wm), prompt), _decode(CloverOracle(cfg_c, wc), prompt))
+
+
+def _per_head_cfg(**kw):
+    return synth.tiny_test_config(draft="medusa", medusa_lm="per_head", topk=(3, 2, 2), tree_tokens=12, **kw)
+
+
+def test_per_head_lm_heads_equal_to_the_target_give_the_shared_draft():
+    """Sec. 3.4: the original Medusa gives every head its own LM head, Clover shares the
+    target's.  With each head's LM head set to the target's the two readings draft the same
+    candidates, log-probabilities and logits."""
+    cfg = _per_head_cfg()
+    w = synth.make_weights(cfg, seed=5, perturb=True)
+    for j in range(cfg.n_spec_heads):
+        w[f"head{j}.lm"] = w["lm_head"].clone()
+    shared = cfg.with_(medusa_lm="shared")
+    ws = {k: v for k, v in w.items() if not k.endswith(".lm")}
+    a, b = oracle.MedusaOracle(cfg, w), oracle.MedusaOracle(shared, ws)
+    prompt = synth.make_prompt(cfg, n=11)
+    ca, cb = a.draft(a.prefill(prompt)), b.draft(b.prefill(prompt))
+    assert np.array_equal(ca.token, cb.token) and np.array_equal(ca.lp, cb.lp)
+    for la, lb in zip(ca.head_logits, cb.head_logits):
+        assert np.array_equal(la, lb)
+
+
+def test_each_head_reads_its_own_lm_head():
+    """Head j's LM head scaled by c_j scales head j's logits by c_j exactly (every head
+    reads the state and the final norm the same way), and no other head's."""
+    cfg = _per_head_cfg()
+    w = synth.make_weights(cfg, seed=6, perturb=True)
+    scales = (1.0, 2.0, 4.0)
+    for j in range(cfg.n_spec_heads):
+        w[f"head{j}.lm"] = w["lm_head"] * scales[j]
+    o = oracle.MedusaOracle(cfg, w)
+    c = o.draft(o.prefill(synth.make_prompt(cfg, n=11)))
+    base = oracle.MedusaOracle(cfg.with_(medusa_lm="shared"), {k: v for k, v in w.items() if not k.endswith(".lm")})
+    cb = base.draft(base.prefill(synth.make_prompt(cfg, n=11)))
+    for j in range(cfg.n_spec_heads):
+        assert np.array_equal(c.head_logits[j], scales[j] * cb.head_logits[j]), j
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_per_head_lm_heads_speculative_equals_greedy(seed):
+    cfg = _per_head_cfg()
+    o = oracle.MedusaOracle(cfg, synth.make_weights(cfg, seed=seed, perturb=True))
+    prompt = synth.make_prompt(cfg, seq=seed, n=12)
+    spec, _ = o.generate(prompt, 14)
+    assert spec == o.base.greedy_generate(prompt, 14)
