@@ -14,8 +14,12 @@
 // output, running max, running sum) that a small merge kernel combines in split order;
 // with one split the output is written directly.
 //
-// Inside a workgroup, waves w and w + 4 take one query tile and the even / odd key
-// blocks of each chunk, merging their states through LDS at the end.  The score
+// Inside a workgroup of four query tiles, waves w and w + 4 take one query tile and the
+// even / odd key blocks of each chunk, merging their states through LDS at the end.  When an
+// item has eight or more query tiles (trees above 64 tokens, grouped KV heads, prefill
+// chunks) a workgroup takes eight tiles, one per wave over every key block, so each K/V
+// chunk staged in LDS feeds twice as many queries and the item's keys are read by half as
+// many workgroups.  The score
 // product is computed transposed (S^T = K Q^T) so the matrix-core accumulator already
 // holds, per lane, four consecutive keys of one query row: exactly the operand layout
 // the P*V product needs.  Softmax is online in the log2 domain.  The next chunk's K/V
@@ -29,9 +33,8 @@
 
 namespace clover {
 
-static constexpr int AT_WAVES = 8;               // 4 query tiles x 2 key halves
+static constexpr int AT_WAVES = 8;               // 4 query tiles x 2 key halves, or 8 x 1
 static constexpr int AT_THREADS = AT_WAVES * 64;
-static constexpr int AT_QT = 4;                  // query tiles per workgroup
 static constexpr int AT_MAX_BLOCKS = 4096;       // 65536 keys
 static constexpr int AT_MAX_SPLITS = 16;
 static constexpr int AT_TARGET_WGS = 256;        // one workgroup per CU
@@ -93,8 +96,11 @@ __device__ __forceinline__ size_t part_rec(const AttnParams& p, int item, int sp
   return ((((size_t)item * p.splits + split) * p.qt_item + qi) * 16 + j) * (size_t)(hd + 2);
 }
 
-template <typename S, int HD>
+// QT: query tiles per workgroup (4: two waves per tile over the even / odd key blocks; 8:
+// one wave per tile over all of them)
+template <typename S, int HD, int QT>
 __global__ __launch_bounds__(AT_THREADS) void attn_kernel(const AttnParams p) {
+  constexpr int HALVES = AT_WAVES / QT;  // waves per query tile, each over every HALVES-th block
   using T = St<S>;
   using SH = AttnShape<S, HD>;
   constexpr int EPL = T::EPL, KC = 4 * EPL, NQC = HD / KC, NT = HD / 16;
@@ -104,7 +110,7 @@ __global__ __launch_bounds__(AT_THREADS) void attn_kernel(const AttnParams p) {
   __shared__ int s_bt[AT_MAX_BLOCKS];
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, j = lane & 15;
-  const int half = wave >> 2;  // key-block parity this wave takes
+  const int half = wave / QT;  // key-block parity this wave takes (HALVES = 2)
   // workgroup -> (item, query group, split); all splits and query groups of an item on
   // one XCD (workgroup ids are dealt to the 8 XCDs round-robin)
   const int per_item = p.qgroups * p.splits;
@@ -118,7 +124,7 @@ __global__ __launch_bounds__(AT_THREADS) void attn_kernel(const AttnParams p) {
   const int P = p.prefix_dev ? p.prefix_dev[slot] : p.prefix_host;
 
   // this wave's query tile
-  const int qi = qg * AT_QT + (wave & 3);
+  const int qi = qg * QT + (wave % QT);
   const bool has_q = qi < p.qt_item;
   const int h = kvh * G + (has_q ? qi / p.qph : 0), qt = has_q ? qi % p.qph : 0;
   const int row = qt * 16 + j;
@@ -127,8 +133,8 @@ __global__ __launch_bounds__(AT_THREADS) void attn_kernel(const AttnParams p) {
   int tail = p.n_tail;
   if (p.causal) {
     int qmax = 0;
-    for (int w = 0; w < AT_QT; ++w) {
-      const int q2 = qg * AT_QT + w;
+    for (int w = 0; w < QT; ++w) {
+      const int q2 = qg * QT + w;
       if (q2 < p.qt_item) qmax = max(qmax, q2 % p.qph);
     }
     tail = min(p.n_tail, qmax * 16 + 16);
@@ -188,12 +194,12 @@ __global__ __launch_bounds__(AT_THREADS) void attn_kernel(const AttnParams p) {
   for (int t = 0; t < NT; ++t) o[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   // One online-softmax update over up to NG of this wave's blocks of the chunk (LDS
-  // blocks cb0, cb0 + 2, ...; key blocks kb0g, kb0g + 2, ...): the cross-lane max and
+  // blocks cb0, cb0 + HALVES, ...; key blocks kb0g, kb0g + HALVES, ...): the cross-lane max and
   // sum reductions and the rescale of the output are paid once per NG blocks.  The
   // running max m_i is kept in raw score units; the scale folds into one multiply-add
   // per exponent.  Groups wholly inside the committed prefix skip the mask logic.
   constexpr int NG = 4;
-  static_assert(CB - 1 + 2 * (NG - 1) < 2 * CB, "score reads of a group stay inside the chunk buffer");
+  static_assert(CB - 1 + HALVES * (NG - 1) < 2 * CB, "score reads of a group stay inside the chunk buffer");
   using VT = typename VFrag<S>::type;
   // tail rule as data, so the score loop has no branch on the mode: causal rows see tail
   // keys up to their own index, tree rows the keys whose mask bit is set
@@ -205,20 +211,20 @@ __global__ __launch_bounds__(AT_THREADS) void attn_kernel(const AttnParams p) {
     f32x4_t s[NG];
 #pragma unroll
     for (int i = 0; i < NG; ++i) {
-      const u32x4_t* kblk = lds + (cb0 + 2 * i) * BVEC;
+      const u32x4_t* kblk = lds + (cb0 + HALVES * i) * BVEC;
       f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int c = 0; c < NQC; ++c) acc = mma_frag(kblk[c * 64 + lane], qf[c], acc, S{});
       s[i] = acc;
     }
-    // s[i][r] = score of key (kb0g + 2i)*16 + 4g + r for query row j
-    const bool plain = nblk == NG && (kb0g + 2 * (NG - 1)) * 16 + 15 < P;  // all keys committed
+    // s[i][r] = score of key (kb0g + HALVES*i)*16 + 4g + r for query row j
+    const bool plain = nblk == NG && (kb0g + HALVES * (NG - 1)) * 16 + 15 < P;  // all keys committed
     if (!plain) {
 #pragma unroll
       for (int i = 0; i < NG; ++i)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int key = (kb0g + 2 * i) * 16 + 4 * g + r;
+          const int key = (kb0g + HALVES * i) * 16 + 4 * g + r;
           const int tk = key - P;
           const uint64_t word = tk < 64 ? mw0 : mw1;
           const bool tree_ok = causal_mode | (((word >> (tk & 63)) & 1ull) != 0);
@@ -256,7 +262,7 @@ __global__ __launch_bounds__(AT_THREADS) void attn_kernel(const AttnParams p) {
 #pragma unroll
     for (int i = 0; i < NG; ++i) {
       if (i < nblk) {
-        const VT* vblk = reinterpret_cast<const VT*>(lds + (CB + cb0 + 2 * i) * BVEC);
+        const VT* vblk = reinterpret_cast<const VT*>(lds + (CB + cb0 + HALVES * i) * BVEC);
 #pragma unroll
         for (int t = 0; t < NT; ++t) o[t] = mma_pv(vblk[t * 64 + lane], pb[i], pr[i], o[t], S{});
       }
@@ -272,8 +278,8 @@ __global__ __launch_bounds__(AT_THREADS) void attn_kernel(const AttnParams p) {
       if (more) load_chunk(ch + 1);  // in flight while this chunk is computed
       if (has_q) {
         const int nbc = min(CB, nb - ch * CB);
-        for (int cb0 = half; cb0 < nbc; cb0 += 2 * NG)
-          consume(cb0, kb0 + ch * CB + cb0, min(NG, (nbc - cb0 + 1) / 2));
+        for (int cb0 = half; cb0 < nbc; cb0 += HALVES * NG)
+          consume(cb0, kb0 + ch * CB + cb0, min(NG, (nbc - cb0 + HALVES - 1) / HALVES));
       }
       __syncthreads();
       if (more) {
@@ -286,9 +292,9 @@ __global__ __launch_bounds__(AT_THREADS) void attn_kernel(const AttnParams p) {
   // from here on the running max is in log2-scaled units, as the merges expect
   m_i = (m_i == -INFINITY) ? -INFINITY : m_i * scale2;
   // merge the two key halves of each query tile through LDS (the chunk buffer is free)
-  float* mo = reinterpret_cast<float*>(smem);  // [AT_QT][16][HD + 2]
-  float* rec = mo + (size_t)((wave & 3) * 16 + j) * (HD + 2);
-  if (half == 1) {
+  float* mo = reinterpret_cast<float*>(smem);  // [QT][16][HD + 2]
+  float* rec = mo + (size_t)((wave % QT) * 16 + j) * (HD + 2);
+  if (HALVES == 2 && half == 1) {
 #pragma unroll
     for (int t = 0; t < NT; ++t)
 #pragma unroll
@@ -298,9 +304,9 @@ __global__ __launch_bounds__(AT_THREADS) void attn_kernel(const AttnParams p) {
       rec[HD + 1] = l_i;
     }
   }
-  __syncthreads();
+  if (HALVES == 2) __syncthreads();
   if (half == 1 || !has_q) return;
-  {
+  if (HALVES == 2) {
     const float m1 = rec[HD], l1 = rec[HD + 1];
     const float M = fmaxf(m_i, m1);
     const float a0 = (m_i == -INFINITY) ? 0.f : exp2f(m_i - M);
@@ -380,7 +386,8 @@ void plan_attention(AttnParams& p) {
   const int G = std::max(1, p.n_heads / std::max(1, p.n_kv));
   p.qph = (p.nq + 15) / 16;
   p.qt_item = G * p.qph;
-  p.qgroups = (p.qt_item + AT_QT - 1) / AT_QT;
+  p.qtile = p.qt_item >= 8 ? 8 : 4;  // eight tiles a workgroup whenever an item has that many
+  p.qgroups = (p.qt_item + p.qtile - 1) / p.qtile;
   const int base = std::max(1, p.nbatch * p.n_kv * p.qgroups);
   p.splits = std::max(1, std::min(AT_MAX_SPLITS, AT_TARGET_WGS / base));
 }
@@ -400,17 +407,22 @@ static hipError_t launch_attn_hd(AttnParams& p, hipStream_t st, const LaunchTimi
   const size_t lds = AttnShape<S, HD>::LDS;
   static bool lds_attr = false;  // dynamic LDS above 64 KB is opted into once per kernel
   if (!lds_attr) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<S, HD>),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
+    for (const void* k : {reinterpret_cast<const void*>(&attn_kernel<S, HD, 4>),
+                          reinterpret_cast<const void*>(&attn_kernel<S, HD, 8>)}) {
+      const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+    }
     lds_attr = true;
   }
-  static_assert((size_t)AT_QT * 16 * (HD + 2) * 4 <= AttnShape<S, HD>::LDS, "merge records fit the chunk buffer");
+  static_assert((size_t)4 * 16 * (HD + 2) * 4 <= AttnShape<S, HD>::LDS, "merge records fit the chunk buffer");
   // the merge kernel, if any, closes the timed interval
   const bool merge = p.splits > 1;
-  if (lt) hipExtLaunchKernelGGL((attn_kernel<S, HD>), grid, block, (uint32_t)lds, st, lt->start,
-                                merge ? nullptr : lt->stop, 0, p);
-  else hipLaunchKernelGGL((attn_kernel<S, HD>), grid, block, lds, st, p);
+  auto go = [&](auto kern) {
+    if (lt) hipExtLaunchKernelGGL(kern, grid, block, (uint32_t)lds, st, lt->start, merge ? nullptr : lt->stop, 0, p);
+    else hipLaunchKernelGGL(kern, grid, block, lds, st, p);
+  };
+  if (p.qtile == 8) go(attn_kernel<S, HD, 8>);
+  else go(attn_kernel<S, HD, 4>);
   if (merge) {
     dim3 mgrid(8 * per_xcd * p.qt_item);
     if (lt) hipExtLaunchKernelGGL((attn_merge_kernel<S, HD>), mgrid, dim3(256), 0, st, nullptr, lt->stop, 0, p);

@@ -109,9 +109,9 @@ struct AttnParams {
   int n_heads, n_kv, hd;
   int nbatch;
   float* part; size_t part_cap;    // fp32 split partials (attention_part_floats), or null
-  // filled by plan_attention: query tiles per head, per (sequence, KV head), workgroups
-  // per (sequence, KV head) in the query direction, key splits
-  int qph, qt_item, qgroups, splits;
+  // filled by plan_attention: query tiles per head, per (sequence, KV head), per
+  // workgroup (4 or 8), workgroups per (sequence, KV head) in the query direction, key splits
+  int qph, qt_item, qtile, qgroups, splits;
 };
 // Plans the launch (fields above) and runs it: the attention kernel and, with more than
 // one key split, the merge kernel.  max_keys bounds prefix + tail over the batch.
