@@ -362,6 +362,8 @@ def main():
                          "MLP over [RMSNorm(h); e] of the components ablation (Sec. 4.3)")
     ap.add_argument("--medusa-lm", default="", choices=["", "shared", "per_head"],
                     help="Medusa draft: heads share the target's LM head, or each has its own (Sec. 3.4)")
+    ap.add_argument("--ab-commit", action="store_true",
+                    help="run the Augmenting Block at commit over the accepted rows at every batch size")
     ap.add_argument("--temperature", type=float, default=-1.0,
                     help="override the sampling temperature (0: greedy; > 0: speculative sampling)")
     ap.add_argument("--surface", action="store_true",
@@ -416,7 +418,8 @@ def main():
     max_context = max(lens) + (args.warmup + args.steps + kt_steps) * H1 + cfg.tree_tokens + 16
     print(f"[bench] workload {cfg.name}: generating weights on device", file=sys.stderr, flush=True)
     w = synth.make_weights(cfg, seed=args.seed, device="cuda")
-    eng = P.CloverEngine(cfg, w, max_batch=cfg.batch, max_context=max_context, free_source=True)
+    base_flags = P.FLAG_AB_COMMIT if args.ab_commit else 0
+    eng = P.CloverEngine(cfg, w, max_batch=cfg.batch, max_context=max_context, free_source=True, flags=base_flags)
     del w
     torch.cuda.empty_cache()
     seqs = list(range(cfg.batch))
@@ -452,11 +455,11 @@ def main():
     # second pass over the same workload with every launch timed by HIP events on the
     # context's stream (eager launches; the graph replay above cannot carry them)
     if kt_steps:
-        eng.set_flags(P.FLAG_PROFILE)
+        eng.set_flags(P.FLAG_PROFILE | base_flags)
         eng.reset_kernel_stats()
         for _ in range(kt_steps):
             eng.step(seqs)
-        eng.set_flags(0)
+        eng.set_flags(base_flags)
     ks = eng.kernel_stats()
     g = ks["gemm_verify"]
     achieved = g["bytes"] / (g["total_ms"] * 1e-3) / 1e9 if g["total_ms"] > 0 else 0.0
@@ -485,7 +488,7 @@ def main():
         "vs_baseline": None,
         "dtype": cfg.dtype,
         "data": "synthetic: random-init N(0,0.02) weights, uniform-random prompt tokens",
-        "config": {"workload": cfg.name, "speculator": cfg.draft, "augmenting_block": cfg.ab_kind,
+        "config": {"workload": cfg.name, "speculator": cfg.draft, "augmenting_block": cfg.ab_kind, "ab_at_commit": bool(args.ab_commit),
                    "decoder_keys": cfg.ad_keys, "regressive_block": cfg.regressive,
                    "medusa_lm_heads": cfg.medusa_lm,
                    "temperature": cfg.temperature,
