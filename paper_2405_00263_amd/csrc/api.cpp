@@ -187,7 +187,7 @@ struct Layout {
   int es, T, W, H, NC, Mv, Mp, Mmax, Fsum, Fmaxrows, mbps, nblocks;
   size_t pool_bytes;
   size_t kpool, vpool, pool_ptrs, block_table, seq_len, seq_ids;
-  size_t x, xa, xn, qbuf, obuf, act, vlogits, row_tok, row_pos, row_slot, row_seq, amax;
+  size_t x, xa, xab, xn, qbuf, obuf, act, vlogits, row_tok, row_pos, row_slot, row_seq, row_kb, amax;
   size_t sample_step;  // per slot: speculate-and-verify steps done since its prefill (sampling counters)
   size_t rope_cs;  // [Mmax][hd/2] (cos, sin) of the current rows' positions
   size_t h0, t0, cand_token, cand_parent, cand_depth, cand_lp;
@@ -236,6 +236,7 @@ Layout make_layout(const clover_config& c) {
   L.sample_step = take(sizeof(int) * c.max_batch);  // zeroed at init with the state
   L.x = take(4 * (size_t)L.Mmax * d);
   L.xa = take(4 * (size_t)L.Mmax * d);
+  L.xab = take(4 * (size_t)c.max_batch * (L.H + 1) * d);  // commit-time Augmenting Block rows
   L.xn = take((size_t)L.es * L.Mmax * d);
   L.qbuf = take((size_t)L.es * L.Mmax * qd);
   L.obuf = take((size_t)L.es * L.Mmax * qd);
@@ -245,6 +246,7 @@ Layout make_layout(const clover_config& c) {
   L.row_pos = take(4 * (size_t)L.Mmax);
   L.row_slot = take(4 * (size_t)L.Mmax);
   L.row_seq = take(4 * (size_t)L.Mmax);
+  L.row_kb = take(4 * (size_t)L.Mmax);
   L.rope_cs = take(4 * (size_t)L.Mmax * c.head_dim);
   L.amax = take(4 * (size_t)L.Mv);
   L.h0 = take(4 * (size_t)c.max_batch * d);
@@ -467,6 +469,15 @@ hipError_t run_gemm(clover_ctx* c, GemmParams p, int M, int K,
   return e;
 }
 
+// Per-row tables of a forward over M rows (rotary factors, KV append slots) from row_pos,
+// row_seq, row_slot and the block table, once before its layers.
+hipError_t row_tables(clover_ctx* c, int M) {
+  const Layout& L = c->L;
+  return launch_rope_table(c->at<int>(L.row_pos), M, c->cfg.head_dim, c->cfg.rope_theta, c->at<float>(L.rope_cs),
+                           c->st, c->at<int>(L.row_seq), c->at<int>(L.row_slot), c->at<int>(L.block_table), L.mbps,
+                           c->at<int>(L.row_kb));
+}
+
 // Residual-stream trace: copy the M rows of x into trace slot `idx` (clover_debug_trace).
 hipError_t trace_rows(clover_ctx* c, int idx, const float* x, int M) {
   if (!c->trace) return hipSuccess;
@@ -497,8 +508,7 @@ hipError_t run_attention_half(clover_ctx* c, const LayerPtrs& lw, int layer_idx,
   g.X = xn; g.ldx = d; g.mode = EP_QKV;
   g.qbuf = c->at<void>(L.qbuf); g.ldq = qd;
   g.kcache = kp; g.vcache = vp;
-  g.row_seq = c->at<int>(L.row_seq); g.row_slot = c->at<int>(L.row_slot);
-  g.block_table = c->at<int>(L.block_table); g.max_blocks = L.mbps;
+  g.row_kb = c->at<int>(L.row_kb);
   g.n_heads = cf.n_heads; g.n_kv = cf.n_kv_heads; g.hd = hd; g.rope_cs = c->at<float>(L.rope_cs);
   const int qkv_tiles = (qd + 2 * kvd) / 16, kc = kc_of(cf.dtype);
   if (plan_gemm(cf.dtype, M, qkv_tiles, d / kc, false, QKV_MAX_SPLITS).S > 1) {
@@ -632,7 +642,7 @@ hipError_t enq_verify(clover_ctx* c, int B, int max_keys) {
   float* x = c->at<float>(L.x);
   float* xa = c->at<float>(L.xa);
   HE(launch_embed(cf.dtype, c->emb, c->at<int>(L.row_tok), M, d, x, c->st));
-  HE(launch_rope_table(c->at<int>(L.row_pos), M, cf.head_dim, cf.rope_theta, c->at<float>(L.rope_cs), c->st));
+  HE(row_tables(c, M));
   AttnParams att{};
   att.seq_ids = c->at<int>(L.seq_ids);
   att.prefix_dev = c->at<int>(L.seq_len);
@@ -706,11 +716,11 @@ hipError_t enq_accept(clover_ctx* c, int B, int max_keys) {
   if (!commit) return hipSuccess;
   // the Augmenting Block over each sequence's accepted rows (x_N), causal against its cache
   const int Mab = B * (H + 1);
-  float* xr = c->at<float>(L.x);
+  float* xr = c->at<float>(L.xab);  // x keeps the verify's last rows
   HE(launch_ab_commit_rows(c->at<int>(L.seq_ids), B, T, H, c->at<int>(L.acc), c->at<int>(L.acc_len),
                            c->at<int>(L.seq_len), c->at<float>(L.xa), d, xr, c->at<int>(L.row_pos),
                            c->at<int>(L.row_slot), c->at<int>(L.row_seq), c->st));
-  HE(launch_rope_table(c->at<int>(L.row_pos), Mab, cf.head_dim, cf.rope_theta, c->at<float>(L.rope_cs), c->st));
+  HE(row_tables(c, Mab));
   AttnParams att{};
   att.seq_ids = c->at<int>(L.seq_ids);
   att.prefix_dev = c->at<int>(L.seq_len);
@@ -1273,7 +1283,7 @@ clover_status clover_prefill(clover_ctx* c, int32_t seq, const int32_t* tokens, 
     HIPCK(c, hipMemcpyAsync(c->at<int>(L.row_slot), meta.data() + 2 * C, sizeof(int) * rows, hipMemcpyHostToDevice, c->st));
     HIPCK(c, hipMemcpyAsync(c->at<int>(L.row_seq), meta.data() + 3 * C, sizeof(int) * rows, hipMemcpyHostToDevice, c->st));
     HIPCK(c, launch_embed(cf.dtype, c->emb, c->at<int>(L.row_tok), rows, d, x, c->st));
-    HIPCK(c, launch_rope_table(c->at<int>(L.row_pos), rows, cf.head_dim, cf.rope_theta, c->at<float>(L.rope_cs), c->st));
+    HIPCK(c, row_tables(c, rows));
     AttnParams att{};
     att.seq_ids = c->at<int>(L.seq_ids);
     att.prefix_dev = nullptr; att.prefix_host = c0;

@@ -126,11 +126,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(const GemmParams p) {
   // KV-append targets of the fused epilogue, loaded once up front so the epilogue's row
   // loop has no dependent global loads
   __shared__ int s_kvbase[MROWS];
-  if (p.mode == EP_QKV && threadIdx.x < MROWS) {
-    const int m = min(m0 + (int)threadIdx.x, p.M - 1);
-    const int slot = p.row_slot[m];
-    s_kvbase[threadIdx.x] = p.block_table[(size_t)p.row_seq[m] * p.max_blocks + (slot >> 4)] * 16 + (slot & 15);
-  }
+  if (p.mode == EP_QKV && threadIdx.x < MROWS) s_kvbase[threadIdx.x] = p.row_kb[min(m0 + (int)threadIdx.x, p.M - 1)];
 
   bool active;
   const u32x4_t* wp = wave_weight_ptr<NW>(p, g, wave, active);
@@ -447,27 +443,90 @@ hipError_t launch_gemm(int dtype, GemmParams& p, hipStream_t st, const LaunchTim
   return dtype == 1 ? launch_gemm_t<bf16_t>(p, pl, st, lt) : launch_gemm_t<float>(p, pl, st, lt);
 }
 
+// eight consecutive storage elements from float values
+__device__ __forceinline__ void store8(bf16_t* dst, const float (&x)[8]) {
+  u32x4_t v;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = (uint32_t)f2bf(x[2 * i]) | ((uint32_t)f2bf(x[2 * i + 1]) << 16);
+  *reinterpret_cast<u32x4_t*>(dst) = v;
+}
+__device__ __forceinline__ void store8(float* dst, const float (&x)[8]) {
+  *reinterpret_cast<float4*>(dst) = make_float4(x[0], x[1], x[2], x[3]);
+  *reinterpret_cast<float4*>(dst + 4) = make_float4(x[4], x[5], x[6], x[7]);
+}
+
 // Q|K|V finished from K-split partials part[s][m][pc] (packed column order), summed in split
-// order, then rotary and stores as in the fused epilogue.  One thread per (row, column).
+// order, then rotary and stores with the same arithmetic as the fused epilogue (qkv_store).
+// One thread per (row, 8-column half of a 16-column tile): the half's partner half is the
+// other half of the same tile, its 8 values are 8 consecutive dims of one head, so Q and K
+// go out as one 16-byte store each (K in the cache's fragment order keeps 8 dims of a key
+// together); V scatters to the cache's key-minor layout.
 template <typename S>
 __global__ __launch_bounds__(256) void qkv_fix_kernel(const GemmParams p, const float* __restrict__ part, int S_, int N) {
-  const int pc = blockIdx.x * 256 + threadIdx.x, m = blockIdx.y;
-  if (pc >= N) return;
-  const int slot = p.row_slot[m];
-  const int kb = p.block_table[(size_t)p.row_seq[m] * p.max_blocks + (slot >> 4)] * 16 + (slot & 15);
-  float v = 0.f, w = 0.f;
+  const int N8 = N >> 3, id = blockIdx.x * 256 + threadIdx.x;
+  const int m = id / N8, pc0 = (id % N8) * 8;
+  if (m >= p.M) return;
+  const int hd = p.hd, half = hd >> 1, qd = p.n_heads * hd, kvd = p.n_kv * hd;
+  const int pt = pc0 >> 4, jj0 = pc0 & 15, qt = qd / 16, kt = kvd / 16;
+  const bool rot = pt < qt + kt;
+  float v[8], w[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = w[e] = 0.f;
   for (int s = 0; s < S_; ++s) {
     const float* r = part + ((size_t)s * p.M + m) * N;
-    v += r[pc];
-    w += r[pc ^ 8];
+    const float4 a0 = *reinterpret_cast<const float4*>(r + pc0), a1 = *reinterpret_cast<const float4*>(r + pc0 + 4);
+    v[0] += a0.x; v[1] += a0.y; v[2] += a0.z; v[3] += a0.w;
+    v[4] += a1.x; v[5] += a1.y; v[6] += a1.z; v[7] += a1.w;
+    if (rot) {
+      const float4 b0 = *reinterpret_cast<const float4*>(r + (pc0 ^ 8));
+      const float4 b1 = *reinterpret_cast<const float4*>(r + (pc0 ^ 8) + 4);
+      w[0] += b0.x; w[1] += b0.y; w[2] += b0.z; w[3] += b0.w;
+      w[4] += b1.x; w[5] += b1.y; w[6] += b1.z; w[7] += b1.w;
+    }
   }
-  qkv_store<S>(p, m, pc, v, w, kb);
+  int n0;  // logical column of the first of the 8
+  if (rot) {
+    const int seg0 = pt < qt ? 0 : qt;
+    n0 = seg0 * 16 + rope_row(pt - seg0, jj0, hd);
+    const int d0 = n0 % hd, dlo0 = d0 < half ? d0 : d0 - half;
+    const float2* cs = reinterpret_cast<const float2*>(p.rope_cs) + (size_t)m * half + dlo0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float2 c = cs[e];
+      v[e] = (jj0 < 8) ? (v[e] * c.x - w[e] * c.y) : (v[e] * c.x + w[e] * c.y);
+    }
+  } else {
+    n0 = pc0;
+  }
+  if (n0 < qd) {
+    store8(reinterpret_cast<S*>(p.qbuf) + (size_t)m * p.ldq + n0, v);
+    return;
+  }
+  using T = St<S>;
+  const int kb = p.row_kb[m], key = kb & 15;
+  const bool isk = n0 < qd + kvd;
+  const int kvh = (isk ? n0 - qd : n0 - qd - kvd) / hd, d0 = n0 % hd;
+  const size_t base = ((size_t)(kb >> 4) * p.n_kv + kvh) * (size_t)(16 * hd);
+  S* kc = reinterpret_cast<S*>(p.kcache) + base;
+  S* vc = reinterpret_cast<S*>(p.vcache) + base;
+  if (isk) {
+    if constexpr (T::EPL == 8) {
+      store8(kc + kblk_off(key, d0, 8), v);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) kc[kblk_off(key, d0 + e, T::EPL)] = T::from_f(v[e]);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) vc[vblk_off(key, d0 + e)] = T::from_f(v[e]);
+  }
 }
 
 hipError_t launch_qkv_fix(int dtype, const GemmParams& p, const float* part, int S, hipStream_t st) {
   const int N = (p.n_heads + 2 * p.n_kv) * p.hd;
   if (p.M <= 0) return hipSuccess;
-  dim3 grid((N + 255) / 256, p.M);
+  if (N % 16 || p.hd % 16) return hipErrorInvalidValue;
+  dim3 grid((unsigned)(((size_t)p.M * (N / 8) + 255) / 256));
   if (dtype == 1)
     hipLaunchKernelGGL(qkv_fix_kernel<bf16_t>, grid, dim3(256), 0, st, p, part, S, N);
   else

@@ -62,11 +62,7 @@ __global__ __launch_bounds__(WR * TWAVES * 64) void tiled_kernel(const GemmParam
   const int nk = c1 - c0;
   const int nst = (nk + TSC - 1) / TSC;
 
-  if (p.mode == EP_QKV && threadIdx.x < BM) {
-    const int m = min(m0 + (int)threadIdx.x, p.M - 1);
-    const int slot = p.row_slot[m];
-    s_kvbase[threadIdx.x] = p.block_table[(size_t)p.row_seq[m] * p.max_blocks + (slot >> 4)] * 16 + (slot & 15);
-  }
+  if (p.mode == EP_QKV && threadIdx.x < BM) s_kvbase[threadIdx.x] = p.row_kb[min(m0 + (int)threadIdx.x, p.M - 1)];
 
   // This wave's weight tiles.  SwiGLU: tiles [0, HT) are gate tiles and [HT, TW) the up
   // tiles of the same columns.  Otherwise tile j is column tile (g*4 + wave)*TW + j over

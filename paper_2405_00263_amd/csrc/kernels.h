@@ -57,8 +57,7 @@ struct GemmParams {
   // EP_QKV
   void* qbuf; int ldq;
   void* kcache; void* vcache;
-  const int* row_seq; const int* row_slot;
-  const int* block_table; int max_blocks;
+  const int* row_kb;  // [M] physical KV slot of each row: cache block * 16 + slot % 16 (launch_rope_table)
   int n_heads, n_kv, hd;
   const float* rope_cs;  // [M][hd/2] (cos, sin) pairs of each row's position (launch_rope_table)
 };
@@ -129,7 +128,13 @@ void plan_attention(AttnParams& p);
 hipError_t launch_embed(int dtype, const void* emb, const int* tok, int M, int d, float* x,
                         hipStream_t st);
 // cs[m][i] = (cos, sin)(pos[m] * theta^(-2i/hd)), i < hd/2: the rotary factors of each row
-hipError_t launch_rope_table(const int* pos, int M, int hd, float theta, float* cs, hipStream_t st);
+// Per-row tables of a forward over M rows, written once before its layers: the rotary
+// factors cs [M][hd/2] of each row's position and, when kb is given, each row's physical KV
+// slot kb[m] = block_table[seq[m]][slot[m] / 16] * 16 + slot[m] % 16 (the Q|K|V epilogues'
+// append target), so the per-layer kernels do not repeat the two dependent table loads.
+hipError_t launch_rope_table(const int* pos, int M, int hd, float theta, float* cs, hipStream_t st,
+                             const int* seq = nullptr, const int* slot = nullptr,
+                             const int* block_table = nullptr, int max_blocks = 0, int* kb = nullptr);
 // out[m] = argmax of row m from the keys[G][M] a GEMM left in GemmParams::amax_part (G =
 // its plan's ngroups)
 hipError_t launch_argmax_groups(const unsigned long long* keys, int G, int M, int* out, hipStream_t st);

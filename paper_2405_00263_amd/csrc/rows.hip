@@ -55,8 +55,15 @@ __global__ void embed_kernel(const S* __restrict__ emb, const int* __restrict__ 
 // Rotary factors of each row's position (rotate-half pairing): the angle is formed and
 // reduced to [-pi, pi] in double precision, then sin/cos are taken in single precision.
 __global__ void rope_table_kernel(const int* __restrict__ pos, int M, int hd, float theta,
-                                  float* __restrict__ cs) {
+                                  float* __restrict__ cs, const int* __restrict__ seq,
+                                  const int* __restrict__ slot, const int* __restrict__ bt,
+                                  int max_blocks, int* __restrict__ kb) {
   const int half = hd / 2;
+  if (kb)
+    for (int m = blockIdx.x * blockDim.x + threadIdx.x; m < M; m += gridDim.x * blockDim.x) {
+      const int s = slot[m];
+      kb[m] = bt[(size_t)seq[m] * max_blocks + (s >> 4)] * 16 + (s & 15);
+    }
   for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < M * half; e += gridDim.x * blockDim.x) {
     const int m = e / half, i = e % half;
     const double inv = pow((double)theta, -2.0 * (double)i / (double)hd);
@@ -69,10 +76,13 @@ __global__ void rope_table_kernel(const int* __restrict__ pos, int M, int hd, fl
   }
 }
 
-hipError_t launch_rope_table(const int* pos, int M, int hd, float theta, float* cs, hipStream_t st) {
+hipError_t launch_rope_table(const int* pos, int M, int hd, float theta, float* cs, hipStream_t st,
+                             const int* seq, const int* slot, const int* block_table, int max_blocks, int* kb) {
   if (M <= 0) return hipSuccess;
+  if (kb && (!seq || !slot || !block_table || max_blocks <= 0)) return hipErrorInvalidValue;
   const int n = M * (hd / 2);
-  hipLaunchKernelGGL(rope_table_kernel, dim3((n + 255) / 256), dim3(256), 0, st, pos, M, hd, theta, cs);
+  hipLaunchKernelGGL(rope_table_kernel, dim3((n + 255) / 256), dim3(256), 0, st, pos, M, hd, theta, cs,
+                     seq, slot, block_table, max_blocks, kb);
   return hipGetLastError();
 }
 
