@@ -144,9 +144,8 @@ __global__ __launch_bounds__(AT_THREADS) void attn_kernel(const AttnParams p) {
   const int bps = (nblocks + p.splits - 1) / p.splits;
   const int kb0 = min(nblocks, split * bps), nb = min(nblocks, kb0 + bps) - kb0;
 
-  const int* bt = p.block_table + (size_t)slot * p.max_blocks;
-  for (int i = threadIdx.x; i < nb; i += AT_THREADS) s_bt[i] = bt[kb0 + i];
-
+  // Q and the mask rows are loaded before the block table, so the three loads share one
+  // memory round trip (the table's store to LDS waits for its load)
   const S* Q = reinterpret_cast<const S*>(p.Q);
   u32x4_t qf[NQC];
 #pragma unroll
@@ -162,6 +161,8 @@ __global__ __launch_bounds__(AT_THREADS) void attn_kernel(const AttnParams p) {
     mw0 = mr[0];
     if (p.mask_words > 1) mw1 = mr[1];
   }
+  const int* bt = p.block_table + (size_t)slot * p.max_blocks;
+  for (int i = threadIdx.x; i < nb; i += AT_THREADS) s_bt[i] = bt[kb0 + i];
   __syncthreads();  // s_bt
 
   const S* kc = reinterpret_cast<const S*>(p.kcache);
@@ -340,27 +341,38 @@ __global__ __launch_bounds__(AT_THREADS) void attn_kernel(const AttnParams p) {
 }
 
 // Combine the splits of one (item, query tile) in split order; same XCD as its splits.
-// Every split's record is loaded up front (one memory latency, not one per split).
+// One single-wave workgroup per 4 rows of a query tile: the records are spread over many
+// compute units (a compute unit moves only tens of GB/s, so bytes per unit set the time).
+// The live splits' records are loaded up front (one memory latency, not one per split).
+static constexpr int MERGE_ROWS = 4;
 template <typename S, int HD>
-__global__ __launch_bounds__(256) void attn_merge_kernel(const AttnParams p) {
+__global__ __launch_bounds__(64) void attn_merge_kernel(const AttnParams p) {
   using T = St<S>;
   constexpr int DPT = HD / 16;  // dims per thread
+  constexpr int RG = 16 / MERGE_ROWS;  // row groups per query tile
   const int id = blockIdx.x, xcd = id & 7, slotx = id >> 3;
-  const int item = (slotx / p.qt_item) * 8 + xcd, qi = slotx % p.qt_item;
+  const int item = (slotx / (p.qt_item * RG)) * 8 + xcd, rem = slotx % (p.qt_item * RG);
+  const int qi = rem / RG, rg = rem % RG;
   if (item >= p.nbatch * p.n_kv) return;
   const int b = item / p.n_kv, kvh = item % p.n_kv, G = p.n_heads / p.n_kv;
   const int h = kvh * G + qi / p.qph, qt = qi % p.qph;
-  const int j = threadIdx.x >> 4, d0 = (threadIdx.x & 15) * DPT;
+  const int j = rg * MERGE_ROWS + (threadIdx.x >> 4), d0 = (threadIdx.x & 15) * DPT;
   const int row = qt * 16 + j;
   if (row >= p.nq) return;
   float ms[AT_MAX_SPLITS], ls[AT_MAX_SPLITS], ov[AT_MAX_SPLITS][DPT];
 #pragma unroll
   for (int s = 0; s < AT_MAX_SPLITS; ++s) {
-    const float* r = p.part + part_rec(p, item, min(s, p.splits - 1), qi, j, HD);
-    ms[s] = r[HD];
-    ls[s] = r[HD + 1];
+    ms[s] = -INFINITY;
+    ls[s] = 0.f;
 #pragma unroll
-    for (int e = 0; e < DPT; ++e) ov[s][e] = r[d0 + e];
+    for (int e = 0; e < DPT; ++e) ov[s][e] = 0.f;
+    if (s < p.splits) {
+      const float* r = p.part + part_rec(p, item, s, qi, j, HD);
+      ms[s] = r[HD];
+      ls[s] = r[HD + 1];
+#pragma unroll
+      for (int e = 0; e < DPT; ++e) ov[s][e] = r[d0 + e];
+    }
   }
   float M = -INFINITY;
 #pragma unroll
@@ -424,9 +436,9 @@ static hipError_t launch_attn_hd(AttnParams& p, hipStream_t st, const LaunchTimi
   if (p.qtile == 8) go(attn_kernel<S, HD, 8>);
   else go(attn_kernel<S, HD, 4>);
   if (merge) {
-    dim3 mgrid(8 * per_xcd * p.qt_item);
-    if (lt) hipExtLaunchKernelGGL((attn_merge_kernel<S, HD>), mgrid, dim3(256), 0, st, nullptr, lt->stop, 0, p);
-    else hipLaunchKernelGGL((attn_merge_kernel<S, HD>), mgrid, dim3(256), 0, st, p);
+    dim3 mgrid(8 * per_xcd * p.qt_item * (16 / MERGE_ROWS));
+    if (lt) hipExtLaunchKernelGGL((attn_merge_kernel<S, HD>), mgrid, dim3(64), 0, st, nullptr, lt->stop, 0, p);
+    else hipLaunchKernelGGL((attn_merge_kernel<S, HD>), mgrid, dim3(64), 0, st, p);
   }
   return hipGetLastError();
 }

@@ -130,14 +130,35 @@ __device__ __forceinline__ size_t kv_block_base(const int* block_table, int max_
   return ((size_t)blk * n_kv + kvh) * (size_t)(16 * hd);
 }
 
-__device__ __forceinline__ float warp_sum(float v) {
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+// Sum over the 64 lanes of a wave in a fixed order with lane moves that stay in the VALU (no
+// LDS round trip per step): DPP inside each 16-lane row (quad swaps 1 and 2, half-row and row mirrors), then the
+// 16- and 32-lane swaps.  Every lane ends with the same value.
+#define CLOVER_DPP_ADD(v, ctrl) \
+  (v) += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), (ctrl), 0xF, 0xF, true))
+__device__ __forceinline__ float wave_sum(float v) {
+  CLOVER_DPP_ADD(v, 0xB1);   // quad_perm [1,0,3,2]
+  CLOVER_DPP_ADD(v, 0x4E);   // quad_perm [2,3,0,1]
+  CLOVER_DPP_ADD(v, 0x141);  // row_half_mirror
+  CLOVER_DPP_ADD(v, 0x140);  // row_mirror
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(b[0]) + __uint_as_float(b[1]);
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(a[0]) + __uint_as_float(a[1]);
 }
-__device__ __forceinline__ float warp_max(float v) {
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
+#define CLOVER_DPP_MAX(v, ctrl) \
+  (v) = fmaxf((v), __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), (ctrl), 0xF, 0xF, true)))
+__device__ __forceinline__ float wave_max(float v) {
+  CLOVER_DPP_MAX(v, 0xB1);
+  CLOVER_DPP_MAX(v, 0x4E);
+  CLOVER_DPP_MAX(v, 0x141);
+  CLOVER_DPP_MAX(v, 0x140);
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
 }
+#undef CLOVER_DPP_MAX
+#undef CLOVER_DPP_ADD
 __device__ __forceinline__ float silu_f(float x) { return x / (1.0f + __expf(-x)); }
 
 // ---- counter-based random numbers and Gumbel-max sampling ----------------------------------

@@ -49,22 +49,35 @@ static_assert(RING % 2 == 0, "stages alternate between two LDS buffers inside a 
 template <int NW>
 __device__ __forceinline__ const u32x4_t* wave_weight_ptr(const GemmParams& p, int g, int wave,
                                                           bool& active) {
-  int seg = 0, t;
+  // The segment fields are read at constant indices (scalar loads of the argument block) and
+  // selected per wave: indexing them by the wave's segment would make them vector loads from
+  // the argument block, two dependent memory round trips before the first weight load.
+  const int tl0 = p.seg[0].tiles, tl1 = p.seg[1].tiles;
+  const void* w0 = p.seg[0].w;
+  const void* w1 = p.seg[1].w;
+  const void* w2 = p.seg[2].w;
+  const void* w = w0;
+  int t;
   if (p.mode == EP_SWIGLU) {  // waves [0, NW/2) gate tiles, [NW/2, NW) the matching up tiles
     constexpr int H = NW / 2;
-    seg = wave >= H ? 1 : 0;
-    t = g * H + wave - seg * H;
-    active = t < p.seg[seg].tiles;
-  } else {
+    const bool up = wave >= H;
+    t = g * H + wave - (up ? H : 0);
+    active = t < (up ? tl1 : tl0);
+    w = up ? w1 : w0;
+  } else {  // tile t of the concatenated segments; the last segment takes the rest
     t = g * NW + wave;
     active = t < p.ntiles;
-    while (active && seg < p.nseg - 1 && t >= p.seg[seg].tiles) {
-      t -= p.seg[seg].tiles;
-      ++seg;
+    if (p.nseg > 1 && t >= tl0) {
+      t -= tl0;
+      w = w1;
+      if (p.nseg > 2 && t >= tl1) {
+        t -= tl1;
+        w = w2;
+      }
     }
   }
   if (!active) return nullptr;
-  return reinterpret_cast<const u32x4_t*>(p.seg[seg].w) + (size_t)t * p.nchunks * 64;
+  return reinterpret_cast<const u32x4_t*>(w) + (size_t)t * p.nchunks * 64;
 }
 
 template <typename S, int NW>
@@ -123,10 +136,11 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(const GemmParams p) {
   const int nk = c1 - c0;
   const int nst = (nk + STAGE_CHUNKS - 1) / STAGE_CHUNKS;
 
-  // KV-append targets of the fused epilogue, loaded once up front so the epilogue's row
-  // loop has no dependent global loads
+  // KV-append targets of the fused epilogue: loaded up front into a register (nothing waits
+  // for it before the epilogue) and staged in LDS for the epilogue's row loop
   __shared__ int s_kvbase[MROWS];
-  if (p.mode == EP_QKV && threadIdx.x < MROWS) s_kvbase[threadIdx.x] = p.row_kb[min(m0 + (int)threadIdx.x, p.M - 1)];
+  int kvb = 0;
+  if (p.mode == EP_QKV && threadIdx.x < MROWS) kvb = p.row_kb[min(m0 + (int)threadIdx.x, p.M - 1)];
 
   bool active;
   const u32x4_t* wp = wave_weight_ptr<NW>(p, g, wave, active);
@@ -257,6 +271,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(const GemmParams p) {
     }
     return;
   }
+  if (threadIdx.x < MROWS) s_kvbase[threadIdx.x] = kvb;
   const int col = wave * 16 + (lane & 15);
   float* tile = reinterpret_cast<float*>(smem);
 #pragma unroll
@@ -457,55 +472,71 @@ __device__ __forceinline__ void store8(float* dst, const float (&x)[8]) {
 
 // Q|K|V finished from K-split partials part[s][m][pc] (packed column order), summed in split
 // order, then rotary and stores with the same arithmetic as the fused epilogue (qkv_store).
-// One thread per (row, 8-column half of a 16-column tile): the half's partner half is the
-// other half of the same tile, its 8 values are 8 consecutive dims of one head, so Q and K
-// go out as one 16-byte store each (K in the cache's fragment order keeps 8 dims of a key
-// together); V scatters to the cache's key-minor layout.
-template <typename S>
-__global__ __launch_bounds__(256) void qkv_fix_kernel(const GemmParams p, const float* __restrict__ part, int S_, int N) {
+// One thread per (row, 8-column half of a 16-column tile).  Thread 2t holds the first half of
+// a tile and 2t + 1 its rotary partners, so each reads only its own 8 columns and takes the
+// partner sums from the neighbouring lane (DPP quad swap); the 8 values are 8 consecutive dims
+// of one head, so Q and K go out as one 16-byte store each (K in the cache's fragment order
+// keeps 8 dims of a key together) and V scatters to the cache's key-minor layout.  Every load
+// (partials, rotary factors, KV slot) is issued before any is used: one memory round trip.
+static constexpr int FIX_QKV_MAXS = 4;
+template <typename S, int NS>
+__global__ __launch_bounds__(256) void qkv_fix_kernel(const GemmParams p, const float* __restrict__ part, int N) {
   const int N8 = N >> 3, id = blockIdx.x * 256 + threadIdx.x;
-  const int m = id / N8, pc0 = (id % N8) * 8;
-  if (m >= p.M) return;
+  // rows past M (the grid's last workgroup) read row M - 1 and store nothing, so every lane
+  // takes part in the partner exchange
+  const int m_raw = id / N8, m = min(m_raw, p.M - 1), pc0 = (id % N8) * 8;
   const int hd = p.hd, half = hd >> 1, qd = p.n_heads * hd, kvd = p.n_kv * hd;
   const int pt = pc0 >> 4, jj0 = pc0 & 15, qt = qd / 16, kt = kvd / 16;
   const bool rot = pt < qt + kt;
-  float v[8], w[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) v[e] = w[e] = 0.f;
-  for (int s = 0; s < S_; ++s) {
-    const float* r = part + ((size_t)s * p.M + m) * N;
-    const float4 a0 = *reinterpret_cast<const float4*>(r + pc0), a1 = *reinterpret_cast<const float4*>(r + pc0 + 4);
-    v[0] += a0.x; v[1] += a0.y; v[2] += a0.z; v[3] += a0.w;
-    v[4] += a1.x; v[5] += a1.y; v[6] += a1.z; v[7] += a1.w;
-    if (rot) {
-      const float4 b0 = *reinterpret_cast<const float4*>(r + (pc0 ^ 8));
-      const float4 b1 = *reinterpret_cast<const float4*>(r + (pc0 ^ 8) + 4);
-      w[0] += b0.x; w[1] += b0.y; w[2] += b0.z; w[3] += b0.w;
-      w[4] += b1.x; w[5] += b1.y; w[6] += b1.z; w[7] += b1.w;
-    }
-  }
   int n0;  // logical column of the first of the 8
   if (rot) {
     const int seg0 = pt < qt ? 0 : qt;
     n0 = seg0 * 16 + rope_row(pt - seg0, jj0, hd);
-    const int d0 = n0 % hd, dlo0 = d0 < half ? d0 : d0 - half;
-    const float2* cs = reinterpret_cast<const float2*>(p.rope_cs) + (size_t)m * half + dlo0;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float2 c = cs[e];
-      v[e] = (jj0 < 8) ? (v[e] * c.x - w[e] * c.y) : (v[e] * c.x + w[e] * c.y);
-    }
   } else {
     n0 = pc0;
+  }
+  const int d0 = n0 % hd, dlo0 = d0 < half ? d0 : d0 - half;
+  float4 pa[NS][2];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    const float* r = part + ((size_t)s * p.M + m) * N + pc0;
+    pa[s][0] = *reinterpret_cast<const float4*>(r);
+    pa[s][1] = *reinterpret_cast<const float4*>(r + 4);
+  }
+  // rotary factors of the 8 dims (V columns read a valid row they do not use)
+  float4 cs4[4];
+  const float4* cs = reinterpret_cast<const float4*>(reinterpret_cast<const float2*>(p.rope_cs) + (size_t)m * half + dlo0);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) cs4[k] = cs[k];
+  const int kb = p.row_kb[m];
+  float v[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = 0.f;
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    v[0] += pa[s][0].x; v[1] += pa[s][0].y; v[2] += pa[s][0].z; v[3] += pa[s][0].w;
+    v[4] += pa[s][1].x; v[5] += pa[s][1].y; v[6] += pa[s][1].z; v[7] += pa[s][1].w;
+  }
+  // partner sums: lane id ^ 1 (the same row, the other half of the tile)
+  float w[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) w[e] = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v[e]), 0xB1, 0xF, 0xF, true));
+  if (m_raw >= p.M) return;
+  if (rot) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float cx = (e & 1) ? cs4[e >> 1].z : cs4[e >> 1].x, sy = (e & 1) ? cs4[e >> 1].w : cs4[e >> 1].y;
+      v[e] = (jj0 < 8) ? (v[e] * cx - w[e] * sy) : (v[e] * cx + w[e] * sy);
+    }
   }
   if (n0 < qd) {
     store8(reinterpret_cast<S*>(p.qbuf) + (size_t)m * p.ldq + n0, v);
     return;
   }
   using T = St<S>;
-  const int kb = p.row_kb[m], key = kb & 15;
+  const int key = kb & 15;
   const bool isk = n0 < qd + kvd;
-  const int kvh = (isk ? n0 - qd : n0 - qd - kvd) / hd, d0 = n0 % hd;
+  const int kvh = (isk ? n0 - qd : n0 - qd - kvd) / hd;
   const size_t base = ((size_t)(kb >> 4) * p.n_kv + kvh) * (size_t)(16 * hd);
   S* kc = reinterpret_cast<S*>(p.kcache) + base;
   S* vc = reinterpret_cast<S*>(p.vcache) + base;
@@ -522,15 +553,24 @@ __global__ __launch_bounds__(256) void qkv_fix_kernel(const GemmParams p, const 
   }
 }
 
+template <typename S>
+static void launch_qkv_fix_t(const GemmParams& p, const float* part, int S_, int N, dim3 grid, hipStream_t st) {
+  switch (S_) {
+    case 1: hipLaunchKernelGGL((qkv_fix_kernel<S, 1>), grid, dim3(256), 0, st, p, part, N); break;
+    case 2: hipLaunchKernelGGL((qkv_fix_kernel<S, 2>), grid, dim3(256), 0, st, p, part, N); break;
+    case 3: hipLaunchKernelGGL((qkv_fix_kernel<S, 3>), grid, dim3(256), 0, st, p, part, N); break;
+    default: hipLaunchKernelGGL((qkv_fix_kernel<S, 4>), grid, dim3(256), 0, st, p, part, N); break;
+  }
+}
+
 hipError_t launch_qkv_fix(int dtype, const GemmParams& p, const float* part, int S, hipStream_t st) {
   const int N = (p.n_heads + 2 * p.n_kv) * p.hd;
   if (p.M <= 0) return hipSuccess;
-  if (N % 16 || p.hd % 16) return hipErrorInvalidValue;
+  if (N % 16 || p.hd % 16 || S < 1 || S > FIX_QKV_MAXS) return hipErrorInvalidValue;
+  // a whole number of 256-thread workgroups; partner lanes (2t, 2t + 1) share a row
   dim3 grid((unsigned)(((size_t)p.M * (N / 8) + 255) / 256));
-  if (dtype == 1)
-    hipLaunchKernelGGL(qkv_fix_kernel<bf16_t>, grid, dim3(256), 0, st, p, part, S, N);
-  else
-    hipLaunchKernelGGL(qkv_fix_kernel<float>, grid, dim3(256), 0, st, p, part, S, N);
+  if (dtype == 1) launch_qkv_fix_t<bf16_t>(p, part, S, N, grid, st);
+  else launch_qkv_fix_t<float>(p, part, S, N, grid, st);
   return hipGetLastError();
 }
 

@@ -62,33 +62,43 @@ __global__ __launch_bounds__(WR * TWAVES * 64) void tiled_kernel(const GemmParam
   const int nk = c1 - c0;
   const int nst = (nk + TSC - 1) / TSC;
 
-  if (p.mode == EP_QKV && threadIdx.x < BM) s_kvbase[threadIdx.x] = p.row_kb[min(m0 + (int)threadIdx.x, p.M - 1)];
+  int kvb = 0;  // KV-append target of row threadIdx.x (fused epilogue), staged in LDS at the end
+  if (p.mode == EP_QKV && threadIdx.x < BM) kvb = p.row_kb[min(m0 + (int)threadIdx.x, p.M - 1)];
 
   // This wave's weight tiles.  SwiGLU: tiles [0, HT) are gate tiles and [HT, TW) the up
   // tiles of the same columns.  Otherwise tile j is column tile (g*4 + wave)*TW + j over
   // the concatenated segments.  Tiles past the end stream tile 0 and store nothing.
+  // (segment fields at constant indices: scalar loads of the argument block, selected per tile)
+  const int tl0 = p.seg[0].tiles, tl1 = p.seg[1].tiles;
+  const u32x4_t* w0 = reinterpret_cast<const u32x4_t*>(p.seg[0].w);
+  const u32x4_t* w1 = reinterpret_cast<const u32x4_t*>(p.seg[1].w);
+  const u32x4_t* w2 = reinterpret_cast<const u32x4_t*>(p.seg[2].w);
   const u32x4_t* wp[TW];
   int otile[TW];
   bool act[TW];
 #pragma unroll
   for (int j = 0; j < TW; ++j) {
-    int seg = 0, t;
+    int t;
+    const u32x4_t* w = w0;
     if (p.mode == EP_SWIGLU) {
-      seg = j < HT ? 0 : 1;
       t = (g * TWAVES + wave) * HT + (j % HT);
-      act[j] = t < p.seg[0].tiles;
+      act[j] = t < tl0;
       otile[j] = t;
+      if (j >= HT) w = w1;
     } else {
       t = (g * TWAVES + wave) * TW + j;
       act[j] = t < p.ntiles;
       otile[j] = t;
-      while (act[j] && seg < p.nseg - 1 && t >= p.seg[seg].tiles) {
-        t -= p.seg[seg].tiles;
-        ++seg;
+      if (p.nseg > 1 && t >= tl0) {
+        t -= tl0;
+        w = w1;
+        if (p.nseg > 2 && t >= tl1) {
+          t -= tl1;
+          w = w2;
+        }
       }
     }
-    const u32x4_t* base = act[j] ? reinterpret_cast<const u32x4_t*>(p.seg[seg].w) + (size_t)t * p.nchunks * 64
-                                 : reinterpret_cast<const u32x4_t*>(p.seg[0].w);
+    const u32x4_t* base = act[j] ? w + (size_t)t * p.nchunks * 64 : w0;
     wp[j] = base + (size_t)c0 * 64 + lane;
   }
 
@@ -252,6 +262,7 @@ __global__ __launch_bounds__(WR * TWAVES * 64) void tiled_kernel(const GemmParam
     constexpr int TS = 17;  // floats per LDS row
     static_assert(WR * TWAVES * WM * TS * 4 <= 2 * XBUF * 2, "epilogue tile fits the X buffers");
     float* tile = reinterpret_cast<float*>(smem) + (wrow * TWAVES + wave) * WM * TS;
+    if (threadIdx.x < BM) s_kvbase[threadIdx.x] = kvb;
 #pragma unroll
     for (int j = 0; j < TW; ++j) {
       __syncthreads();  // previous readers of this LDS space are done

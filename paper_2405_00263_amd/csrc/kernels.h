@@ -167,6 +167,7 @@ struct RowFixParams {
   const void* gain; float eps;         // RMSNorm gain (storage)
   void* out_norm; int ldn;             // optional RMSNorm(result) * gain, storage
   unsigned long long* zero_keys; int zero_n;  // optional: clear argmax keys
+  int no_resid;                        // set by launch_rowfix: resid was null (read, then zeroed)
 };
 hipError_t launch_rowfix(int dtype, RowFixParams& p, hipStream_t st);
 

@@ -98,7 +98,7 @@ hipError_t launch_embed(int dtype, const void* emb, const int* tok, int M, int d
 
 // block-wide sum over 256 threads
 __device__ __forceinline__ float block_sum256(float v, float* red) {
-  v = warp_sum(v);
+  v = wave_sum(v);
   const int w = threadIdx.x >> 6;
   __syncthreads();
   if ((threadIdx.x & 63) == 0) red[w] = v;
@@ -282,7 +282,7 @@ __global__ __launch_bounds__(RED_THREADS) void topk_stage1_kernel(const float* _
     mx = fmaxf(mx, v[u]);
   }
   // chunk max and sum of exponentials
-  float bm = warp_max(mx);
+  float bm = wave_max(mx);
   const int w = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) sred[w] = bm;
   __syncthreads();
@@ -291,7 +291,7 @@ __global__ __launch_bounds__(RED_THREADS) void topk_stage1_kernel(const float* _
   float se = 0.f;
 #pragma unroll
   for (int u = 0; u < TOPK_EPT; ++u) se += (v[u] == -INFINITY) ? 0.f : expf(v[u] - cmax);
-  se = warp_sum(se);
+  se = wave_sum(se);
   // the wave's k best, then the chunk's from the waves' lists
   wave_topk<TOPK_EPT>(v, ix, k, s_v + w * KMAX, s_i + w * KMAX);
   __syncthreads();
@@ -401,83 +401,119 @@ __device__ __forceinline__ void store4(float* p, float a, float b, float c, floa
   *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);
 }
 
-template <typename S>
+// four consecutive storage elements as one packed load, unpacked to floats later
+template <typename S> struct Raw4;
+template <> struct Raw4<bf16_t> { typedef u32x2_t type; };
+template <> struct Raw4<float> { typedef float4 type; };
+__device__ __forceinline__ float4 raw4_to_f(u32x2_t r) {
+  return make_float4(__uint_as_float(r[0] << 16), __uint_as_float(r[0] & 0xffff0000u), __uint_as_float(r[1] << 16),
+                     __uint_as_float(r[1] & 0xffff0000u));
+}
+__device__ __forceinline__ float4 raw4_to_f(float4 r) { return r; }
+
+// VEC float4 per thread (d <= VEC * 4096), NS split partials.  Every load is unconditional, at
+// a clamped column (lanes past d re-read the row's last 4 elements and store nothing), and the
+// gain and bias come from a valid row when unused, so all loads are in flight before the first
+// use: one memory round trip.  The gain and bias stay packed storage words until then.
+template <typename S, int VEC, int NS>
 __global__ __launch_bounds__(FIX_THREADS) void rowfix_kernel(const RowFixParams p) {
   using T = St<S>;
+  using R4 = typename Raw4<S>::type;
   __shared__ float red[FIX_THREADS / 64];
   const int m = blockIdx.x, d = p.d;
   if (p.zero_keys && m == 0)
     for (int i = threadIdx.x; i < p.zero_n; i += FIX_THREADS) p.zero_keys[i] = 0ull;
-  float4 acc[FIX_VEC];
-  float4 part[FIX_MAXS][FIX_VEC];
-  float4 res[FIX_VEC];
-  float4 gn[FIX_VEC];  // RMSNorm gain, loaded with everything else before the reduction
+  const S* gp = reinterpret_cast<const S*>(p.out_norm ? p.gain : static_cast<const void*>(p.resid));
+  const S* bp = reinterpret_cast<const S*>(p.act == 1 ? p.bias : static_cast<const void*>(p.resid));
+  float4 acc[VEC];
+  float4 part[NS > 0 ? NS : 1][VEC];
+  float4 res[VEC];
+  R4 graw[VEC], braw[VEC];
 #pragma unroll
-  for (int i = 0; i < FIX_VEC; ++i) {
-    const int e = threadIdx.x * 4 + i * FIX_THREADS * 4;
-    gn[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (e < d && p.out_norm) {
-      const S* g = reinterpret_cast<const S*>(p.gain) + e;
-      gn[i] = make_float4(T::to_f(g[0]), T::to_f(g[1]), T::to_f(g[2]), T::to_f(g[3]));
-    }
-    res[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (e < d && p.resid) res[i] = *reinterpret_cast<const float4*>(p.resid + (size_t)m * p.ldr + e);
+  for (int i = 0; i < VEC; ++i) {
+    const int e = min((int)threadIdx.x * 4 + i * FIX_THREADS * 4, d - 4);
+    graw[i] = *reinterpret_cast<const R4*>(gp + e);
+    braw[i] = *reinterpret_cast<const R4*>(bp + e);
+    res[i] = *reinterpret_cast<const float4*>(p.resid + (size_t)m * p.ldr + e);
 #pragma unroll
-    for (int s = 0; s < FIX_MAXS; ++s) {
-      part[s][i] = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (s < p.S && e < d)
-        part[s][i] = *reinterpret_cast<const float4*>(p.part + ((size_t)s * p.M + m) * p.ldp + e);
-    }
+    for (int s = 0; s < NS; ++s) part[s][i] = *reinterpret_cast<const float4*>(p.part + ((size_t)s * p.M + m) * p.ldp + e);
   }
   float ss = 0.f;
 #pragma unroll
-  for (int i = 0; i < FIX_VEC; ++i) {
+  for (int i = 0; i < VEC; ++i) {
     const int e = threadIdx.x * 4 + i * FIX_THREADS * 4;
-    float4 y = part[0][i];
+    float4 y = NS > 0 ? part[0][i] : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-    for (int s = 1; s < FIX_MAXS; ++s)
-      if (s < p.S) { y.x += part[s][i].x; y.y += part[s][i].y; y.z += part[s][i].z; y.w += part[s][i].w; }
-    if (p.act == 1 && e < d) {
-      const S* b = reinterpret_cast<const S*>(p.bias) + e;
-      y.x = silu_f(y.x + T::to_f(b[0])); y.y = silu_f(y.y + T::to_f(b[1]));
-      y.z = silu_f(y.z + T::to_f(b[2])); y.w = silu_f(y.w + T::to_f(b[3]));
-    }
+    for (int s = 1; s < NS; ++s) { y.x += part[s][i].x; y.y += part[s][i].y; y.z += part[s][i].z; y.w += part[s][i].w; }
+    // the activation as a select, so the bias load is not moved behind a branch on act
+    const float4 b = raw4_to_f(braw[i]);
+    const bool act = p.act == 1;
+    y.x = act ? silu_f(y.x + b.x) : y.x; y.y = act ? silu_f(y.y + b.y) : y.y;
+    y.z = act ? silu_f(y.z + b.z) : y.z; y.w = act ? silu_f(y.w + b.w) : y.w;
+    if (p.no_resid) res[i] = make_float4(0.f, 0.f, 0.f, 0.f);
     float4 o = make_float4(res[i].x + y.x, res[i].y + y.y, res[i].z + y.z, res[i].w + y.w);
     acc[i] = o;
     if (e < d) {
       if (p.out_f) *reinterpret_cast<float4*>(p.out_f + (size_t)m * p.ldo + e) = o;
       if (p.out_copy_f) *reinterpret_cast<float4*>(p.out_copy_f + (size_t)m * d + e) = o;
-      if (p.out_copy_s) {
-        S* cs = reinterpret_cast<S*>(p.out_copy_s) + (size_t)m * d + e;
-        cs[0] = T::from_f(o.x); cs[1] = T::from_f(o.y); cs[2] = T::from_f(o.z); cs[3] = T::from_f(o.w);
-      }
+      if (p.out_copy_s) store4(reinterpret_cast<S*>(p.out_copy_s) + (size_t)m * d + e, o.x, o.y, o.z, o.w);
       ss += o.x * o.x + o.y * o.y + o.z * o.z + o.w * o.w;
     }
   }
   if (!p.out_norm) return;
-  ss = warp_sum(ss);
+  ss = wave_sum(ss);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
   __syncthreads();
   float tot = 0.f;
   for (int q = 0; q < FIX_THREADS / 64; ++q) tot += red[q];
   const float rinv = 1.0f / sqrtf(tot / (float)d + p.eps);
 #pragma unroll
-  for (int i = 0; i < FIX_VEC; ++i) {
+  for (int i = 0; i < VEC; ++i) {
     const int e = threadIdx.x * 4 + i * FIX_THREADS * 4;
     if (e >= d) continue;
     S* on = reinterpret_cast<S*>(p.out_norm) + (size_t)m * p.ldn + e;
-    store4(on, acc[i].x * rinv * gn[i].x, acc[i].y * rinv * gn[i].y, acc[i].z * rinv * gn[i].z,
-           acc[i].w * rinv * gn[i].w);
+    const float4 gn = raw4_to_f(graw[i]);
+    store4(on, acc[i].x * rinv * gn.x, acc[i].y * rinv * gn.y, acc[i].z * rinv * gn.z, acc[i].w * rinv * gn.w);
   }
+}
+
+template <typename S, int VEC>
+static void launch_rowfix_v(RowFixParams& p, hipStream_t st) {
+  const dim3 g(p.M), b(FIX_THREADS);
+  switch (p.S) {
+    case 0: hipLaunchKernelGGL((rowfix_kernel<S, VEC, 0>), g, b, 0, st, p); break;
+    case 1: hipLaunchKernelGGL((rowfix_kernel<S, VEC, 1>), g, b, 0, st, p); break;
+    case 2: hipLaunchKernelGGL((rowfix_kernel<S, VEC, 2>), g, b, 0, st, p); break;
+    case 3: hipLaunchKernelGGL((rowfix_kernel<S, VEC, 3>), g, b, 0, st, p); break;
+    case 4: hipLaunchKernelGGL((rowfix_kernel<S, VEC, 4>), g, b, 0, st, p); break;
+    case 5: hipLaunchKernelGGL((rowfix_kernel<S, VEC, 5>), g, b, 0, st, p); break;
+    case 6: hipLaunchKernelGGL((rowfix_kernel<S, VEC, 6>), g, b, 0, st, p); break;
+    case 7: hipLaunchKernelGGL((rowfix_kernel<S, VEC, 7>), g, b, 0, st, p); break;
+    default: hipLaunchKernelGGL((rowfix_kernel<S, VEC, 8>), g, b, 0, st, p); break;
+  }
+}
+
+template <typename S>
+static void launch_rowfix_t(RowFixParams& p, hipStream_t st) {
+  if (p.d <= FIX_THREADS * 4) launch_rowfix_v<S, 1>(p, st);
+  else launch_rowfix_v<S, 2>(p, st);
 }
 
 hipError_t launch_rowfix(int dtype, RowFixParams& p, hipStream_t st) {
   if (p.M <= 0) return hipSuccess;
-  if (p.S > FIX_MAXS || p.d > FIX_VEC * FIX_THREADS * 4 || p.d % 4) return hipErrorInvalidValue;
-  if (dtype == 1)
-    hipLaunchKernelGGL(rowfix_kernel<bf16_t>, dim3(p.M), dim3(FIX_THREADS), 0, st, p);
-  else
-    hipLaunchKernelGGL(rowfix_kernel<float>, dim3(p.M), dim3(FIX_THREADS), 0, st, p);
+  if (p.S < 0 || p.S > FIX_MAXS || p.d < 4 || p.d > FIX_VEC * FIX_THREADS * 4 || p.d % 4) return hipErrorInvalidValue;
+  if ((p.S > 0 && !p.part) || (p.out_norm && !p.gain) || (p.act == 1 && !p.bias)) return hipErrorInvalidValue;
+  // the residual is read unconditionally: without one the kernel reads the first partial's
+  // rows in its place and zeroes them
+  p.no_resid = 0;
+  if (!p.resid) {
+    if (p.S < 1) return hipErrorInvalidValue;
+    p.resid = p.part;
+    p.ldr = p.ldp;
+    p.no_resid = 1;
+  }
+  if (dtype == 1) launch_rowfix_t<bf16_t>(p, st);
+  else launch_rowfix_t<float>(p, st);
   return hipGetLastError();
 }
 
@@ -538,8 +574,8 @@ __global__ __launch_bounds__(256) void ad_prep_kernel(const AdPrepParams p) {
       }
     }
   }
-  ss = warp_sum(ss);
-  se = warp_sum(se);
+  ss = wave_sum(ss);
+  se = wave_sum(se);
   if ((threadIdx.x & 63) == 0) {
     red[0][threadIdx.x >> 6] = ss;
     red[1][threadIdx.x >> 6] = se;
@@ -679,7 +715,7 @@ __global__ __launch_bounds__(64) void ad_attn_kernel(const AdAttnParams p) {
     float dot = 0.f;
 #pragma unroll
     for (int u = 0; u < AD_DPL; ++u) dot += q[u] * kk[t][u];
-    sc[t] = warp_sum(dot) * scale;
+    sc[t] = wave_sum(dot) * scale;
     if (t < nk) mx = fmaxf(mx, sc[t]);
   }
   float l = 0.f;
