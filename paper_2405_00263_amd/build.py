@@ -14,7 +14,10 @@ SRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libclover.so")
 BUILD = os.path.join(HERE, "_build")
 ARCH = "gfx950"
-SOURCES = ["gemm.hip", "gemm_tiled.hip", "attention.hip", "rows.hip", "tree.hip", "api.cpp", "noalloc.hip"]
+SOURCES = ["gemm.hip", "gemm_tiled.hip", "gemm_wide.hip", "attention.hip", "rows.hip", "tree.hip", "api.cpp", "noalloc.hip"]
+# per-source extra flags: the 32x32 matrix-core kernel keeps its accumulators in VGPRs (the
+# alternative form moves them between register files inside the loop)
+EXTRA_FLAGS = {"gemm_wide.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 CFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           # per-kernel resource report, read by _check_no_scratch
           "-Rpass-analysis=kernel-resource-usage",
@@ -62,7 +65,7 @@ def build(verbose: bool = False) -> str:
     for s in SOURCES:
         o = os.path.join(BUILD, os.path.splitext(s)[0] + ".o")
         objs.append(o)
-        cmds.append([hipcc, *CFLAGS, "-c", os.path.join(SRC, s), "-o", o])
+        cmds.append([hipcc, *CFLAGS, *EXTRA_FLAGS.get(s, []), "-c", os.path.join(SRC, s), "-o", o])
     with ThreadPoolExecutor(max_workers=min(len(cmds), os.cpu_count() or 4)) as ex:
         for src, out in zip(SOURCES, ex.map(_run, cmds)):
             _check_no_scratch(out, src)

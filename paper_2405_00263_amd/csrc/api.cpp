@@ -511,7 +511,8 @@ hipError_t run_attention_half(clover_ctx* c, const LayerPtrs& lw, int layer_idx,
   g.row_kb = c->at<int>(L.row_kb);
   g.n_heads = cf.n_heads; g.n_kv = cf.n_kv_heads; g.hd = hd; g.rope_cs = c->at<float>(L.rope_cs);
   const int qkv_tiles = (qd + 2 * kvd) / 16, kc = kc_of(cf.dtype);
-  if (plan_gemm(cf.dtype, M, qkv_tiles, d / kc, false, QKV_MAX_SPLITS).S > 1) {
+  const int qkv_seg[3] = {qd / 16, kvd / 16, kvd / 16};
+  if (plan_gemm(cf.dtype, M, qkv_tiles, d / kc, false, QKV_MAX_SPLITS, EP_QKV, qkv_seg, 3).S > 1) {
     // K-split Q|K|V: partials, then the fix-up pass (sums, rotary, stores)
     g.mode = EP_PARTIAL; g.max_splits = QKV_MAX_SPLITS; g.part = part;
     int sq = 1;

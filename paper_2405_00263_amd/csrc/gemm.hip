@@ -335,7 +335,11 @@ static int chunk_mt(int dtype, int M) {
   return (M <= 64 || dtype != 1) ? 4 : 8;
 }
 
-GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int max_splits) {
+GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int max_splits, int mode,
+                   const int* seg_tiles, int nseg, bool amax) {
+  GemmPlan wide;
+  if (dtype == 1 && !swiglu && !amax && plan_wide(M, ntiles, nchunks, mode, max_splits, seg_tiles, nseg, wide))
+    return wide;
   if (dtype == 1 && M >= TILED_MIN_M) return plan_tiled(M, ntiles, nchunks, swiglu, max_splits);
   const int es = es_of(dtype), EPL = 16 / es, KC = 4 * EPL;
   GemmPlan best{};
@@ -442,7 +446,10 @@ static hipError_t launch_gemm_t(GemmParams& p, const GemmPlan& pl, hipStream_t s
 
 hipError_t launch_gemm(int dtype, GemmParams& p, hipStream_t st, const LaunchTiming* lt) {
   const int maxs = p.mode == EP_PARTIAL && !p.amax_part ? std::max(1, p.max_splits) : 1;
-  const GemmPlan pl = plan_gemm(dtype, p.M, p.ntiles, p.nchunks, p.mode == EP_SWIGLU, maxs);
+  int seg_tiles[3];
+  for (int s = 0; s < p.nseg && s < 3; ++s) seg_tiles[s] = p.seg[s].tiles;
+  const GemmPlan pl = plan_gemm(dtype, p.M, p.ntiles, p.nchunks, p.mode == EP_SWIGLU, maxs, p.mode, seg_tiles,
+                                std::min(p.nseg, 3), p.amax_part != nullptr);
   p.ngroups = pl.ngroups;
   p.mchunks = pl.mchunks;
   p.S = pl.S;
@@ -454,30 +461,17 @@ hipError_t launch_gemm(int dtype, GemmParams& p, hipStream_t st, const LaunchTim
     }
     return hipSuccess;
   }
+  if (pl.tiled == 2) return launch_wide(p, pl, st, lt);
   if (pl.tiled) return launch_tiled(p, pl, st, lt);
   return dtype == 1 ? launch_gemm_t<bf16_t>(p, pl, st, lt) : launch_gemm_t<float>(p, pl, st, lt);
 }
 
-// eight consecutive storage elements from float values
-__device__ __forceinline__ void store8(bf16_t* dst, const float (&x)[8]) {
-  u32x4_t v;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) v[i] = (uint32_t)f2bf(x[2 * i]) | ((uint32_t)f2bf(x[2 * i + 1]) << 16);
-  *reinterpret_cast<u32x4_t*>(dst) = v;
-}
-__device__ __forceinline__ void store8(float* dst, const float (&x)[8]) {
-  *reinterpret_cast<float4*>(dst) = make_float4(x[0], x[1], x[2], x[3]);
-  *reinterpret_cast<float4*>(dst + 4) = make_float4(x[4], x[5], x[6], x[7]);
-}
-
 // Q|K|V finished from K-split partials part[s][m][pc] (packed column order), summed in split
-// order, then rotary and stores with the same arithmetic as the fused epilogue (qkv_store).
+// order, then rotary and stores with the same arithmetic as the fused epilogue (qkv_store8).
 // One thread per (row, 8-column half of a 16-column tile).  Thread 2t holds the first half of
 // a tile and 2t + 1 its rotary partners, so each reads only its own 8 columns and takes the
-// partner sums from the neighbouring lane (DPP quad swap); the 8 values are 8 consecutive dims
-// of one head, so Q and K go out as one 16-byte store each (K in the cache's fragment order
-// keeps 8 dims of a key together) and V scatters to the cache's key-minor layout.  Every load
-// (partials, rotary factors, KV slot) is issued before any is used: one memory round trip.
+// partner sums from the neighbouring lane (DPP quad swap).  Every load (partials, rotary
+// factors, KV slot) is issued before any is used: one memory round trip.
 static constexpr int FIX_QKV_MAXS = 4;
 template <typename S, int NS>
 __global__ __launch_bounds__(256) void qkv_fix_kernel(const GemmParams p, const float* __restrict__ part, int N) {
@@ -485,17 +479,7 @@ __global__ __launch_bounds__(256) void qkv_fix_kernel(const GemmParams p, const 
   // rows past M (the grid's last workgroup) read row M - 1 and store nothing, so every lane
   // takes part in the partner exchange
   const int m_raw = id / N8, m = min(m_raw, p.M - 1), pc0 = (id % N8) * 8;
-  const int hd = p.hd, half = hd >> 1, qd = p.n_heads * hd, kvd = p.n_kv * hd;
-  const int pt = pc0 >> 4, jj0 = pc0 & 15, qt = qd / 16, kt = kvd / 16;
-  const bool rot = pt < qt + kt;
-  int n0;  // logical column of the first of the 8
-  if (rot) {
-    const int seg0 = pt < qt ? 0 : qt;
-    n0 = seg0 * 16 + rope_row(pt - seg0, jj0, hd);
-  } else {
-    n0 = pc0;
-  }
-  const int d0 = n0 % hd, dlo0 = d0 < half ? d0 : d0 - half;
+  const QkvCols8 cols = qkv_cols8(p, pc0);
   float4 pa[NS][2];
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
@@ -503,11 +487,8 @@ __global__ __launch_bounds__(256) void qkv_fix_kernel(const GemmParams p, const 
     pa[s][0] = *reinterpret_cast<const float4*>(r);
     pa[s][1] = *reinterpret_cast<const float4*>(r + 4);
   }
-  // rotary factors of the 8 dims (V columns read a valid row they do not use)
   float4 cs4[4];
-  const float4* cs = reinterpret_cast<const float4*>(reinterpret_cast<const float2*>(p.rope_cs) + (size_t)m * half + dlo0);
-#pragma unroll
-  for (int k = 0; k < 4; ++k) cs4[k] = cs[k];
+  qkv_cs8(p, m, cols, cs4);
   const int kb = p.row_kb[m];
   float v[8];
 #pragma unroll
@@ -522,35 +503,7 @@ __global__ __launch_bounds__(256) void qkv_fix_kernel(const GemmParams p, const 
 #pragma unroll
   for (int e = 0; e < 8; ++e) w[e] = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v[e]), 0xB1, 0xF, 0xF, true));
   if (m_raw >= p.M) return;
-  if (rot) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float cx = (e & 1) ? cs4[e >> 1].z : cs4[e >> 1].x, sy = (e & 1) ? cs4[e >> 1].w : cs4[e >> 1].y;
-      v[e] = (jj0 < 8) ? (v[e] * cx - w[e] * sy) : (v[e] * cx + w[e] * sy);
-    }
-  }
-  if (n0 < qd) {
-    store8(reinterpret_cast<S*>(p.qbuf) + (size_t)m * p.ldq + n0, v);
-    return;
-  }
-  using T = St<S>;
-  const int key = kb & 15;
-  const bool isk = n0 < qd + kvd;
-  const int kvh = (isk ? n0 - qd : n0 - qd - kvd) / hd;
-  const size_t base = ((size_t)(kb >> 4) * p.n_kv + kvh) * (size_t)(16 * hd);
-  S* kc = reinterpret_cast<S*>(p.kcache) + base;
-  S* vc = reinterpret_cast<S*>(p.vcache) + base;
-  if (isk) {
-    if constexpr (T::EPL == 8) {
-      store8(kc + kblk_off(key, d0, 8), v);
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) kc[kblk_off(key, d0 + e, T::EPL)] = T::from_f(v[e]);
-    }
-  } else {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) vc[vblk_off(key, d0 + e)] = T::from_f(v[e]);
-  }
+  qkv_store8<S>(p, m, cols, v, w, cs4, kb);
 }
 
 template <typename S>

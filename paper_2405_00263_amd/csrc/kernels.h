@@ -63,7 +63,8 @@ struct GemmParams {
 };
 
 struct GemmPlan {
-  int tiled;     // 0: weight-streaming kernel; 1: register-blocked kernel (bf16, large M)
+  int tiled;     // 0: weight-streaming kernel; 1: register-blocked kernel (bf16, large M);
+                 // 2: 32x32 matrix-core kernel (gemm_wide.hip; mt, tw, ring = its MB, NB, stages)
   int nw;        // waves per workgroup (streaming: one 16-row weight tile each, 2..8; tiled: 4 or 8)
   int mt;        // m-tiles of 16 rows per chunk (streaming 1, 2 or 4) or per wave (tiled, 4)
   int tw;        // tiled: 16-row weight tiles per wave
@@ -73,7 +74,15 @@ struct GemmPlan {
   size_t part_floats;
 };
 
-GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int max_splits);
+// mode: the epilogue (EP_PARTIAL, EP_QKV, EP_SWIGLU); seg_tiles/nseg: the weight segments'
+// 16-row tile counts; amax: EP_PARTIAL with argmax keys.  Plans depend on all of them.
+GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int max_splits, int mode = EP_PARTIAL,
+                   const int* seg_tiles = nullptr, int nseg = 0, bool amax = false);
+// From this many rows on, bf16 Q|K|V and split-K projections may use the 32x32 kernel.
+constexpr int WIDE_MIN_M = 512;
+bool plan_wide(int M, int ntiles, int nchunks, int mode, int max_splits, const int* seg_tiles, int nseg,
+               GemmPlan& out);
+hipError_t launch_wide(GemmParams& p, const GemmPlan& pl, hipStream_t st, const LaunchTiming* lt);
 // Plan and launch of the register-blocked kernel (plan_gemm picks it for bf16 and large M).
 GemmPlan plan_tiled(int M, int ntiles, int nchunks, bool swiglu, int max_splits);
 // a plan of one instantiated shape (mt, tw, ring, nw waves) and split, for sweeps
