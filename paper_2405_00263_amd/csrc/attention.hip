@@ -60,6 +60,20 @@ __device__ __forceinline__ f32x4_t mma_pv(u32x4_t v, u32x2_t, const float p[4], 
   return c;
 }
 
+// P*V over two key blocks in one 16x16x32 product (bf16): the sum over keys may take them in
+// any order, so the k index of lane group g pairs its 4 keys of the first block (elements 0..3)
+// with its 4 keys of the second (4..7) in both operands; each lane already holds exactly those
+// probabilities and value columns.  Same output layout as the single-block product.
+__device__ __forceinline__ f32x4_t mma_pv2(u32x2_t v0, u32x2_t v1, u32x2_t p0, u32x2_t p1, const float*, const float*,
+                                           f32x4_t c, bf16_t) {
+  const u32x4_t a = {v0[0], v0[1], v1[0], v1[1]}, b = {p0[0], p0[1], p1[0], p1[1]};
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4_t mma_pv2(u32x4_t v0, u32x4_t v1, u32x2_t p0, u32x2_t p1, const float* q0, const float* q1,
+                                           f32x4_t c, float) {
+  return mma_pv(v1, p1, q1, mma_pv(v0, p0, q0, c, float{}), float{});
+}
+
 // Reductions over the four lanes that hold one query row's keys (lanes j, j+16, j+32,
 // j+48): VALU lane swaps (upper/lower 32 lanes, then odd/even 16-lane rows) instead of
 // LDS-routed shuffles.  Every lane of the row ends with the same value, summed in the
@@ -261,11 +275,15 @@ __global__ __launch_bounds__(AT_THREADS) void attn_kernel(const AttnParams p) {
       for (int t = 0; t < NT; ++t) o[t] *= alpha;
     }
 #pragma unroll
-    for (int i = 0; i < NG; ++i) {
-      if (i < nblk) {
-        const VT* vblk = reinterpret_cast<const VT*>(lds + (CB + cb0 + HALVES * i) * BVEC);
+    for (int i = 0; i < NG; i += 2) {
+      const VT* v0 = reinterpret_cast<const VT*>(lds + (CB + cb0 + HALVES * i) * BVEC);
+      if (i + 1 < nblk) {  // two blocks per product
+        const VT* v1 = reinterpret_cast<const VT*>(lds + (CB + cb0 + HALVES * (i + 1)) * BVEC);
 #pragma unroll
-        for (int t = 0; t < NT; ++t) o[t] = mma_pv(vblk[t * 64 + lane], pb[i], pr[i], o[t], S{});
+        for (int t = 0; t < NT; ++t) o[t] = mma_pv2(v0[t * 64 + lane], v1[t * 64 + lane], pb[i], pb[i + 1], pr[i], pr[i + 1], o[t], S{});
+      } else if (i < nblk) {
+#pragma unroll
+        for (int t = 0; t < NT; ++t) o[t] = mma_pv(v0[t * 64 + lane], pb[i], pr[i], o[t], S{});
       }
     }
   };
