@@ -320,6 +320,17 @@ size_t clover_op_linear_noalloc_max_bytes(void);
 clover_status clover_op_linear_noalloc(int32_t dtype, const void* X, int32_t M, int32_t K, const void* Wp,
                                        int32_t N, float* Y, void* hip_stream);
 
+/* The target layer's gated MLP activation (the SwiGLU feed-forward of the pre-norm decoder
+ * whose forward the verify runs, Sec. 2.1): act[M][F] (storage, device, row-major) =
+ * silu(X W_gate^T) * (X W_up^T), each product in fp32, the result rounded once to the storage
+ * type.  X: [M][K] storage (device, row-major); Wg_p, Wu_p: [F][K] matrices packed by
+ * clover_pack_matrix (F a multiple of 16, K of 32 for bf16 and 16 for f32).  Uses the
+ * kernel and plan the verify's MLP takes for M rows.  Needs no scratch; returns
+ * CLOVER_ERR_INVALID_ARG for bad sizes or null pointers, CLOVER_ERR_DEVICE if the launch
+ * fails. */
+clover_status clover_op_swiglu(int32_t dtype, const void* X, int32_t M, int32_t K, const void* Wg_p,
+                               const void* Wu_p, int32_t F, void* act, void* hip_stream);
+
 /* Tree attention (Sec. 2.2) for one sequence: queries Q[T][n_heads][head_dim] at
  * positions L + depth attend to prefix keys 0..L-1 and to tree keys j with
  * mask[i][j] (ancestor-or-self of i, from parents).  Kpre/Vpre: [L][n_kv][hd] and

@@ -90,6 +90,7 @@ EXPORTS = {
     "clover_op_linear": (ctypes.c_int, [ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "clover_packed_matrix_bytes": (ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
     "clover_pack_matrix": (ctypes.c_int, [ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]),
+    "clover_op_swiglu": (ctypes.c_int, [ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]),
     "clover_op_attention_scratch_bytes": (ctypes.c_size_t, [ctypes.c_int32] * 6),
     "clover_op_attention": (ctypes.c_int, [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "clover_op_argmax": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
@@ -366,6 +367,17 @@ def op_linear_noalloc(X, Wp, N: int):
     _check(lib().clover_op_linear_noalloc(dt, _ptr(X.contiguous()), M, K, _ptr(Wp), N, _ptr(Y),
                                           ctypes.c_void_p(_stream_handle())))
     return Y
+
+
+def op_swiglu(X, Wg_p, Wu_p, F: int):
+    """silu(X W_gate^T) * (X W_up^T) in the storage type of X, from packed gate and up matrices."""
+    import torch
+    dt = 1 if X.dtype == torch.bfloat16 else 0
+    M, K = X.shape
+    act = torch.empty(M, F, dtype=X.dtype, device=X.device)
+    _check(lib().clover_op_swiglu(dt, _ptr(X.contiguous()), M, K, _ptr(Wg_p), _ptr(Wu_p), F, _ptr(act),
+                                  ctypes.c_void_p(_stream_handle())))
+    return act
 
 
 def op_attention(Q, Kpre, Vpre, Ktree, Vtree, parents=None, causal=False):

@@ -14,9 +14,10 @@ SRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libclover.so")
 BUILD = os.path.join(HERE, "_build")
 ARCH = "gfx950"
-SOURCES = ["gemm.hip", "gemm_tiled.hip", "gemm_wide.hip", "attention.hip", "rows.hip", "tree.hip", "api.cpp", "noalloc.hip"]
-# per-source extra flags: the 32x32 matrix-core kernel keeps its accumulators in VGPRs (the
-# alternative form moves them between register files inside the loop)
+SOURCES = ["gemm.hip", "gemm_tiled.hip", "gemm_wide.hip", "gemm_wide_acc.hip", "attention.hip", "rows.hip", "tree.hip", "api.cpp", "noalloc.hip"]
+# per-source extra flags: the 32x32 matrix-core kernel's 128-row shapes keep their accumulators
+# in VGPRs (the alternative form moves them between register files inside the loop); its
+# 256-row shape (gemm_wide_acc.hip) needs the accumulation registers and takes the default
 EXTRA_FLAGS = {"gemm_wide.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 CFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           # per-kernel resource report, read by _check_no_scratch

@@ -1629,6 +1629,27 @@ clover_status clover_op_linear(int32_t dtype, const void* X, int32_t M, int32_t 
   return CLOVER_OK;
 }
 
+clover_status clover_op_swiglu(int32_t dtype, const void* X, int32_t M, int32_t K, const void* Wg_p,
+                               const void* Wu_p, int32_t F, void* act, void* hip_stream) {
+  // the sizes a model's ffn_dim and d_model may take (clover_config)
+  const int fq = dtype == 1 ? 32 : 16;
+  if ((dtype != 0 && dtype != 1) || M < 1 || K < 1 || K % kc_of(dtype) || F < fq || F % fq || !X || !Wg_p ||
+      !Wu_p || !act) {
+    set_global_err("op_swiglu: bad arguments");
+    return CLOVER_ERR_INVALID_ARG;
+  }
+  GemmParams p{};
+  p.X = X; p.ldx = K; p.M = M; p.K = K; p.nchunks = K / kc_of(dtype);
+  p.seg[0] = GemmSeg{Wg_p, F / 16}; p.seg[1] = GemmSeg{Wu_p, F / 16}; p.nseg = 2; p.ntiles = 2 * (F / 16);
+  p.N = F; p.mode = EP_SWIGLU; p.out_s = act; p.ldos = F;
+  const hipError_t e = launch_gemm(dtype, p, (hipStream_t)hip_stream);
+  if (e != hipSuccess) {
+    set_global_err("op_swiglu: %s", hipGetErrorString(e));
+    return CLOVER_ERR_DEVICE;
+  }
+  return CLOVER_OK;
+}
+
 size_t clover_op_attention_scratch_bytes(int32_t dtype, int32_t L, int32_t T, int32_t n_heads,
                                          int32_t n_kv, int32_t head_dim) {
   if ((dtype != 0 && dtype != 1) || L < 0 || T < 1 || L + T > 65536 || n_heads < 1 || n_kv < 1 || n_heads % n_kv ||

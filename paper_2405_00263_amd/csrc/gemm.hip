@@ -338,7 +338,7 @@ static int chunk_mt(int dtype, int M) {
 GemmPlan plan_gemm(int dtype, int M, int ntiles, int nchunks, bool swiglu, int max_splits, int mode,
                    const int* seg_tiles, int nseg, bool amax) {
   GemmPlan wide;
-  if (dtype == 1 && !swiglu && !amax && plan_wide(M, ntiles, nchunks, mode, max_splits, seg_tiles, nseg, wide))
+  if (dtype == 1 && !amax && plan_wide(M, ntiles, nchunks, swiglu ? EP_SWIGLU : mode, max_splits, seg_tiles, nseg, wide))
     return wide;
   if (dtype == 1 && M >= TILED_MIN_M) return plan_tiled(M, ntiles, nchunks, swiglu, max_splits);
   const int es = es_of(dtype), EPL = 16 / es, KC = 4 * EPL;

@@ -54,6 +54,44 @@ def test_linear_matches_definition(dt, M, N, K, sampled):
     assert np.all(err <= bound), float(np.max(err / bound))
 
 
+SWIGLU_CASES = [
+    # dtype, M, F, K, sampled: the 7B MLP at 64 rows (streaming), 300 and 1024 rows
+    # (register-blocked), 512 rows (256-row matrix-core workgroups); ragged rows and a last
+    # feature group with 4 of its 6 tile pairs past F on the matrix-core kernel; f32
+    ("bf16", 64, 11008, 4096, True), ("bf16", 300, 11008, 4096, True), ("bf16", 512, 11008, 4096, True),
+    ("bf16", 1024, 11008, 4096, True), ("bf16", 520, 1408, 512, False), ("bf16", 777, 1408, 512, False),
+    ("f32", 41, 1376, 256, False),
+]
+
+
+@pytest.mark.parametrize("dt,M,F,K,sampled", SWIGLU_CASES)
+def test_swiglu_matches_definition(dt, M, F, K, sampled):
+    """The target layer's gated MLP activation against its definition in float64 on the same
+    inputs: each product within the fp32-accumulation bound of the linear test, the result
+    within one ulp of the storage type plus the products' errors carried through."""
+    P = need_gpu()
+    note(f"swiglu {dt} M={M} F={F} K={K}")
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+    X = seeded((M, K), 3000 + M, 1.0, tdt)
+    Wg = seeded((F, K), 4000 + F, 0.02, tdt)
+    Wu = seeded((F, K), 5000 + F, 0.02, tdt)
+    act = to_np(P.op_swiglu(X, P.pack_matrix(Wg), P.pack_matrix(Wu), F).float())
+    torch.cuda.synchronize()
+    cols = np.arange(F)
+    if sampled:
+        rng = np.random.default_rng(1)
+        cols = np.unique(np.concatenate([np.arange(64), np.arange(F - 96, F), rng.choice(F, 384, replace=False)]))
+    idx = torch.as_tensor(cols, device=Wg.device)
+    Xn, Gn, Un = to_np(X).astype(np.float64), to_np(Wg[idx]).astype(np.float64), to_np(Wu[idx]).astype(np.float64)
+    g, u = Xn @ Gn.T, Xn @ Un.T
+    ref = oracle.silu(g) * u
+    dg, du = 1e-4 * (np.abs(Xn) @ np.abs(Gn).T), 1e-4 * (np.abs(Xn) @ np.abs(Un).T)
+    ulp = 2.0 ** -7 if dt == "bf16" else 2.0 ** -22
+    bound = ulp * np.abs(ref) + 1.1 * np.abs(u) * dg + np.abs(oracle.silu(g)) * du + 1e-7
+    err = np.abs(act[:, cols] - ref)
+    assert np.all(err <= bound), float(np.max(err / bound))
+
+
 def test_linear_is_deterministic():
     P = need_gpu()
     note("linear determinism")
