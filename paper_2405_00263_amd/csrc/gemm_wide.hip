@@ -26,10 +26,8 @@ bool plan_wide(int M, int ntiles, int nchunks, int mode, int max_splits, const i
     return true;
   }
   if (mode != EP_PARTIAL) return false;
-  // split-K projections with K up to 4096 only (measured in the 7B verify at 512 rows: the
-  // 4096-wide output projection 40 -> 28 us, the 11008-wide down projection no faster), and
-  // only shapes whose unsplit grid covers at most half the compute units
-  if (nchunks > 128) return false;
+  // split-K projections whose unsplit grid covers at most half the compute units (the 7B
+  // output and down projections at 512 rows: 4 splits)
   const GemmPlan one = make_wide(kWidePartial, M, ntiles, nchunks, 1);
   if ((long)one.ngroups * one.mchunks * 2 > WIDE_N_CU) return false;
   GemmPlan pl = one;

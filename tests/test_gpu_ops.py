@@ -30,6 +30,9 @@ GEMM_CASES = [
     ("bf16", 1024, 4096, 11008, True), ("bf16", 1024, 125696, 4096, True),
     ("bf16", 2048, 12288, 4096, True), ("bf16", 2048, 4096, 4096, True), ("bf16", 2048, 22016, 4096, True),
     ("bf16", 2048, 4096, 11008, True), ("bf16", 2048, 125696, 4096, True), ("bf16", 1500, 4096, 4096, True),
+    # 32x32 matrix-core kernel: the 7B output and down projections at 512 rows (4 K splits),
+    # ragged rows
+    ("bf16", 512, 4096, 11008, True), ("bf16", 520, 4096, 11008, True), ("bf16", 700, 4096, 4096, False),
 ]
 
 
