@@ -514,8 +514,11 @@ def main():
             "unit": "TFLOP/s" if mfma_bound else "GB/s",
             "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4) if mfma_bound else round(achieved / HBM_PEAK_GBS, 4),
             "traffic": measured_traffic(cfg.name),
-            "kernel": ("verify-forward GEMMs (register-blocked tiled_kernel)" if mfma_bound
-                       else "verify-forward GEMMs (streaming gemm_kernel)"),
+            "kernel": ("verify-forward GEMMs (32x32 wide_kernel; LM head on the register-blocked tiled_kernel)"
+                       if mfma_bound else "verify-forward GEMMs (streaming gemm_kernel)"),
+            # the whole verify forward (GEMMs, attention, norms, fix-ups) against the HBM peak:
+            # verify weight bytes over the verify's event-timed latency
+            "verify_forward_frac_of_hbm_peak": round(verify_wbytes / (med["verify_ms"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
             "weight_stream_GBps": round(achieved, 1),
             "frac_of_measured_copy": None if mfma_bound else round(achieved / copy_gbps, 4),
             "timed_steps": kt_steps,
