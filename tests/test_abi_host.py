@@ -111,3 +111,11 @@ def test_op_entry_points_validate():
     assert L.clover_op_topk(None, 1, 10, 3, None, None, None, None) == 1
     assert L.clover_op_topk_scratch_bytes(4, 125696, 16) > 0
     assert L.clover_op_topk_scratch_bytes(4, 125696, 17) == 0
+    # gated MLP: sizes a model may take, no null operands; rejected before any device call
+    one = ctypes.c_void_p(1)
+    assert L.clover_op_swiglu(1, one, 64, 4096, one, one, 11008 + 16, one, None) == 1  # F not a multiple of 32 (bf16)
+    assert L.clover_op_swiglu(1, one, 64, 4016, one, one, 11008, one, None) == 1       # K not a multiple of 32
+    assert L.clover_op_swiglu(0, one, 0, 256, one, one, 688, one, None) == 1           # no rows
+    assert L.clover_op_swiglu(1, one, 64, 4096, None, one, 11008, one, None) == 1      # null gate
+    assert L.clover_op_swiglu(2, one, 64, 4096, one, one, 11008, one, None) == 1       # unknown dtype
+    assert b"op_swiglu" in L.clover_last_error(None)
