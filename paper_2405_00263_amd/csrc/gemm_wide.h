@@ -78,9 +78,9 @@ __global__ __launch_bounds__(WIDE_THREADS) __attribute__((amdgpu_waves_per_eu(1,
   if (MODE == EP_QKV && threadIdx.x < BM) kvb = p.row_kb[min(m0 + (int)threadIdx.x, p.M - 1)];
 
   // Sources of this wave's LPW operands of chunk c0: a wave-uniform base (advanced per chunk)
-  // plus a per-lane byte offset.  Operand f < FA: X rows of block f / 2, k half f % 2; else
-  // W columns of block (f - FA) / 2, k half (f - FA) % 2.  Rows past M and columns past N read
-  // valid rows and tiles whose results are never stored.
+  // plus a per-lane byte offset.  Operand f < FA: X rows 16 f .. 16 f + 15, the whole chunk;
+  // else W columns of block (f - FA) / 2, k half (f - FA) % 2.  Rows past M and columns past N
+  // read valid rows and tiles whose results are never stored.
   const char* ubase[LPW];
   uint32_t loff[LPW];
   int ustep[LPW];
