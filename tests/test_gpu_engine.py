@@ -401,28 +401,28 @@ def test_bf16_batch_of_eight_verify_rows():
     note(f"batch 8: {compared} sequences compared")
 
 
-@pytest.mark.parametrize("T,topk", [(64, (8, 4, 2)), (128, (16, 4, 2))])
-def test_bf16_batch_of_sixteen_verify_rows(T, topk):
-    """Sixteen sequences verify 1024 or 2048 tree rows in one forward (the batch x tree cost
-    surface's largest cells: register-blocked GEMMs at those row counts with every epilogue,
-    attention over 16 paged sequences); each sequence's draft and verify logits stay within
-    the bf16 tolerance of its oracle over two teacher-forced steps."""
+@pytest.mark.parametrize("B,T,topk", [(16, 64, (8, 4, 2)), (16, 128, (16, 4, 2)), (48, 128, (16, 4, 2))])
+def test_bf16_large_batches_verify_rows(B, T, topk):
+    """Sixteen or forty-eight sequences verify 1024, 2048 or 6144 tree rows in one forward (the
+    batch x tree cost surface's largest cells: register-blocked GEMMs at those row counts with
+    every epilogue, attention over many paged sequences); each sequence's draft and verify
+    logits stay within the bf16 tolerance of its oracle over two teacher-forced steps."""
     P = need_gpu()
-    note(f"engine bf16 batch 16, T={T}")
-    cfg = _bf16_small().with_(batch=16, topk=topk, tree_tokens=T, max_context=512)
+    note(f"engine bf16 batch {B}, T={T}")
+    cfg = _bf16_small().with_(batch=B, topk=topk, tree_tokens=T, max_context=512)
     w = synth.make_weights(cfg, seed=12, perturb=True)
     eng = _engine(P, cfg, w)
     o = oracle.CloverOracle(cfg, w)
     states = []
-    for s in range(16):
-        prompt = synth.make_prompt(cfg, seq=s, n=20 + 17 * s)
+    for s in range(B):
+        prompt = synth.make_prompt(cfg, seq=s, n=20 + (17 * s) % 300)
         assert eng.prefill(s, prompt) == (st := o.prefill(prompt)).t0
         states.append(st)
     stats = dict(steps=0, draft_rows=0, verify_rows=0, draft_ties=0, target_ties=0)
     for _ in range(2):
         teacher_forced_step(eng, o, states, 2e-2, stats)
-    note(f"batch 16, T={T}: {stats}")
-    assert stats["steps"] == 32 and stats["verify_rows"] == 32 * T
+    note(f"batch {B}, T={T}: {stats}")
+    assert stats["steps"] == 2 * B and stats["verify_rows"] == 2 * B * T
     eng.close()
 
 

@@ -33,6 +33,9 @@ GEMM_CASES = [
     # 32x32 matrix-core kernel: the 7B output and down projections at 512 rows (4 K splits),
     # ragged rows
     ("bf16", 512, 4096, 11008, True), ("bf16", 520, 4096, 11008, True), ("bf16", 700, 4096, 4096, False),
+    # the cost surface's batch-48 cells: 3072 and 6144 verify rows (48 x 64- and 128-token trees)
+    ("bf16", 3072, 12288, 4096, True), ("bf16", 6144, 12288, 4096, True), ("bf16", 6144, 4096, 4096, True),
+    ("bf16", 6144, 4096, 11008, True), ("bf16", 6144, 22016, 4096, True), ("bf16", 6144, 125696, 4096, True),
 ]
 
 
@@ -44,16 +47,20 @@ def test_linear_matches_definition(dt, M, N, K, sampled):
     X = seeded((M, K), 1000 + M, 1.0, tdt)
     W = seeded((N, K), 2000 + N, 0.02, tdt)
     Wp = P.pack_matrix(W)
-    Y = to_np(P.op_linear(X, Wp, N))
+    Yd = P.op_linear(X, Wp, N)
     torch.cuda.synchronize()
-    cols = np.arange(N)
+    cols, rows = np.arange(N), np.arange(M)
     if sampled:
         rng = np.random.default_rng(0)
         cols = np.unique(np.concatenate([np.arange(64), np.arange(N - 64, N), rng.choice(N, 512, replace=False)]))
-    Xn, Wn = to_np(X), to_np(W[torch.as_tensor(cols, device=W.device)])
+        if M > 2048:  # first and last row tiles and a random sample between
+            rows = np.unique(np.concatenate([np.arange(64), np.arange(M - 64, M), rng.choice(M, 256, replace=False)]))
+    ri, ci = torch.as_tensor(rows, device=X.device), torch.as_tensor(cols, device=X.device)
+    Y = to_np(Yd[ri][:, ci])
+    Xn, Wn = to_np(X[ri]), to_np(W[ci])
     ref = Xn @ Wn.T
     bound = 1e-4 * (np.abs(Xn) @ np.abs(Wn).T) + 1e-7
-    err = np.abs(Y[:, cols] - ref)
+    err = np.abs(Y - ref)
     assert np.all(err <= bound), float(np.max(err / bound))
 
 
@@ -63,7 +70,7 @@ SWIGLU_CASES = [
     # feature group with 4 of its 6 tile pairs past F on the matrix-core kernel; f32
     ("bf16", 64, 11008, 4096, True), ("bf16", 300, 11008, 4096, True), ("bf16", 512, 11008, 4096, True),
     ("bf16", 1024, 11008, 4096, True), ("bf16", 520, 1408, 512, False), ("bf16", 777, 1408, 512, False),
-    ("f32", 41, 1376, 256, False),
+    ("f32", 41, 1376, 256, False), ("bf16", 6144, 11008, 4096, True),
 ]
 
 
@@ -78,20 +85,23 @@ def test_swiglu_matches_definition(dt, M, F, K, sampled):
     X = seeded((M, K), 3000 + M, 1.0, tdt)
     Wg = seeded((F, K), 4000 + F, 0.02, tdt)
     Wu = seeded((F, K), 5000 + F, 0.02, tdt)
-    act = to_np(P.op_swiglu(X, P.pack_matrix(Wg), P.pack_matrix(Wu), F).float())
+    actd = P.op_swiglu(X, P.pack_matrix(Wg), P.pack_matrix(Wu), F).float()
     torch.cuda.synchronize()
-    cols = np.arange(F)
+    cols, rows = np.arange(F), np.arange(M)
     if sampled:
         rng = np.random.default_rng(1)
         cols = np.unique(np.concatenate([np.arange(64), np.arange(F - 96, F), rng.choice(F, 384, replace=False)]))
-    idx = torch.as_tensor(cols, device=Wg.device)
-    Xn, Gn, Un = to_np(X).astype(np.float64), to_np(Wg[idx]).astype(np.float64), to_np(Wu[idx]).astype(np.float64)
+        if M > 2048:
+            rows = np.unique(np.concatenate([np.arange(256), np.arange(M - 256, M), rng.choice(M, 256, replace=False)]))
+    idx, ri = torch.as_tensor(cols, device=Wg.device), torch.as_tensor(rows, device=Wg.device)
+    act = to_np(actd[ri][:, idx])
+    Xn, Gn, Un = to_np(X[ri]).astype(np.float64), to_np(Wg[idx]).astype(np.float64), to_np(Wu[idx]).astype(np.float64)
     g, u = Xn @ Gn.T, Xn @ Un.T
     ref = oracle.silu(g) * u
     dg, du = 1e-4 * (np.abs(Xn) @ np.abs(Gn).T), 1e-4 * (np.abs(Xn) @ np.abs(Un).T)
     ulp = 2.0 ** -7 if dt == "bf16" else 2.0 ** -22
     bound = ulp * np.abs(ref) + 1.1 * np.abs(u) * dg + np.abs(oracle.silu(g)) * du + 1e-7
-    err = np.abs(act[:, cols] - ref)
+    err = np.abs(act - ref)
     assert np.all(err <= bound), float(np.max(err / bound))
 
 
